@@ -1,0 +1,183 @@
+#!/usr/bin/env python3
+"""Decode throughput of the IndexTTS-2-shaped GPT on one MI355X.
+
+One bench step is one whole generation job: prefill of the conditioning
+prefix, then `--decode` greedy decode steps for every sequence of the batch,
+each step's sampled ids fed straight back as the next step's tokens (device to
+device, no host round trip).  Inputs are seeded synthetic tensors resident in
+HBM before timing starts.  The JSON line reports generated tokens per second
+over the whole job, the HBM roofline of the decode step, and the CPU oracle's
+rate on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GPT decode tokens/s on 1 MI355X at batch 1 & 32; achieved HBM GB/s vs peak"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=3, help="timed generation jobs")
+    p.add_argument("--warmup", type=int, default=1)
+    p.add_argument("--mode", default="bf16", choices=["bf16", "w8a16", "w4a16", "f32"])
+    p.add_argument("--batch", type=int, default=1)
+    p.add_argument("--prefix", type=int, default=256)
+    p.add_argument("--decode", type=int, default=512)
+    p.add_argument("--cpu-steps", type=int, default=16, help="decode steps timed for the CPU oracle baseline")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args()
+
+
+def algorithmic_step_bytes(shape, dm, B, ctx_lens, kv_elem):
+    """Bytes one decode step must move: every parameter once, the KV rows it
+    attends over (the new one included), its KV writes, the embedding rows read
+    and the fp32 logits written."""
+    per_tok_kv = shape.n_layer * 2 * shape.d_model * kv_elem
+    kv_read = sum(c + 1 for c in ctx_lens) * per_tok_kv
+    kv_write = B * per_tok_kv
+    emb = B * 2 * shape.d_model * kv_elem
+    logits = B * shape.vocab * 4
+    embed_tables = (shape.vocab + shape.n_pos) * shape.d_model * kv_elem  # read sparsely, not streamed
+    return dm.weight_bytes() - embed_tables + kv_read + kv_write + emb + logits
+
+
+def cpu_baseline(inputs, shape, mode, prefix, n_steps):
+    import threadpoolctl
+    from oracle import gpt as ogpt
+    from oracle import quant as oquant
+
+    cores = len(os.sched_getaffinity(0))
+    with threadpoolctl.threadpool_limits(cores):
+        w = inputs if mode in ("f32", "bf16") else oquant.dequantized_model(
+            inputs, "w8" if mode == "w8a16" else "w4")
+        om = ogpt.GPT(w, shape.n_head, shape.d_head, dtype=np.float32)
+        cache, _ = om.prefill(prefix)
+        tok = shape.start_token
+        t0 = time.perf_counter()
+        for t in range(n_steps):
+            logits, _ = om.decode_step(cache, tok, t)
+            tok = int(np.argmax(logits))
+        dt = time.perf_counter() - t0
+        used = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
+    return {"value": round(n_steps / dt, 3), "unit": "tokens/s", "cores": int(min(used, cores)), "kind": "oracle",
+            "sample": f"{n_steps} greedy decode steps (batch 1) after an untimed {prefix.shape[0]}-row prefill, "
+                      f"numpy fp32 oracle on the same {mode} weights"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    from paper_2607_21042_amd import ftts, workload
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    shape = workload.INDEXTTS2
+    mode = args.mode
+    wdtype = {"f32": ftts.F32, "bf16": ftts.BF16, "w8a16": ftts.W8A16, "w4a16": ftts.W4A16}[mode]
+    B, P, T = args.batch, args.prefix, args.decode
+    master = workload.master_weights(shape, seed=0)
+    if mode == "f32":
+        inputs = master
+    elif mode == "bf16":
+        inputs = workload.bf16_weights(master)
+    else:
+        inputs = workload.quantisable_weights(master)
+    dm = ftts.DeviceModel(inputs, shape, wdtype)
+    adt = ftts.act_dtype(wdtype)
+    prefix_np = workload.prefix_embeddings([P] * B, shape.d_model, seed=1, bf16=(mode != "f32"))
+    prefix = torch.from_numpy(prefix_np).cuda().to(adt)
+
+    max_pages = math.ceil((P + T) / 64)
+    n_pages = B * max_pages
+    bt = torch.arange(n_pages, dtype=torch.int32, device="cuda").reshape(B, max_pages)
+    kv = ftts.KVCache(shape, wdtype, n_pages)
+    steps = torch.arange(T, dtype=torch.int32, device="cuda")
+    positions = steps[:, None].repeat(1, B).contiguous()              # [T][B]
+    seq_lens = (steps[:, None] + P).repeat(1, B).contiguous()         # [T][B]
+    toks = torch.full((T + 1, B), shape.start_token, dtype=torch.int32, device="cuda")
+    logits = torch.empty((B, shape.vocab), dtype=torch.float32, device="cuda")
+    last = torch.empty((B, shape.vocab), dtype=torch.float32, device="cuda")
+    ws = torch.empty(ftts.workspace_bytes(dm.cfg, B, B * P), dtype=torch.uint8, device="cuda")
+    greedy = ftts.Sampling(1.0, 1, 1.0)
+
+    class _PT:  # page-table view of one step (block table shared, seq_lens row t)
+        def __init__(self, t):
+            self.c = ftts.PageTable(bt.data_ptr(), seq_lens[t].data_ptr(), max_pages)
+    pts = [_PT(t) for t in range(T)]
+    pt_prefill = _PT(0)
+
+    stream = torch.cuda.current_stream()
+
+    def job(ev=None):
+        ftts.prefill(dm, prefix, [P] * B, pt_prefill, kv, last, ws)
+        if ev is not None:
+            ev[0].record(stream)
+        for t in range(T):
+            ftts.decode_step(dm, toks[t], positions[t], pts[t], kv, logits, toks[t + 1], None, greedy, ws)
+        if ev is not None:
+            ev[1].record(stream)
+
+    for _ in range(args.warmup):
+        job()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for k in range(args.steps):
+        job(evs[k])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+    decode_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
+    job_ms = total_ms / args.steps
+    tokens = B * T
+    value = tokens / (job_ms / 1e3)
+
+    kv_elem = 4 if mode == "f32" else 2
+    step_bytes = [algorithmic_step_bytes(shape, dm, B, [P + t] * B, kv_elem) for t in range(T)]
+    per_step_s = decode_ms / 1e3 / T
+    achieved = (sum(step_bytes) / T) / per_step_s / 1e9
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(job_ms, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": {"f32": "f32", "bf16": "bf16", "w8a16": "int8-w/bf16", "w4a16": "int4-w/bf16"}[mode],
+        "data": "synthetic: seeded random-init IndexTTS-2-shaped GPT (24x1280, 20 heads, FFN 5120, vocab 8194)",
+        "config": {"workload": f"indextts2-gpt {mode} batch={B} prefix={P} greedy decode={T}", "batch": B,
+                   "prefix": P, "decode_tokens": T, "weights": mode},
+        "decode_ms_per_token_step": round(decode_ms / T, 4),
+        "prefill_ms": round(job_ms - decode_ms, 3),
+        "wall_s": round(wall, 3),
+        "roofline": {"bound": "hbm", "kernel": "decode step (all kernels of one ftts_decode_step)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "algorithmic_bytes_per_step": int(sum(step_bytes) / T), "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(inputs, shape, mode, prefix_np[:P], args.cpu_steps)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

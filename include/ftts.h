@@ -1,0 +1,238 @@
+/*
+ * ftts.h -- C ABI of the MI355X (gfx950) GPT decode library.
+ *
+ * The library runs the autoregressive Text-to-Semantic GPT of IndexTTS-2, a
+ * decoder-only GPT-2 style network (Sec. II-A of "Faster IndexTTS-2"), one
+ * token per call for a batch of sequences, after a dense prefill of each
+ * sequence's conditioning prefix.  The prefix arrives as embeddings rather than
+ * token ids and the decoded tokens carry their own position ids, as in the
+ * paper's first and third adaptations of the serving engine (Sec. II-C).
+ * Linear weights may be bf16 or fp32, or weight-only quantised to W8A16 /
+ * W4A16 (Table I caption; Sec. III-B).
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ *  - Pointers are DEVICE pointers unless marked [host].  The caller allocates
+ *    and owns every buffer; the library borrows them for the duration of the
+ *    call, allocates no device memory and keeps no device state.
+ *  - All work is enqueued asynchronously on `stream` (a hipStream_t; NULL is
+ *    the default stream).  No call synchronises the host.
+ *  - Arguments are validated before anything is enqueued: a call that returns
+ *    an error has no side effects.  Errors are negative FTTS_E_* codes, with
+ *    a message in ftts_last_error() (thread-local).  A HIP launch failure is
+ *    reported as FTTS_E_HIP.  Nothing aborts, exits or throws.
+ *  - Device-side data that the host cannot check without synchronising
+ *    (token ids, positions, page-table entries, sequence lengths) is
+ *    bounds-checked by the kernels: a row whose token, position or page lies
+ *    out of range is treated as inactive (no KV write, zero attention output,
+ *    sampled id -1) so that no access leaves its buffer.
+ *  - Row-major everywhere.  A linear layer y = x W^T + b stores W as [N][K]
+ *    (output row n, input column k, k contiguous).
+ */
+#ifndef FTTS_H
+#define FTTS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- error codes ---------------------------------------------------------- */
+#define FTTS_OK 0
+#define FTTS_E_INVALID_ARG -1 /* null pointer, bad enum, bad count          */
+#define FTTS_E_SHAPE -2       /* inconsistent or unsupported dimensions      */
+#define FTTS_E_DTYPE -3       /* unknown or mismatched weight dtype          */
+#define FTTS_E_ALIGN -4       /* pointer not 16-byte aligned                 */
+#define FTTS_E_RANGE -5       /* a host-visible value out of range           */
+#define FTTS_E_HIP -6         /* a HIP runtime call or launch failed         */
+#define FTTS_E_UNSUPPORTED -7 /* valid but not implemented in this build     */
+#define FTTS_E_WORKSPACE -8   /* workspace missing or smaller than needed    */
+
+/* ---- weight storage modes (ftts_config.wdtype) ----------------------------- */
+/* FTTS_F32    every tensor fp32, KV cache fp32, activations fp32.
+ * FTTS_BF16   every tensor bf16, KV cache bf16.
+ * FTTS_W8A16  the four per-layer linears hold int8 codes [N][K] with one bf16
+ *             scale per output row [N]; weight = code * scale.  Every other
+ *             tensor (embeddings, LayerNorms, biases, LM head) is bf16.
+ * FTTS_W4A16  the four per-layer linears hold 4-bit codes packed eight to an
+ *             int32 [N][K/8] (column k in bits 4*(k%8) .. 4*(k%8)+3), with one
+ *             bf16 scale and one bf16 zero-point per output row and group of
+ *             group_size consecutive columns, both [N][K/group_size];
+ *             weight = (code - zero) * scale.  Other tensors bf16.
+ * In the three 16-bit modes the KV cache is bf16, the residual stream and all
+ * accumulation are fp32, and logits are fp32.                               */
+#define FTTS_F32 0
+#define FTTS_BF16 1
+#define FTTS_W8A16 2
+#define FTTS_W4A16 3
+
+typedef struct {
+    int32_t n_layer;    /* decoder blocks                                        */
+    int32_t d_model;    /* residual width; multiple of 128, <= 4096             */
+    int32_t n_head;     /* attention heads; n_head * d_head == d_model          */
+    int32_t d_head;     /* must be 64                                           */
+    int32_t d_ff;       /* MLP width; multiple of 128, <= 16384                 */
+    int32_t vocab;      /* semantic vocabulary rows of tok_emb and the LM head  */
+    int32_t n_pos;      /* rows of pos_emb                                      */
+    int32_t page_size;  /* KV tokens per page; must be 64                       */
+    int32_t wdtype;     /* FTTS_F32 / FTTS_BF16 / FTTS_W8A16 / FTTS_W4A16       */
+    int32_t group_size; /* W4A16 group along K; must be 128 (ignored otherwise) */
+    float ln_eps;       /* LayerNorm epsilon (biased variance)                   */
+} ftts_config;
+
+/* One linear layer.  `w` is [N][K] in the mode's storage; `scale` / `zero`
+ * are the quantisation parameters (NULL when unused); `bias` is [N] in the
+ * activation dtype (fp32 for FTTS_F32, bf16 otherwise). */
+typedef struct {
+    const void* w;
+    const void* scale;
+    const void* zero;
+    const void* bias;
+} ftts_linear;
+
+/* One pre-LayerNorm decoder block (Sec. II-A: GPT-2 family):
+ *   x += attn(LN1(x)) W_out^T + b_out ;  x += gelu(LN2(x) W_fc1^T + b_fc1) W_fc2^T + b_fc2
+ * qkv.w is [3*d_model][d_model], rows ordered [q | k | v], each block split into
+ * n_head heads of d_head consecutive rows; out.w [d][d]; fc1.w [d_ff][d];
+ * fc2.w [d][d_ff].  LayerNorm gains/biases are [d] in the activation dtype. */
+typedef struct {
+    const void* ln1_g;
+    const void* ln1_b;
+    ftts_linear qkv;
+    ftts_linear out;
+    const void* ln2_g;
+    const void* ln2_b;
+    ftts_linear fc1;
+    ftts_linear fc2;
+} ftts_layer;
+
+/* The whole model.  tok_emb [vocab][d] and pos_emb [n_pos][d] in the activation
+ * dtype; layers is a [host] array of n_layer blocks; lnf_g / lnf_b [d]; the LM
+ * head [vocab][d] (+ bias [vocab]) is never quantised: fp32 in FTTS_F32 mode,
+ * bf16 otherwise.  Every device pointer must be 16-byte aligned. */
+typedef struct {
+    ftts_config cfg;
+    const void* tok_emb;
+    const void* pos_emb;
+    const ftts_layer* layers;
+    const void* lnf_g;
+    const void* lnf_b;
+    ftts_linear head;
+} ftts_weights;
+
+/* Paged KV cache shared by all sequences.  Layout of `base`, in the KV dtype:
+ *   [n_layer][n_pages][2 (k, v)][n_head][page_size][d_head]
+ * A sequence's token t lives in physical page block_table[b][t / page_size] at
+ * slot t % page_size.  Splits of the attention follow logical pages, so results
+ * do not depend on which physical pages a sequence holds. */
+typedef struct {
+    void* base;
+    int32_t n_pages;
+} ftts_kv_pool;
+
+/* block_table [B][max_pages] int32 physical page ids; seq_lens [B] int32, the
+ * number of tokens already cached for each sequence. */
+typedef struct {
+    const int32_t* block_table;
+    const int32_t* seq_lens;
+    int32_t max_pages;
+} ftts_page_table;
+
+/* Next-token choice.  top_k == 1 is greedy: the largest raw logit, lowest index
+ * on ties (temperature and top_p ignored).  Otherwise, in fp32: z = logit / T;
+ * keep the top_k largest z (1 <= top_k <= FTTS_MAX_TOP_K; lower index first on
+ * ties); weights exp(z - z_max) summed in that order; keep the shortest prefix
+ * whose sum reaches top_p times the total; draw by inverse CDF with the
+ * caller's uniform u in [0, 1). */
+#define FTTS_MAX_TOP_K 64
+typedef struct {
+    float temperature; /* > 0 */
+    int32_t top_k;     /* 1 .. FTTS_MAX_TOP_K */
+    float top_p;       /* (0, 1] */
+} ftts_sampling;
+
+#define FTTS_MAX_BATCH 64
+
+/* Bytes of device workspace needed by ftts_prefill / ftts_decode_step for up
+ * to `max_batch` sequences and, in prefill, up to `max_rows` prefix rows in
+ * total.  Returns 0 for an invalid config. */
+size_t ftts_workspace_bytes(const ftts_config* cfg, int32_t max_batch, int32_t max_rows);
+
+/* Message for the last error returned on this thread ("" if none). */
+const char* ftts_last_error(void);
+
+/* Library version string. */
+const char* ftts_version(void);
+
+/*
+ * Weight-only quantisation of one fp32 matrix w [N][K] (Table I caption and
+ * Sec. III-B: only the GPT's weights are quantised; activations stay 16-bit).
+ * Deterministic and bit-exact:
+ *   FTTS_W8A16: per row n, s = bf16(max_k |w| / 127) (s = 1 if that is 0),
+ *               code = clamp(rint(w / s), -127, 127) as int8 into codes [N][K];
+ *               scales [N] receives the bf16 bits of s; zeros must be NULL.
+ *   FTTS_W4A16: per row n and group g of group_size columns,
+ *               mn = min(0, min w), mx = max(0, max w),
+ *               s = bf16((mx - mn) / 15) (s = 1 if that is 0),
+ *               z = clamp(rint(-mn / s), 0, 15),
+ *               code = clamp(rint(w / s) + z, 0, 15), packed eight per int32
+ *               into codes [N][K/8]; scales and zeros [N][K/group_size] receive
+ *               the bf16 bits of s and z.
+ * Divisions are IEEE fp32, rint rounds half to even.  w must be finite.
+ * K must be a multiple of 16 (W8A16) or of group_size (W4A16, group_size 128).
+ */
+int ftts_quantize_weights(int32_t wdtype, const float* w, int64_t N, int64_t K,
+                          int32_t group_size, void* codes, uint16_t* scales,
+                          uint16_t* zeros, void* stream);
+
+/*
+ * Dense prefill of B conditioning prefixes (Sec. II-C: conditioning rows enter
+ * as embeddings; they receive no position embedding).
+ *   prefix_emb  [sum(lens)][d_model] in the activation dtype, sequences packed
+ *               in order.
+ *   lens        [host] B prefix lengths, each >= 1.
+ *   pt, kv      the page table and pool: token t of sequence b is written to
+ *               page block_table[b][t / 64], slot t % 64, for every layer.
+ *               seq_lens is not read; the caller sets it to lens afterwards.
+ *   last_logits [B][vocab] fp32 logits of each sequence's last prefix row, or
+ *               NULL to skip the head.
+ *   ws          workspace of at least ftts_workspace_bytes(cfg, B, sum(lens)).
+ */
+int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* lens,
+                 int32_t B, const ftts_page_table* pt, const ftts_kv_pool* kv,
+                 float* last_logits, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * One decode step for B sequences (the per-token generation step of the
+ * autoregressive GPT, Sec. II-A / II-C).
+ *   tokens      [B] int32 token ids; a negative id marks an inactive slot.
+ *   positions   [B] int32 rows of pos_emb (the semantic tokens' own range).
+ *   pt          the new token's key/value go to slot seq_lens[b]; attention
+ *               covers slots 0 .. seq_lens[b] inclusive.  The caller
+ *               increments seq_lens afterwards.
+ *   logits_out  [B][vocab] fp32.
+ *   sampled_out [B] int32 chosen ids (-1 for inactive slots).
+ *   uniforms    [B] fp32 in [0, 1); may be NULL when samp->top_k == 1.
+ *   samp        [host] sampling parameters, shared by the batch.
+ *   ws          workspace of at least ftts_workspace_bytes(cfg, B, 0).
+ * Safe to capture in a HIP graph: no host synchronisation, no memset, and all
+ * per-step inputs are read through device pointers.
+ */
+int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
+                     const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out,
+                     int32_t* sampled_out, const float* uniforms, const ftts_sampling* samp,
+                     int32_t B, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * The sampler of ftts_decode_step on its own: logits [B][V] fp32, uniforms [B]
+ * (may be NULL when top_k == 1), sampled_out [B] int32.  No workspace.
+ */
+int ftts_sample(const float* logits, int32_t B, int32_t V, const ftts_sampling* samp,
+                const float* uniforms, int32_t* sampled_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FTTS_H */

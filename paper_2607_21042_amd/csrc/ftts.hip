@@ -1,0 +1,437 @@
+// C ABI entry points of libftts: argument validation, workspace carving and the
+// order of kernel launches for prefill and for one decode step.  Every check
+// happens before the first enqueue, so a rejected call has no side effects.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+
+#include "ftts_internal.hpp"
+
+using namespace ftts;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+    return fail(FTTS_E_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+size_t round256(size_t n) { return (n + 255) & ~size_t(255); }
+int act_bytes(const ftts_config& c) { return c.wdtype == FTTS_F32 ? 4 : 2; }
+
+int check_config(const ftts_config* c) {
+    if (!c) return fail(FTTS_E_INVALID_ARG, "config is NULL");
+    if (c->wdtype < FTTS_F32 || c->wdtype > FTTS_W4A16) return fail(FTTS_E_DTYPE, "unknown wdtype %d", c->wdtype);
+    if (c->n_layer < 1) return fail(FTTS_E_SHAPE, "n_layer must be >= 1");
+    if (c->d_head != kHeadDim) return fail(FTTS_E_UNSUPPORTED, "d_head must be 64 (got %d)", c->d_head);
+    if (c->page_size != kPage) return fail(FTTS_E_UNSUPPORTED, "page_size must be 64 (got %d)", c->page_size);
+    if (c->n_head < 1 || c->n_head * kHeadDim != c->d_model)
+        return fail(FTTS_E_SHAPE, "n_head * d_head must equal d_model");
+    if (c->d_model % 128 || c->d_model > 4096) return fail(FTTS_E_SHAPE, "d_model must be a multiple of 128, <= 4096");
+    if (c->d_ff < 128 || c->d_ff % 128 || c->d_ff > 16384)
+        return fail(FTTS_E_SHAPE, "d_ff must be a multiple of 128, <= 16384");
+    if (c->vocab < 2 || c->vocab > 16384) return fail(FTTS_E_SHAPE, "vocab must be in [2, 16384]");
+    if (c->n_pos < 1) return fail(FTTS_E_SHAPE, "n_pos must be >= 1");
+    if (c->wdtype == FTTS_W4A16 && c->group_size != 128)
+        return fail(FTTS_E_UNSUPPORTED, "W4A16 group_size must be 128 (got %d)", c->group_size);
+    if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return fail(FTTS_E_RANGE, "ln_eps must be finite and > 0");
+    return FTTS_OK;
+}
+
+int check_ptr(const void* p, const char* name) {
+    if (!p) return fail(FTTS_E_INVALID_ARG, "%s is NULL", name);
+    if (!aligned16(p)) return fail(FTTS_E_ALIGN, "%s is not 16-byte aligned", name);
+    return FTTS_OK;
+}
+
+#define TRY(expr)                       \
+    do {                                \
+        int rc_ = (expr);               \
+        if (rc_ != FTTS_OK) return rc_; \
+    } while (0)
+
+int check_linear(const ftts_linear& l, int wdtype, const char* name) {
+    char buf[64];
+    snprintf(buf, sizeof buf, "%s.w", name);
+    TRY(check_ptr(l.w, buf));
+    snprintf(buf, sizeof buf, "%s.bias", name);
+    TRY(check_ptr(l.bias, buf));
+    if (wdtype == FTTS_W8A16 || wdtype == FTTS_W4A16) {
+        snprintf(buf, sizeof buf, "%s.scale", name);
+        TRY(check_ptr(l.scale, buf));
+    }
+    if (wdtype == FTTS_W4A16) {
+        snprintf(buf, sizeof buf, "%s.zero", name);
+        TRY(check_ptr(l.zero, buf));
+    }
+    return FTTS_OK;
+}
+
+int check_weights(const ftts_weights* w) {
+    if (!w) return fail(FTTS_E_INVALID_ARG, "weights is NULL");
+    TRY(check_config(&w->cfg));
+    TRY(check_ptr(w->tok_emb, "tok_emb"));
+    TRY(check_ptr(w->pos_emb, "pos_emb"));
+    TRY(check_ptr(w->lnf_g, "lnf_g"));
+    TRY(check_ptr(w->lnf_b, "lnf_b"));
+    TRY(check_ptr(w->head.w, "head.w"));
+    TRY(check_ptr(w->head.bias, "head.bias"));
+    if (!w->layers) return fail(FTTS_E_INVALID_ARG, "layers is NULL");
+    for (int l = 0; l < w->cfg.n_layer; ++l) {
+        const ftts_layer& L = w->layers[l];
+        TRY(check_ptr(L.ln1_g, "ln1_g"));
+        TRY(check_ptr(L.ln1_b, "ln1_b"));
+        TRY(check_ptr(L.ln2_g, "ln2_g"));
+        TRY(check_ptr(L.ln2_b, "ln2_b"));
+        TRY(check_linear(L.qkv, w->cfg.wdtype, "qkv"));
+        TRY(check_linear(L.out, w->cfg.wdtype, "out"));
+        TRY(check_linear(L.fc1, w->cfg.wdtype, "fc1"));
+        TRY(check_linear(L.fc2, w->cfg.wdtype, "fc2"));
+    }
+    return FTTS_OK;
+}
+
+int check_kv(const ftts_page_table* pt, const ftts_kv_pool* kv, bool need_seq_lens) {
+    if (!pt) return fail(FTTS_E_INVALID_ARG, "page table is NULL");
+    if (!kv) return fail(FTTS_E_INVALID_ARG, "kv pool is NULL");
+    TRY(check_ptr(kv->base, "kv.base"));
+    if (!pt->block_table) return fail(FTTS_E_INVALID_ARG, "block_table is NULL");
+    if (need_seq_lens && !pt->seq_lens) return fail(FTTS_E_INVALID_ARG, "seq_lens is NULL");
+    if (pt->max_pages < 1) return fail(FTTS_E_SHAPE, "max_pages must be >= 1");
+    if (kv->n_pages < 1) return fail(FTTS_E_SHAPE, "n_pages must be >= 1");
+    return FTTS_OK;
+}
+
+int check_sampling(const ftts_sampling* s, int V, const float* uniforms) {
+    if (!s) return fail(FTTS_E_INVALID_ARG, "sampling is NULL");
+    if (s->top_k < 1 || s->top_k > FTTS_MAX_TOP_K || s->top_k > V)
+        return fail(FTTS_E_RANGE, "top_k must be in [1, min(%d, vocab)]", FTTS_MAX_TOP_K);
+    if (s->top_k > 1) {
+        if (!(s->temperature > 0.f) || !std::isfinite(s->temperature))
+            return fail(FTTS_E_RANGE, "temperature must be finite and > 0");
+        if (!(s->top_p > 0.f && s->top_p <= 1.f)) return fail(FTTS_E_RANGE, "top_p must be in (0, 1]");
+        if (!uniforms) return fail(FTTS_E_INVALID_ARG, "uniforms is NULL but top_k > 1");
+    }
+    return FTTS_OK;
+}
+
+// Workspace regions (all 256-byte aligned).  Decode and prefill never run at the
+// same time on one workspace, so their regions overlap.
+struct DecodeWs {
+    float *x, *qkv, *o, *h, *part;
+    int32_t* active;
+};
+struct PrefillWs {
+    float* x;        // [M][d] fp32 residual
+    void* a;         // [M][d] LayerNorm output, later the attention output
+    void* qkv;       // [M][3d]
+    void* h;         // [M][d_ff]
+    float* xlast;    // [B][d]
+    int32_t* active; // [B] all ones (head GEMV reads no flags; kept for symmetry)
+};
+
+size_t decode_bytes(const ftts_config& c, int B, DecodeWs* out, char* base) {
+    size_t off = 0;
+    auto take = [&](size_t n) { size_t o = off; off += round256(n); return base ? base + o : nullptr; };
+    char* x = take((size_t)B * c.d_model * 4);
+    char* qkv = take((size_t)B * 3 * c.d_model * 4);
+    char* o = take((size_t)B * c.d_model * 4);
+    char* h = take((size_t)B * c.d_ff * 4);
+    char* part = take((size_t)B * c.n_head * kMaxSplits * kPartStride * 4);
+    char* act = take((size_t)B * 4);
+    if (out) *out = DecodeWs{(float*)x, (float*)qkv, (float*)o, (float*)h, (float*)part, (int32_t*)act};
+    return off;
+}
+
+size_t prefill_bytes(const ftts_config& c, int B, int M, PrefillWs* out, char* base) {
+    const size_t e = act_bytes(c);
+    size_t off = 0;
+    auto take = [&](size_t n) { size_t o = off; off += round256(n); return base ? base + o : nullptr; };
+    char* x = take((size_t)M * c.d_model * 4);
+    char* a = take((size_t)M * c.d_model * e);
+    char* qkv = take((size_t)M * 3 * c.d_model * e);
+    char* h = take((size_t)M * c.d_ff * e);
+    char* xl = take((size_t)B * c.d_model * 4);
+    char* act = take((size_t)B * 4);
+    if (out) *out = PrefillWs{(float*)x, a, qkv, h, (float*)xl, (int32_t*)act};
+    return off;
+}
+
+GemvArgs gemv_args(const ftts_linear& L, int N, int K, int B, const float* act, float* out, int out_stride) {
+    GemvArgs a{};
+    a.w = L.w;
+    a.scale = reinterpret_cast<const uint16_t*>(L.scale);
+    a.zero = reinterpret_cast<const uint16_t*>(L.zero);
+    a.bias = L.bias;
+    a.N = N;
+    a.K = K;
+    a.B = B;
+    a.act = act;
+    a.out = out;
+    a.out_stride = out_stride;
+    return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ftts_last_error(void) { return g_err; }
+
+const char* ftts_version(void) { return "ftts 0.1.0 gfx950"; }
+
+size_t ftts_workspace_bytes(const ftts_config* cfg, int32_t max_batch, int32_t max_rows) {
+    if (check_config(cfg) != FTTS_OK) return 0;
+    if (max_batch < 1 || max_batch > FTTS_MAX_BATCH || max_rows < 0) {
+        fail(FTTS_E_RANGE, "max_batch must be in [1, %d] and max_rows >= 0", FTTS_MAX_BATCH);
+        return 0;
+    }
+    const size_t d = decode_bytes(*cfg, max_batch, nullptr, nullptr);
+    const size_t p = prefill_bytes(*cfg, max_batch, max_rows, nullptr, nullptr);
+    return d > p ? d : p;
+}
+
+int ftts_quantize_weights(int32_t wdtype, const float* w, int64_t N, int64_t K, int32_t group_size, void* codes,
+                          uint16_t* scales, uint16_t* zeros, void* stream) {
+    if (wdtype != FTTS_W8A16 && wdtype != FTTS_W4A16)
+        return fail(FTTS_E_DTYPE, "quantize: wdtype must be FTTS_W8A16 or FTTS_W4A16");
+    if (!w || !codes || !scales) return fail(FTTS_E_INVALID_ARG, "quantize: NULL pointer");
+    if (N < 1 || K < 1 || N > 65535LL * 32768LL) return fail(FTTS_E_SHAPE, "quantize: bad N or K");
+    if (wdtype == FTTS_W8A16) {
+        if (K % 16) return fail(FTTS_E_SHAPE, "quantize: K must be a multiple of 16 for W8A16");
+        if (N > 0x7FFFFFFF) return fail(FTTS_E_SHAPE, "quantize: N too large");
+    } else {
+        if (group_size != 128) return fail(FTTS_E_UNSUPPORTED, "quantize: group_size must be 128");
+        if (K % group_size) return fail(FTTS_E_SHAPE, "quantize: K must be a multiple of group_size");
+        if (!zeros) return fail(FTTS_E_INVALID_ARG, "quantize: zeros is NULL for W4A16");
+        if (N > 65535) return fail(FTTS_E_SHAPE, "quantize: N must be <= 65535 for W4A16");
+        if (reinterpret_cast<uintptr_t>(codes) & 3u) return fail(FTTS_E_ALIGN, "quantize: codes not 4-byte aligned");
+    }
+    if (reinterpret_cast<uintptr_t>(w) & 3u) return fail(FTTS_E_ALIGN, "quantize: w not 4-byte aligned");
+    (void)hipGetLastError();
+    hipError_t e = launch_quantize(wdtype, w, N, K, group_size, codes, scales, zeros, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "quantize launch");
+    return FTTS_OK;
+}
+
+int ftts_sample(const float* logits, int32_t B, int32_t V, const ftts_sampling* samp, const float* uniforms,
+                int32_t* sampled_out, void* stream) {
+    if (!logits || !sampled_out) return fail(FTTS_E_INVALID_ARG, "sample: NULL pointer");
+    if (B < 1 || B > 65535) return fail(FTTS_E_SHAPE, "sample: B must be in [1, 65535]");
+    if (V < 1 || V > 16384) return fail(FTTS_E_SHAPE, "sample: V must be in [1, 16384]");
+    TRY(check_sampling(samp, V, uniforms));
+    (void)hipGetLastError();
+    hipError_t e = launch_sample(logits, B, V, *samp, uniforms, nullptr, sampled_out, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "sample launch");
+    return FTTS_OK;
+}
+
+int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
+                     const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out, int32_t* sampled_out,
+                     const float* uniforms, const ftts_sampling* samp, int32_t B, void* ws, size_t ws_bytes,
+                     void* stream) {
+    TRY(check_weights(w));
+    const ftts_config& c = w->cfg;
+    if (B < 1 || B > FTTS_MAX_BATCH) return fail(FTTS_E_SHAPE, "B must be in [1, %d]", FTTS_MAX_BATCH);
+    if (!tokens || !positions) return fail(FTTS_E_INVALID_ARG, "tokens/positions is NULL");
+    if (!logits_out || !sampled_out) return fail(FTTS_E_INVALID_ARG, "logits_out/sampled_out is NULL");
+    TRY(check_kv(pt, kv, true));
+    TRY(check_sampling(samp, c.vocab, uniforms));
+    TRY(check_ptr(ws, "workspace"));
+    const size_t need = decode_bytes(c, B, nullptr, nullptr);
+    if (ws_bytes < need) return fail(FTTS_E_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
+
+    hipStream_t st = (hipStream_t)stream;
+    DecodeWs W;
+    decode_bytes(c, B, &W, reinterpret_cast<char*>(ws));
+    const int d = c.d_model, H = c.n_head, F = c.d_ff, V = c.vocab;
+
+    // Split the KV walk so that about 2048 waves share the attention.
+    const int want = (2048 + B * H - 1) / (B * H);
+    const int splits = want < 1 ? 1 : (want > kMaxSplits ? kMaxSplits : want);
+    const int pps = (pt->max_pages + splits - 1) / splits;
+    const int n_splits = (pt->max_pages + pps - 1) / pps;
+
+    (void)hipGetLastError();
+    hipError_t e = launch_embed(c.wdtype, w->tok_emb, w->pos_emb, V, c.n_pos, d, tokens, positions, pt->seq_lens,
+                                pt->block_table, pt->max_pages, kv->n_pages, B, W.x, W.active, st);
+    if (e != hipSuccess) return hip_fail(e, "embed");
+
+    KvAppend kva{};
+    kva.base = kv->base;
+    kva.n_pages = kv->n_pages;
+    kva.n_head = H;
+    kva.d_model = d;
+    kva.max_pages = pt->max_pages;
+    kva.block_table = pt->block_table;
+    kva.seq_lens = pt->seq_lens;
+    kva.active = W.active;
+
+    AttnDecodeArgs at{};
+    at.qkv = W.qkv;
+    at.qkv_stride = 3 * d;
+    at.kv_base = kv->base;
+    at.n_pages = kv->n_pages;
+    at.n_head = H;
+    at.max_pages = pt->max_pages;
+    at.pps = pps;
+    at.n_splits = n_splits;
+    at.block_table = pt->block_table;
+    at.seq_lens = pt->seq_lens;
+    at.active = W.active;
+    at.part = W.part;
+    at.o = W.o;
+    at.o_stride = d;
+
+    for (int l = 0; l < c.n_layer; ++l) {
+        const ftts_layer& L = w->layers[l];
+        GemvArgs g = gemv_args(L.qkv, 3 * d, d, B, W.x, W.qkv, 3 * d);
+        g.ln_g = L.ln1_g;
+        g.ln_b = L.ln1_b;
+        g.eps = c.ln_eps;
+        g.kv = kva;
+        g.kv.layer = l;
+        if ((e = launch_gemv(c.wdtype, EPI_QKV, true, g, st)) != hipSuccess) return hip_fail(e, "qkv");
+        at.layer = l;
+        if ((e = launch_attn_decode(c.wdtype, at, B, st)) != hipSuccess) return hip_fail(e, "attention");
+        g = gemv_args(L.out, d, d, B, W.o, W.x, d);
+        if ((e = launch_gemv(c.wdtype, EPI_RESID, false, g, st)) != hipSuccess) return hip_fail(e, "out-proj");
+        g = gemv_args(L.fc1, F, d, B, W.x, W.h, F);
+        g.ln_g = L.ln2_g;
+        g.ln_b = L.ln2_b;
+        g.eps = c.ln_eps;
+        if ((e = launch_gemv(c.wdtype, EPI_GELU, true, g, st)) != hipSuccess) return hip_fail(e, "fc1");
+        g = gemv_args(L.fc2, d, F, B, W.h, W.x, d);
+        if ((e = launch_gemv(c.wdtype, EPI_RESID, false, g, st)) != hipSuccess) return hip_fail(e, "fc2");
+    }
+    GemvArgs g = gemv_args(w->head, V, d, B, W.x, logits_out, V);
+    g.ln_g = w->lnf_g;
+    g.ln_b = w->lnf_b;
+    g.eps = c.ln_eps;
+    if ((e = launch_gemv(c.wdtype, EPI_STORE, true, g, st)) != hipSuccess) return hip_fail(e, "lm head");
+    if ((e = launch_sample(logits_out, B, V, *samp, uniforms, W.active, sampled_out, st)) != hipSuccess)
+        return hip_fail(e, "sampler");
+    return FTTS_OK;
+}
+
+int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* lens, int32_t B,
+                 const ftts_page_table* pt, const ftts_kv_pool* kv, float* last_logits, void* ws, size_t ws_bytes,
+                 void* stream) {
+    TRY(check_weights(w));
+    const ftts_config& c = w->cfg;
+    if (B < 1 || B > FTTS_MAX_BATCH) return fail(FTTS_E_SHAPE, "B must be in [1, %d]", FTTS_MAX_BATCH);
+    TRY(check_ptr(prefix_emb, "prefix_emb"));
+    if (!lens) return fail(FTTS_E_INVALID_ARG, "lens is NULL");
+    TRY(check_kv(pt, kv, false));
+    TRY(check_ptr(ws, "workspace"));
+    SeqTable seqs{};
+    AttnPrefillArgs ap{};
+    seqs.n = B;
+    seqs.cu[0] = 0;
+    ap.tiles_cu[0] = 0;
+    int64_t M = 0;
+    for (int b = 0; b < B; ++b) {
+        if (lens[b] < 1) return fail(FTTS_E_RANGE, "lens[%d] = %d must be >= 1", b, lens[b]);
+        if ((int64_t)lens[b] > (int64_t)pt->max_pages * kPage)
+            return fail(FTTS_E_RANGE, "lens[%d] = %d exceeds max_pages * 64", b, lens[b]);
+        M += lens[b];
+        if (M > (1 << 24)) return fail(FTTS_E_RANGE, "total prefix rows too large");
+        seqs.cu[b + 1] = (int)M;
+        ap.tiles_cu[b + 1] = ap.tiles_cu[b] + (lens[b] + 63) / 64;
+    }
+    const size_t need = prefill_bytes(c, B, (int)M, nullptr, nullptr);
+    if (ws_bytes < need) return fail(FTTS_E_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
+
+    hipStream_t st = (hipStream_t)stream;
+    PrefillWs P;
+    prefill_bytes(c, B, (int)M, &P, reinterpret_cast<char*>(ws));
+    const int d = c.d_model, F = c.d_ff, V = c.vocab, Mi = (int)M;
+
+    (void)hipGetLastError();
+    hipError_t e = launch_act_to_f32(c.wdtype, prefix_emb, Mi, d, P.x, st);
+    if (e != hipSuccess) return hip_fail(e, "prefix copy");
+
+    KvAppend kva{};
+    kva.base = kv->base;
+    kva.n_pages = kv->n_pages;
+    kva.n_head = c.n_head;
+    kva.d_model = d;
+    kva.max_pages = pt->max_pages;
+    kva.block_table = pt->block_table;
+
+    ap.qkv = P.qkv;
+    ap.o = P.a;
+    ap.d_model = d;
+    ap.n_head = c.n_head;
+    ap.seqs = seqs;
+
+    for (int l = 0; l < c.n_layer; ++l) {
+        const ftts_layer& L = w->layers[l];
+        if ((e = launch_ln_rows(c.wdtype, P.x, L.ln1_g, L.ln1_b, c.ln_eps, Mi, d, P.a, st)) != hipSuccess)
+            return hip_fail(e, "ln1");
+        GemmArgs g{};
+        g.a = P.a;
+        g.w = L.qkv.w;
+        g.scale = (const uint16_t*)L.qkv.scale;
+        g.zero = (const uint16_t*)L.qkv.zero;
+        g.bias = L.qkv.bias;
+        g.M = Mi;
+        g.N = 3 * d;
+        g.K = d;
+        g.out = P.qkv;
+        g.kv = kva;
+        g.kv.layer = l;
+        g.seqs = seqs;
+        if ((e = launch_gemm(c.wdtype, EPI_QKV, g, st)) != hipSuccess) return hip_fail(e, "qkv gemm");
+        if ((e = launch_attn_prefill(c.wdtype, ap, ap.tiles_cu[B], st)) != hipSuccess)
+            return hip_fail(e, "prefill attention");
+        g.w = L.out.w;
+        g.scale = (const uint16_t*)L.out.scale;
+        g.zero = (const uint16_t*)L.out.zero;
+        g.bias = L.out.bias;
+        g.N = d;
+        g.K = d;
+        g.out = P.x;
+        if ((e = launch_gemm(c.wdtype, EPI_RESID, g, st)) != hipSuccess) return hip_fail(e, "out gemm");
+        if ((e = launch_ln_rows(c.wdtype, P.x, L.ln2_g, L.ln2_b, c.ln_eps, Mi, d, P.a, st)) != hipSuccess)
+            return hip_fail(e, "ln2");
+        g.w = L.fc1.w;
+        g.scale = (const uint16_t*)L.fc1.scale;
+        g.zero = (const uint16_t*)L.fc1.zero;
+        g.bias = L.fc1.bias;
+        g.N = F;
+        g.K = d;
+        g.out = P.h;
+        if ((e = launch_gemm(c.wdtype, EPI_GELU, g, st)) != hipSuccess) return hip_fail(e, "fc1 gemm");
+        g.a = P.h;
+        g.w = L.fc2.w;
+        g.scale = (const uint16_t*)L.fc2.scale;
+        g.zero = (const uint16_t*)L.fc2.zero;
+        g.bias = L.fc2.bias;
+        g.N = d;
+        g.K = F;
+        g.out = P.x;
+        if ((e = launch_gemm(c.wdtype, EPI_RESID, g, st)) != hipSuccess) return hip_fail(e, "fc2 gemm");
+    }
+    if (last_logits) {
+        if ((e = launch_gather_rows(P.x, d, seqs, P.xlast, st)) != hipSuccess) return hip_fail(e, "gather");
+        GemvArgs g = gemv_args(w->head, V, d, B, P.xlast, last_logits, V);
+        g.ln_g = w->lnf_g;
+        g.ln_b = w->lnf_b;
+        g.eps = c.ln_eps;
+        if ((e = launch_gemv(c.wdtype, EPI_STORE, true, g, st)) != hipSuccess) return hip_fail(e, "lm head");
+    }
+    return FTTS_OK;
+}
+
+}  // extern "C"

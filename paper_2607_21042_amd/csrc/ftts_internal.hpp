@@ -1,0 +1,154 @@
+// Internal declarations shared by the HIP translation units of libftts.
+// Device helpers (bf16 conversion, wave reductions) and the launch-argument
+// structs of every kernel family.  Nothing here is part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ftts.h"
+
+namespace ftts {
+
+constexpr int kWave = 64;        // CDNA wavefront width
+constexpr int kPage = 64;        // KV tokens per page
+constexpr int kHeadDim = 64;     // attention head width
+constexpr int kMaxSplits = 32;   // split-K partitions per (sequence, head) in decode attention
+constexpr int kPartStride = 68;  // floats per split partial: o[64], m, l, pad
+
+// ---- bf16 <-> fp32 --------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Round to nearest bf16, ties to even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x7FFFFFu)) return (uint16_t)((u >> 16) | 0x40);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// Activation/parameter element: fp32 in FTTS_F32 mode, bf16 in the 16-bit modes.
+template <bool F32>
+__device__ __forceinline__ float ld_act(const void* p, size_t i) {
+    if constexpr (F32) return reinterpret_cast<const float*>(p)[i];
+    else return bf16_to_f32(reinterpret_cast<const uint16_t*>(p)[i]);
+}
+template <bool F32>
+__device__ __forceinline__ void st_act(void* p, size_t i, float v) {
+    if constexpr (F32) reinterpret_cast<float*>(p)[i] = v;
+    else reinterpret_cast<uint16_t*>(p)[i] = f32_to_bf16(v);
+}
+
+// ---- reductions -------------------------------------------------------------------
+template <int W>
+__device__ __forceinline__ float group_sum(float v) {
+#pragma unroll
+    for (int o = W / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+__device__ __forceinline__ float wave_sum(float v) { return group_sum<kWave>(v); }
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+// GPT-2 tanh GELU.
+__device__ __forceinline__ float gelu_tanh(float u) {
+    const float c = 0.7978845608028654f;  // sqrt(2/pi)
+    return 0.5f * u * (1.0f + tanhf(c * (u + 0.044715f * u * u * u)));
+}
+
+// Element offset of (layer, physical page, k|v, head, slot, dim) in the KV pool.
+__device__ __forceinline__ size_t kv_offset(int layer, int n_pages, int phys, int kv, int n_head, int head,
+                                            int slot) {
+    return ((((size_t)layer * n_pages + phys) * 2 + kv) * n_head + head) * (size_t)(kPage * kHeadDim) +
+           (size_t)slot * kHeadDim;
+}
+
+// ---- launch arguments -------------------------------------------------------------
+enum Epi { EPI_STORE = 0, EPI_QKV = 1, EPI_GELU = 2, EPI_RESID = 3 };
+
+struct KvAppend {            // where the QKV epilogue writes keys and values
+    void* base;
+    int n_pages, layer, n_head, d_model, max_pages;
+    const int32_t* block_table;
+    const int32_t* seq_lens;  // decode: slot = seq_lens[b]
+    const int32_t* active;    // decode: per-row flag
+};
+
+struct GemvArgs {
+    const void* w;           // [N][K] weights in the mode's storage
+    const uint16_t* scale;   // W8: [N]; W4: [N][K/128]
+    const uint16_t* zero;    // W4: [N][K/128]
+    const void* bias;        // [N] activation dtype
+    int N, K, B, lpr;        // lpr: lanes cooperating on one row
+    const float* act;        // [B][K] fp32 input (x when LayerNorm is fused)
+    const void* ln_g;        // LayerNorm gain / bias (activation dtype) or null
+    const void* ln_b;
+    float eps;
+    float* out;              // [B][out_stride] fp32
+    int out_stride;
+    KvAppend kv;
+};
+
+struct AttnDecodeArgs {
+    const float* qkv;        // [B][3d] fp32; q of head h at h*64
+    int qkv_stride;
+    const void* kv_base;
+    int n_pages, layer, n_head, max_pages, pps, n_splits;
+    const int32_t* block_table;
+    const int32_t* seq_lens;
+    const int32_t* active;
+    float* part;             // [B][H][n_splits][kPartStride]
+    float* o;                // [B][o_stride] fp32 merged output
+    int o_stride;
+};
+
+constexpr int kMaxPrefillSeqs = FTTS_MAX_BATCH;
+struct SeqTable {            // packed varlen sequences, passed by value
+    int n;
+    int cu[kMaxPrefillSeqs + 1];  // row offsets
+};
+
+struct GemmArgs {
+    const void* a;           // [M][K] activation dtype
+    const void* w;           // [N][K] weights
+    const uint16_t* scale;
+    const uint16_t* zero;
+    const void* bias;
+    int M, N, K;
+    void* out;               // STORE/QKV/GELU: [M][N] activation dtype; RESID: fp32 [M][N] in place
+    KvAppend kv;             // QKV epilogue (prefill form: slot = position within the sequence)
+    SeqTable seqs;
+};
+
+struct AttnPrefillArgs {
+    const void* qkv;         // [M][3d] activation dtype
+    void* o;                 // [M][d] activation dtype
+    int d_model, n_head;
+    SeqTable seqs;
+    int tiles_cu[kMaxPrefillSeqs + 1];  // prefix sums of 64-row query tiles per sequence
+};
+
+// ---- launchers (each returns a hipError_t from the launch) --------------------------
+hipError_t launch_embed(int wdtype, const void* tok_emb, const void* pos_emb, int vocab, int n_pos, int d,
+                        const int32_t* tokens, const int32_t* positions, const int32_t* seq_lens,
+                        const int32_t* block_table, int max_pages, int n_pages, int B, float* x,
+                        int32_t* active, hipStream_t st);
+hipError_t launch_gemv(int wdtype, int epi, bool ln, const GemvArgs& a, hipStream_t st);
+hipError_t launch_attn_decode(int wdtype, const AttnDecodeArgs& a, int B, hipStream_t st);
+hipError_t launch_sample(const float* logits, int B, int V, const ftts_sampling& s, const float* uniforms,
+                         const int32_t* active, int32_t* out, hipStream_t st);
+hipError_t launch_quantize(int wdtype, const float* w, int64_t N, int64_t K, int group, void* codes,
+                           uint16_t* scales, uint16_t* zeros, hipStream_t st);
+hipError_t launch_ln_rows(int wdtype, const float* x, const void* g, const void* b, float eps, int M, int d,
+                          void* out, hipStream_t st);
+hipError_t launch_gemm(int wdtype, int epi, const GemmArgs& a, hipStream_t st);
+hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_tiles, hipStream_t st);
+hipError_t launch_gather_rows(const float* x, int d, const SeqTable& seqs, float* out, hipStream_t st);
+hipError_t launch_act_to_f32(int wdtype, const void* src, int rows, int d, float* dst, hipStream_t st);
+
+}  // namespace ftts

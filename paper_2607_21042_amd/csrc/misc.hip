@@ -1,0 +1,316 @@
+// Small kernels around the hot path: token+position embedding (with the
+// per-row activity flag every later kernel reads), LayerNorm over packed rows
+// (prefill), row gathers, the next-token sampler and the weight quantiser.
+#include <climits>
+
+#include "ftts_internal.hpp"
+
+namespace ftts {
+
+// ---- embedding ------------------------------------------------------------------------
+// x[b] = tok_emb[tokens[b]] + pos_emb[positions[b]] (fp32).  A row is active when
+// its token, position, KV slot and page are all in range; inactive rows get x = 0.
+template <bool F32>
+__global__ __launch_bounds__(256) void embed_kernel(const void* tok_emb, const void* pos_emb, int vocab,
+                                                    int n_pos, int d, const int32_t* tokens,
+                                                    const int32_t* positions, const int32_t* seq_lens,
+                                                    const int32_t* block_table, int max_pages, int n_pages,
+                                                    float* x, int32_t* active) {
+    const int b = blockIdx.x;
+    const int t = tokens[b], p = positions[b], s = seq_lens[b];
+    bool ok = t >= 0 && t < vocab && p >= 0 && p < n_pos && s >= 0 && s < max_pages * kPage;
+    if (ok) {
+        const int phys = block_table[(size_t)b * max_pages + s / kPage];
+        ok = phys >= 0 && phys < n_pages;
+    }
+    if (threadIdx.x == 0) active[b] = ok ? 1 : 0;
+    float* xr = x + (size_t)b * d;
+    for (int k = threadIdx.x; k < d; k += blockDim.x)
+        xr[k] = ok ? ld_act<F32>(tok_emb, (size_t)t * d + k) + ld_act<F32>(pos_emb, (size_t)p * d + k) : 0.f;
+}
+
+hipError_t launch_embed(int wdtype, const void* tok_emb, const void* pos_emb, int vocab, int n_pos, int d,
+                        const int32_t* tokens, const int32_t* positions, const int32_t* seq_lens,
+                        const int32_t* block_table, int max_pages, int n_pages, int B, float* x,
+                        int32_t* active, hipStream_t st) {
+    if (wdtype == FTTS_F32)
+        hipLaunchKernelGGL(embed_kernel<true>, dim3(B), dim3(256), 0, st, tok_emb, pos_emb, vocab, n_pos, d,
+                           tokens, positions, seq_lens, block_table, max_pages, n_pages, x, active);
+    else
+        hipLaunchKernelGGL(embed_kernel<false>, dim3(B), dim3(256), 0, st, tok_emb, pos_emb, vocab, n_pos, d,
+                           tokens, positions, seq_lens, block_table, max_pages, n_pages, x, active);
+    return hipGetLastError();
+}
+
+// ---- block reductions -------------------------------------------------------------------
+__device__ __forceinline__ float block_sum256(float v, float* red) {
+    v = wave_sum(v);
+    const int w = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[w] = v;
+    __syncthreads();
+    return red[0] + red[1] + red[2] + red[3];
+}
+
+// ---- LayerNorm over packed rows (prefill): fp32 x -> activation dtype ----------------------
+template <bool F32>
+__global__ __launch_bounds__(256) void ln_rows_kernel(const float* x, const void* g, const void* bb, float eps,
+                                                      int d, void* out) {
+    __shared__ float red[4];
+    const size_t r = blockIdx.x;
+    const float* xr = x + r * d;
+    float s = 0.f;
+    for (int k = threadIdx.x; k < d; k += 256) s += xr[k];
+    const float mean = block_sum256(s, red) / (float)d;
+    float v = 0.f;
+    for (int k = threadIdx.x; k < d; k += 256) {
+        const float t = xr[k] - mean;
+        v = fmaf(t, t, v);
+    }
+    const float var = block_sum256(v, red) / (float)d;
+    const float rstd = 1.0f / sqrtf(var + eps);
+    for (int k = threadIdx.x; k < d; k += 256)
+        st_act<F32>(out, r * d + k, (xr[k] - mean) * rstd * ld_act<F32>(g, k) + ld_act<F32>(bb, k));
+}
+
+hipError_t launch_ln_rows(int wdtype, const float* x, const void* g, const void* b, float eps, int M, int d,
+                          void* out, hipStream_t st) {
+    if (wdtype == FTTS_F32) hipLaunchKernelGGL(ln_rows_kernel<true>, dim3(M), dim3(256), 0, st, x, g, b, eps, d, out);
+    else hipLaunchKernelGGL(ln_rows_kernel<false>, dim3(M), dim3(256), 0, st, x, g, b, eps, d, out);
+    return hipGetLastError();
+}
+
+// ---- row copies ----------------------------------------------------------------------------
+__global__ void gather_last_kernel(const float* x, int d, SeqTable seqs, float* out) {
+    const int b = blockIdx.x;
+    const float* src = x + (size_t)(seqs.cu[b + 1] - 1) * d;
+    for (int k = threadIdx.x; k < d; k += blockDim.x) out[(size_t)b * d + k] = src[k];
+}
+
+hipError_t launch_gather_rows(const float* x, int d, const SeqTable& seqs, float* out, hipStream_t st) {
+    hipLaunchKernelGGL(gather_last_kernel, dim3(seqs.n), dim3(256), 0, st, x, d, seqs, out);
+    return hipGetLastError();
+}
+
+template <bool F32>
+__global__ void act_to_f32_kernel(const void* src, size_t n, float* dst) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        dst[i] = ld_act<F32>(src, i);
+}
+
+hipError_t launch_act_to_f32(int wdtype, const void* src, int rows, int d, float* dst, hipStream_t st) {
+    const size_t n = (size_t)rows * d;
+    const int blocks = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+    if (wdtype == FTTS_F32) hipLaunchKernelGGL(act_to_f32_kernel<true>, dim3(blocks), dim3(256), 0, st, src, n, dst);
+    else hipLaunchKernelGGL(act_to_f32_kernel<false>, dim3(blocks), dim3(256), 0, st, src, n, dst);
+    return hipGetLastError();
+}
+
+// ---- sampler ------------------------------------------------------------------------------
+// Winner of two (value, index) candidates: larger value, lower index on ties; NaN never wins.
+__device__ __forceinline__ bool beats(float v, int i, float bv, int bi) {
+    return v > bv || (v == bv && i < bi);
+}
+
+__device__ __forceinline__ void wave_best(float& v, int& i) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(v, o, kWave);
+        const int oi = __shfl_xor(i, o, kWave);
+        if (beats(ov, oi, v, i)) {
+            v = ov;
+            i = oi;
+        }
+    }
+}
+
+// Block-wide best of every thread's candidate; all threads receive the winner.
+__device__ __forceinline__ void block_best(float& v, int& i, float* rv, int* ri) {
+    wave_best(v, i);
+    const int w = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        rv[w] = v;
+        ri[w] = i;
+    }
+    __syncthreads();
+    v = rv[0];
+    i = ri[0];
+    for (int j = 1; j < 4; ++j)
+        if (beats(rv[j], ri[j], v, i)) {
+            v = rv[j];
+            i = ri[j];
+        }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(256) void sample_kernel(const float* logits, int V, float temperature, int top_k,
+                                                     float top_p, const float* uniforms, const int32_t* active,
+                                                     int32_t* out) {
+    extern __shared__ float sz[];   // [V] tempered logits (top_k > 1)
+    __shared__ float rv[4];
+    __shared__ int ri[4];
+    __shared__ float selv[FTTS_MAX_TOP_K];
+    __shared__ int seli[FTTS_MAX_TOP_K];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    if (active && !active[b]) {
+        if (tid == 0) out[b] = -1;
+        return;
+    }
+    const float* row = logits + (size_t)b * V;
+    if (top_k == 1) {
+        float bv = -INFINITY;
+        int bi = INT_MAX;
+        for (int i = tid; i < V; i += 256) {
+            const float v = row[i];
+            if (beats(v, i, bv, bi)) {
+                bv = v;
+                bi = i;
+            }
+        }
+        block_best(bv, bi, rv, ri);
+        if (tid == 0) out[b] = bi < V ? bi : 0;
+        return;
+    }
+    for (int i = tid; i < V; i += 256) sz[i] = row[i] / temperature;
+    __syncthreads();
+    // Each thread keeps the best of its own (strided) indices; taken entries become NaN.
+    float cv = -INFINITY;
+    int ci = INT_MAX;
+    for (int i = tid; i < V; i += 256)
+        if (beats(sz[i], i, cv, ci)) {
+            cv = sz[i];
+            ci = i;
+        }
+    for (int r = 0; r < top_k; ++r) {
+        float wv = cv;
+        int wi = ci;
+        block_best(wv, wi, rv, ri);
+        if (tid == 0) {
+            selv[r] = wv;
+            seli[r] = wi;
+        }
+        if (wi == ci && ci < V) {  // this thread owned the winner: drop it and rescan
+            sz[wi] = __int_as_float(0x7FC00000);
+            cv = -INFINITY;
+            ci = INT_MAX;
+            for (int i = tid; i < V; i += 256)
+                if (beats(sz[i], i, cv, ci)) {
+                    cv = sz[i];
+                    ci = i;
+                }
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        // Sequential fp32 part: weights, running sums, nucleus cut, inverse-CDF draw.
+        const float z1 = selv[0];
+        float acc = 0.f;
+        for (int i = 0; i < top_k; ++i) {
+            acc = acc + expf(selv[i] - z1);
+            selv[i] = acc;  // cumulative sums replace the values
+        }
+        const float thresh = top_p * selv[top_k - 1];
+        int n = top_k;
+        for (int i = 0; i < top_k; ++i)
+            if (selv[i] >= thresh) {
+                n = i + 1;
+                break;
+            }
+        const float rr = uniforms[b] * selv[n - 1];
+        int j = n - 1;
+        for (int i = 0; i < n; ++i)
+            if (selv[i] > rr) {
+                j = i;
+                break;
+            }
+        out[b] = seli[j] < V ? seli[j] : 0;
+    }
+}
+
+hipError_t launch_sample(const float* logits, int B, int V, const ftts_sampling& s, const float* uniforms,
+                         const int32_t* active, int32_t* out, hipStream_t st) {
+    const size_t lds = s.top_k == 1 ? 0 : (size_t)V * sizeof(float);
+    hipLaunchKernelGGL(sample_kernel, dim3(B), dim3(256), lds, st, logits, V, s.temperature, s.top_k, s.top_p,
+                       uniforms, active, out);
+    return hipGetLastError();
+}
+
+// ---- weight quantiser ----------------------------------------------------------------------
+// W8A16: one block per row.  s = bf16(amax / 127) (1 if 0); code = clamp(rint(w / s), -127, 127).
+__global__ __launch_bounds__(256) void quant_w8_kernel(const float* w, int64_t K, int8_t* codes,
+                                                       uint16_t* scales) {
+    __shared__ float red[4];
+    const int64_t n = blockIdx.x;
+    const float* wr = w + n * K;
+    float m = 0.f;
+    for (int64_t k = threadIdx.x; k < K; k += 256) m = fmaxf(m, fabsf(wr[k]));
+    m = wave_max(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    const float amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    uint16_t sb = f32_to_bf16(amax / 127.0f);
+    if ((sb & 0x7FFF) == 0) sb = 0x3F80;  // zero scale -> 1
+    const float s = bf16_to_f32(sb);
+    if (threadIdx.x == 0) scales[n] = sb;
+    for (int64_t k = threadIdx.x; k < K; k += 256) {
+        const float q = fminf(fmaxf(rintf(wr[k] / s), -127.f), 127.f);
+        codes[n * K + k] = (int8_t)q;
+    }
+}
+
+// W4A16: one block of `group` threads per (row, group).  The range [min(0, mn), max(0, mx)]
+// sets s = bf16((mx - mn) / 15) (1 if 0) and z = clamp(rint(-mn / s), 0, 15);
+// code = clamp(rint(w / s) + z, 0, 15), packed eight to an int32, low nibble first.
+__global__ __launch_bounds__(128) void quant_w4_kernel(const float* w, int64_t K, int group, int32_t* codes,
+                                                       uint16_t* scales, uint16_t* zeros) {
+    __shared__ float rmin[2], rmax[2];
+    __shared__ uint8_t q8[128];
+    const int g = blockIdx.x;
+    const int64_t n = blockIdx.y;
+    const int t = threadIdx.x;
+    const float v = w[n * K + (int64_t)g * group + t];
+    float mn = v, mx = v;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        mn = fminf(mn, __shfl_xor(mn, o, kWave));
+        mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+    }
+    if ((t & 63) == 0) {
+        rmin[t >> 6] = mn;
+        rmax[t >> 6] = mx;
+    }
+    __syncthreads();
+    mn = fminf(fminf(rmin[0], rmin[1]), 0.f);
+    mx = fmaxf(fmaxf(rmax[0], rmax[1]), 0.f);
+    uint16_t sb = f32_to_bf16((mx - mn) / 15.0f);
+    if ((sb & 0x7FFF) == 0) sb = 0x3F80;
+    const float s = bf16_to_f32(sb);
+    const float z = fminf(fmaxf(rintf(-mn / s), 0.f), 15.f);
+    const float q = fminf(fmaxf(rintf(v / s) + z, 0.f), 15.f);
+    q8[t] = (uint8_t)q;
+    __syncthreads();
+    const int n_groups = (int)(K / group);
+    if (t == 0) {
+        scales[n * n_groups + g] = sb;
+        zeros[n * n_groups + g] = f32_to_bf16(z);
+    }
+    if (t < group / 8) {
+        uint32_t word = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) word |= (uint32_t)q8[t * 8 + j] << (4 * j);
+        codes[n * (K / 8) + (int64_t)g * (group / 8) + t] = (int32_t)word;
+    }
+}
+
+hipError_t launch_quantize(int wdtype, const float* w, int64_t N, int64_t K, int group, void* codes,
+                           uint16_t* scales, uint16_t* zeros, hipStream_t st) {
+    if (wdtype == FTTS_W8A16) {
+        hipLaunchKernelGGL(quant_w8_kernel, dim3((unsigned)N), dim3(256), 0, st, w, K, (int8_t*)codes, scales);
+    } else {
+        hipLaunchKernelGGL(quant_w4_kernel, dim3((unsigned)(K / group), (unsigned)N), dim3(group), 0, st, w, K,
+                           group, (int32_t*)codes, scales, zeros);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace ftts

@@ -1,0 +1,299 @@
+"""Python binding of libftts (the C ABI in include/ftts.h).
+
+Argument marshalling only: every step of the decode path runs in the HIP
+kernels of libftts.so.  torch tensors provide device memory and the stream;
+their data pointers are handed to the C entry points, which carry the same
+names here.  If the library is missing the binding raises instead of falling
+back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libftts.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "ftts.h")
+
+F32, BF16, W8A16, W4A16 = 0, 1, 2, 3
+WDTYPE_NAMES = {F32: "f32", BF16: "bf16", W8A16: "w8a16", W4A16: "w4a16"}
+MAX_TOP_K = 64
+MAX_BATCH = 64
+PAGE = 64
+
+_c = ctypes
+i32, f32, vp = _c.c_int32, _c.c_float, _c.c_void_p
+
+
+class FTTSError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"ftts error {code}: {msg}")
+        self.code = code
+
+
+class Config(_c.Structure):
+    _fields_ = [("n_layer", i32), ("d_model", i32), ("n_head", i32), ("d_head", i32), ("d_ff", i32),
+                ("vocab", i32), ("n_pos", i32), ("page_size", i32), ("wdtype", i32), ("group_size", i32),
+                ("ln_eps", f32)]
+
+
+class Linear(_c.Structure):
+    _fields_ = [("w", vp), ("scale", vp), ("zero", vp), ("bias", vp)]
+
+
+class Layer(_c.Structure):
+    _fields_ = [("ln1_g", vp), ("ln1_b", vp), ("qkv", Linear), ("out", Linear), ("ln2_g", vp), ("ln2_b", vp),
+                ("fc1", Linear), ("fc2", Linear)]
+
+
+class Weights(_c.Structure):
+    _fields_ = [("cfg", Config), ("tok_emb", vp), ("pos_emb", vp), ("layers", _c.POINTER(Layer)),
+                ("lnf_g", vp), ("lnf_b", vp), ("head", Linear)]
+
+
+class KvPool(_c.Structure):
+    _fields_ = [("base", vp), ("n_pages", i32)]
+
+
+class PageTable(_c.Structure):
+    _fields_ = [("block_table", vp), ("seq_lens", vp), ("max_pages", i32)]
+
+
+class Sampling(_c.Structure):
+    _fields_ = [("temperature", f32), ("top_k", i32), ("top_p", f32)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libftts.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise FTTSError(-7, f"{LIB_PATH} is missing; build it with `python -m paper_2607_21042_amd.build`")
+        L = _c.CDLL(LIB_PATH)
+        P = _c.POINTER
+        L.ftts_last_error.restype = _c.c_char_p
+        L.ftts_version.restype = _c.c_char_p
+        L.ftts_workspace_bytes.restype = _c.c_size_t
+        L.ftts_workspace_bytes.argtypes = [P(Config), i32, i32]
+        L.ftts_quantize_weights.restype = _c.c_int
+        L.ftts_quantize_weights.argtypes = [i32, vp, _c.c_int64, _c.c_int64, i32, vp, vp, vp, vp]
+        L.ftts_prefill.restype = _c.c_int
+        L.ftts_prefill.argtypes = [P(Weights), vp, P(i32), i32, P(PageTable), P(KvPool), vp, vp, _c.c_size_t, vp]
+        L.ftts_decode_step.restype = _c.c_int
+        L.ftts_decode_step.argtypes = [P(Weights), vp, vp, P(PageTable), P(KvPool), vp, vp, vp, P(Sampling), i32,
+                                       vp, _c.c_size_t, vp]
+        L.ftts_sample.restype = _c.c_int
+        L.ftts_sample.argtypes = [vp, i32, i32, P(Sampling), vp, vp, vp]
+        _lib = L
+    return _lib
+
+
+def header_functions():
+    """Names of the functions declared in include/ftts.h."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(ftts_\w+)\s*\(", text, flags=re.M)))
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise FTTSError(rc, lib().ftts_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise FTTSError(-1, "tensor must live on the GPU")
+    if not t.is_contiguous():
+        raise FTTSError(-1, "tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def version() -> str:
+    return lib().ftts_version().decode()
+
+
+def workspace_bytes(cfg: Config, max_batch: int, max_rows: int = 0) -> int:
+    n = lib().ftts_workspace_bytes(_c.byref(cfg), max_batch, max_rows)
+    if n == 0:
+        raise FTTSError(-1, lib().ftts_last_error().decode())
+    return n
+
+
+def quantize_weights(wdtype: int, w, codes, scales, zeros=None, group_size: int = 128, stream=None):
+    """ftts_quantize_weights on fp32 w [N][K] (device tensors)."""
+    N, K = w.shape
+    if w.dtype != torch.float32:
+        raise FTTSError(-3, "w must be fp32")
+    _check(lib().ftts_quantize_weights(wdtype, _ptr(w), N, K, group_size, _ptr(codes), _ptr(scales), _ptr(zeros),
+                                       _stream(stream)))
+
+
+def sample(logits, sampling: Sampling, uniforms, sampled_out, stream=None):
+    """ftts_sample: logits [B][V] fp32 -> sampled_out [B] int32."""
+    B, V = logits.shape
+    _check(lib().ftts_sample(_ptr(logits), B, V, _c.byref(sampling), _ptr(uniforms), _ptr(sampled_out),
+                             _stream(stream)))
+
+
+def prefill(model, prefix_emb, lens, page_table, kv, last_logits, ws, stream=None):
+    """ftts_prefill; `lens` is a host sequence of prefix lengths."""
+    B = len(lens)
+    lens_arr = (i32 * B)(*[int(x) for x in lens])
+    _check(lib().ftts_prefill(_c.byref(model.c), _ptr(prefix_emb), lens_arr, B, _c.byref(page_table.c),
+                              _c.byref(kv.c), _ptr(last_logits), _ptr(ws), ws.numel() * ws.element_size(),
+                              _stream(stream)))
+
+
+def decode_step(model, tokens, positions, page_table, kv, logits_out, sampled_out, uniforms, sampling: Sampling,
+                ws, stream=None):
+    """ftts_decode_step for B = tokens.numel() sequences."""
+    B = tokens.numel()
+    _check(lib().ftts_decode_step(_c.byref(model.c), _ptr(tokens), _ptr(positions), _c.byref(page_table.c),
+                                  _c.byref(kv.c), _ptr(logits_out), _ptr(sampled_out), _ptr(uniforms),
+                                  _c.byref(sampling), B, _ptr(ws), ws.numel() * ws.element_size(),
+                                  _stream(stream)))
+
+
+# --------------------------------------------------------------------------- device state
+def make_config(shape, wdtype: int, eps: float = 1e-5) -> Config:
+    return Config(shape.n_layer, shape.d_model, shape.n_head, shape.d_head, shape.d_ff, shape.vocab, shape.n_pos,
+                  PAGE, wdtype, 128, eps)
+
+
+def act_dtype(wdtype: int):
+    return torch.float32 if wdtype == F32 else torch.bfloat16
+
+
+class DeviceModel:
+    """Model weights resident in HBM plus the ftts_weights struct pointing at them.
+
+    `weights` is the numpy dict of the seeded input generator (fp32 arrays; in
+    the 16-bit modes their values must be bf16-representable).  For W8A16 and
+    W4A16 the four per-layer matrices are quantised on the GPU by
+    ftts_quantize_weights from the fp32 values given here.
+    """
+
+    def __init__(self, weights: dict, shape, wdtype: int, device="cuda", stream=None):
+        self.shape, self.wdtype = shape, wdtype
+        self.cfg = make_config(shape, wdtype)
+        adt = act_dtype(wdtype)
+        self._keep = []
+
+        def up(a, dtype=adt):
+            t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+            if dtype != torch.float32:
+                t = t.to(dtype)
+            self._keep.append(t)
+            return t
+
+        def linear(w, b, quantise: bool):
+            L = Linear()
+            L.bias = up(b).data_ptr()
+            if not quantise or wdtype in (F32, BF16):
+                L.w = up(w).data_ptr()
+                return L
+            N, K = w.shape
+            w32 = torch.from_numpy(np.ascontiguousarray(w, dtype=np.float32)).to(device)
+            if wdtype == W8A16:
+                codes = torch.empty((N, K), dtype=torch.int8, device=device)
+                scales = torch.empty((N,), dtype=torch.int16, device=device)
+                quantize_weights(W8A16, w32, codes, scales, None, stream=stream)
+                zeros = None
+            else:
+                codes = torch.empty((N, K // 8), dtype=torch.int32, device=device)
+                scales = torch.empty((N, K // 128), dtype=torch.int16, device=device)
+                zeros = torch.empty((N, K // 128), dtype=torch.int16, device=device)
+                quantize_weights(W4A16, w32, codes, scales, zeros, stream=stream)
+            self._keep += [codes, scales] + ([zeros] if zeros is not None else [])
+            torch.cuda.current_stream().synchronize()
+            del w32
+            L.w, L.scale = codes.data_ptr(), scales.data_ptr()
+            L.zero = zeros.data_ptr() if zeros is not None else None
+            L._tensors = (codes, scales, zeros)
+            return L
+
+        n = shape.n_layer
+        self.layers = (Layer * n)()
+        self.quantised = []
+        for l, lw in enumerate(weights["layers"]):
+            Ly = self.layers[l]
+            Ly.ln1_g, Ly.ln1_b = up(lw["ln1_g"]).data_ptr(), up(lw["ln1_b"]).data_ptr()
+            Ly.ln2_g, Ly.ln2_b = up(lw["ln2_g"]).data_ptr(), up(lw["ln2_b"]).data_ptr()
+            lins = {}
+            for name in ("qkv", "out", "fc1", "fc2"):
+                L = linear(lw["w_" + name], lw["b_" + name], True)
+                setattr(Ly, name, L)
+                lins[name] = getattr(L, "_tensors", None)
+            self.quantised.append(lins)
+        c = Weights()
+        c.cfg = self.cfg
+        c.tok_emb = up(weights["tok_emb"]).data_ptr()
+        c.pos_emb = up(weights["pos_emb"]).data_ptr()
+        c.layers = self.layers
+        c.lnf_g, c.lnf_b = up(weights["lnf_g"]).data_ptr(), up(weights["lnf_b"]).data_ptr()
+        c.head = linear(weights["w_head"], weights["b_head"], False)
+        self.c = c
+
+    def weight_bytes(self) -> int:
+        """Bytes of every parameter tensor held on the device."""
+        seen, total = set(), 0
+        for t in self._keep:
+            if t.data_ptr() not in seen:
+                seen.add(t.data_ptr())
+                total += t.numel() * t.element_size()
+        return total
+
+
+class PagePool:
+    """Host-side page allocator over a fixed number of KV pages (a free list)."""
+
+    def __init__(self, n_pages: int):
+        self.free = list(range(n_pages - 1, -1, -1))
+
+    def alloc(self, n: int):
+        if n > len(self.free):
+            raise FTTSError(-5, "KV pool exhausted")
+        return [self.free.pop() for _ in range(n)]
+
+    def release(self, pages):
+        self.free.extend(reversed(list(pages)))
+
+
+class KVCache:
+    """The paged KV pool [n_layer][n_pages][2][n_head][64][64] and its C view."""
+
+    def __init__(self, shape, wdtype: int, n_pages: int, device="cuda", fill=None):
+        dt = act_dtype(wdtype)
+        dims = (shape.n_layer, n_pages, 2, shape.n_head, PAGE, shape.d_head)
+        self.pool = (torch.full(dims, fill, dtype=dt, device=device) if fill is not None
+                     else torch.zeros(dims, dtype=dt, device=device))
+        self.n_pages = n_pages
+        self.c = KvPool(self.pool.data_ptr(), n_pages)
+
+
+class PageTableView:
+    """Device block table [B][max_pages] and seq_lens [B] with their C view."""
+
+    def __init__(self, block_table, seq_lens):
+        self.block_table = block_table.to(torch.int32).contiguous()
+        self.seq_lens = seq_lens.to(torch.int32).contiguous()
+        self.c = PageTable(self.block_table.data_ptr(), self.seq_lens.data_ptr(), self.block_table.shape[1])

@@ -194,3 +194,18 @@ def random_logits(batch: int, vocab: int, seed: int = 5, scale: float = 3.0) -> 
     """fp32 logits for exercising a sampler on its own, shape [batch, vocab]."""
     rng = np.random.default_rng(seed)
     return (rng.standard_normal((batch, vocab), dtype=np.float32) * np.float32(scale))
+
+
+LINEAR_KEYS = ("w_qkv", "w_out", "w_fc1", "w_fc2")
+
+
+def quantisable_weights(master: dict, threads: int = 8) -> dict:
+    """Inputs of a weight-only-quantised model: the four per-layer matrices keep
+    their fp32 master values (each side quantises them itself); every other
+    tensor is rounded to bf16."""
+    out = bf16_weights({k: v for k, v in master.items()} | {"layers": [
+        {k: v for k, v in lw.items() if k not in LINEAR_KEYS} for lw in master["layers"]]}, threads)
+    for lw_out, lw in zip(out["layers"], master["layers"]):
+        for k in LINEAR_KEYS:
+            lw_out[k] = lw[k]
+    return out

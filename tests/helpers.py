@@ -1,0 +1,120 @@
+"""Shared test machinery: running the GPU path through the binding and the
+oracle on the same seeded inputs, and the comparison rules.
+
+Tolerances: fp32 logits agree to a normwise relative error of 1e-4
+(max |gpu - oracle| / max |oracle| per step); bf16-storage modes agree to an
+absolute 3e-2 against the fp32 oracle run on the same (dequantised) weights.
+Greedy choices must agree wherever the oracle's top-1 / top-2 gap exceeds twice
+the tolerance; closer cases are near-ties and are only counted.
+"""
+import math
+
+import numpy as np
+
+from oracle import gpt as ogpt
+from oracle import quant as oquant
+from paper_2607_21042_amd import workload
+
+FP32_REL_TOL = 1e-4
+BF16_ABS_TOL = 3e-2
+
+
+def oracle_weights(inputs: dict, wdtype_name: str) -> dict:
+    """The weights the oracle runs on: as given, or with the four matrices
+    replaced by the oracle's own quantise-then-dequantise values."""
+    if wdtype_name in ("f32", "bf16"):
+        return inputs
+    return oquant.dequantized_model(inputs, "w8" if wdtype_name == "w8a16" else "w4")
+
+
+def oracle_teacher_forced(model: ogpt.GPT, prefix: np.ndarray, fed: np.ndarray):
+    """Logits of the last prefix row and of every decoded row, by one full causal forward."""
+    logits, _ = model.full_forward(model.rows(prefix, fed))
+    P = prefix.shape[0]
+    return logits[P - 1], logits[P:P + len(fed)]
+
+
+def tolerance_ok(gpu, ref, wdtype_name):
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    err = np.max(np.abs(gpu - ref))
+    if wdtype_name == "f32":
+        return err / max(np.max(np.abs(ref)), 1e-30) <= FP32_REL_TOL, err
+    return err <= BF16_ABS_TOL, err
+
+
+def argmax_agrees(gpu_tok, ref_logits, wdtype_name):
+    """True if the GPU's greedy token matches, or the oracle's top two are a near-tie."""
+    ref = np.asarray(ref_logits, np.float64)
+    top = np.argsort(-ref, kind="stable")[:2]
+    if int(gpu_tok) == int(top[0]):
+        return True, False
+    tol = BF16_ABS_TOL if wdtype_name != "f32" else FP32_REL_TOL * np.max(np.abs(ref))
+    near = (ref[top[0]] - ref[top[1]]) <= 2 * tol and int(gpu_tok) == int(top[1])
+    return near, near
+
+
+def pages_needed(n_tokens: int) -> int:
+    return math.ceil(n_tokens / 64)
+
+
+def make_block_table(lens_total, seed=None, spare=0):
+    """Physical page ids per sequence (optionally a seeded random permutation)."""
+    need = [pages_needed(n) for n in lens_total]
+    max_pages = max(need)
+    n_pages = sum(need) + spare
+    ids = np.arange(n_pages)
+    if seed is not None:
+        ids = np.random.default_rng(seed).permutation(n_pages)
+    bt = np.full((len(lens_total), max_pages), -1, dtype=np.int32)
+    k = 0
+    for b, n in enumerate(need):
+        bt[b, :n] = ids[k:k + n]
+        k += n
+    return bt, n_pages
+
+
+def run_gpu(dev_model, shape, prefixes, fed, sampling=None, uniforms=None, block_table=None, n_pages=None,
+            pool_fill=None, graph=False):
+    """Prefill every prefix, then feed fed[t] (int32 [T][B]) at step t.
+
+    Returns dict(prefill [B][V], logits [T][B][V], sampled [T][B], kv, page table).
+    """
+    import torch
+    from paper_2607_21042_amd import ftts
+
+    B = len(prefixes)
+    T = fed.shape[0]
+    lens = [p.shape[0] for p in prefixes]
+    if block_table is None:
+        block_table, n_pages = make_block_table([n + T for n in lens])
+    kv = ftts.KVCache(shape, dev_model.wdtype, n_pages, fill=pool_fill)
+    bt = torch.from_numpy(block_table).cuda()
+    seq_lens = torch.zeros(B, dtype=torch.int32, device="cuda")
+    pt = ftts.PageTableView(bt, seq_lens)
+    adt = ftts.act_dtype(dev_model.wdtype)
+    prefix = torch.from_numpy(np.concatenate(prefixes).astype(np.float32)).cuda().to(adt)
+    ws = torch.empty(ftts.workspace_bytes(dev_model.cfg, B, sum(lens)), dtype=torch.uint8, device="cuda")
+    V = shape.vocab
+    last = torch.empty((B, V), dtype=torch.float32, device="cuda")
+    ftts.prefill(dev_model, prefix, lens, pt, kv, last, ws)
+    pt.seq_lens.copy_(torch.tensor(lens, dtype=torch.int32))
+    if sampling is None:
+        sampling = ftts.Sampling(1.0, 1, 1.0)
+    tok = torch.empty(B, dtype=torch.int32, device="cuda")
+    pos = torch.empty(B, dtype=torch.int32, device="cuda")
+    u = torch.zeros(B, dtype=torch.float32, device="cuda")
+    logits = torch.empty((T, B, V), dtype=torch.float32, device="cuda")
+    sampled = torch.empty((T, B), dtype=torch.int32, device="cuda")
+    fed_d = torch.from_numpy(np.ascontiguousarray(fed, dtype=np.int32)).cuda()
+    un_d = torch.from_numpy(np.ascontiguousarray(uniforms, dtype=np.float32)).cuda() if uniforms is not None else None
+    for t in range(T):
+        tok.copy_(fed_d[t])
+        pos.fill_(t)
+        if un_d is not None:
+            u.copy_(un_d[t])
+        ftts.decode_step(dev_model, tok, pos, pt, kv, logits[t], sampled[t], u, sampling, ws)
+        pt.seq_lens.add_((fed_d[t] >= 0).to(torch.int32))
+    torch.cuda.synchronize()
+    return {"prefill": last.cpu().numpy(), "logits": logits.cpu().numpy(), "sampled": sampled.cpu().numpy(),
+            "kv": kv, "pt": pt, "lens": lens}

@@ -1,0 +1,147 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/ftts.h declares, sizes workspaces, and rejects bad
+arguments before anything is enqueued (every call below fails validation, so
+no kernel is launched and no pointer is dereferenced)."""
+import ctypes
+
+import pytest
+
+from paper_2607_21042_amd import ftts, workload
+
+FAKE = 0x100000  # aligned, never dereferenced: every call here fails validation first
+
+
+def test_library_exports_every_header_function():
+    names = ftts.header_functions()
+    assert set(names) >= {"ftts_prefill", "ftts_decode_step", "ftts_quantize_weights", "ftts_sample",
+                          "ftts_workspace_bytes", "ftts_last_error", "ftts_version"}
+    L = ftts.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert "gfx950" in ftts.version()
+
+
+def test_workspace_bytes_grows_with_batch_and_rows():
+    cfg = ftts.make_config(workload.INDEXTTS2, ftts.BF16)
+    a = ftts.workspace_bytes(cfg, 1, 0)
+    b = ftts.workspace_bytes(cfg, 32, 0)
+    c = ftts.workspace_bytes(cfg, 1, 512)
+    assert 0 < a < b and a < c
+    assert a % 256 == 0
+    with pytest.raises(ftts.FTTSError):
+        ftts.workspace_bytes(cfg, 0, 0)
+    with pytest.raises(ftts.FTTSError):
+        ftts.workspace_bytes(cfg, ftts.MAX_BATCH + 1, 0)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("d_head", 32, -7), ("page_size", 16, -7), ("n_head", 3, -2), ("d_model", 200, -2),
+    ("d_ff", 100, -2), ("wdtype", 9, -3), ("vocab", 1, -2), ("n_layer", 0, -2), ("ln_eps", 0.0, -5)])
+def test_bad_config_rejected(field, value, code):
+    cfg = ftts.make_config(workload.TINY, ftts.F32)
+    setattr(cfg, field, value)
+    assert ftts.lib().ftts_workspace_bytes(ctypes.byref(cfg), 1, 0) == 0
+    w = _fake_weights(cfg)
+    rc = _decode(w, B=1)
+    assert rc == code, ftts.lib().ftts_last_error()
+
+
+def _fake_weights(cfg):
+    n = max(cfg.n_layer, 1)
+    layers = (ftts.Layer * n)()
+    for L in layers:
+        L.ln1_g = L.ln1_b = L.ln2_g = L.ln2_b = FAKE
+        for lin in (L.qkv, L.out, L.fc1, L.fc2):
+            lin.w = lin.bias = lin.scale = lin.zero = FAKE
+    w = ftts.Weights()
+    w.cfg = cfg
+    w.tok_emb = w.pos_emb = w.lnf_g = w.lnf_b = FAKE
+    w.layers = layers
+    w.head.w = w.head.bias = FAKE
+    w._layers = layers
+    return w
+
+
+def _decode(w, B=1, samp=None, ws_bytes=1 << 30, tokens=FAKE, uniforms=FAKE, pt=None, kv=None, ws=FAKE):
+    pt = pt or ftts.PageTable(FAKE, FAKE, 4)
+    kv = kv or ftts.KvPool(FAKE, 16)
+    samp = samp or ftts.Sampling(1.0, 1, 1.0)
+    return ftts.lib().ftts_decode_step(ctypes.byref(w), tokens, FAKE, ctypes.byref(pt), ctypes.byref(kv), FAKE,
+                                       FAKE, uniforms, ctypes.byref(samp), B, ws, ws_bytes, None)
+
+
+def test_decode_argument_errors():
+    cfg = ftts.make_config(workload.TINY, ftts.F32)
+    w = _fake_weights(cfg)
+    assert _decode(w, B=0) == -2
+    assert _decode(w, B=ftts.MAX_BATCH + 1) == -2
+    assert _decode(w, tokens=None) == -1
+    assert _decode(w, samp=ftts.Sampling(1.0, 0, 1.0)) == -5
+    assert _decode(w, samp=ftts.Sampling(1.0, ftts.MAX_TOP_K + 1, 1.0)) == -5
+    assert _decode(w, samp=ftts.Sampling(0.0, 5, 0.9)) == -5
+    assert _decode(w, samp=ftts.Sampling(1.0, 5, 1.5)) == -5
+    assert _decode(w, samp=ftts.Sampling(1.0, 5, 0.9), uniforms=None) == -1
+    assert _decode(w, ws_bytes=16) == -8
+    assert _decode(w, ws=FAKE + 4) == -4
+    assert _decode(w, pt=ftts.PageTable(FAKE, FAKE, 0)) == -2
+    assert _decode(w, kv=ftts.KvPool(None, 4)) == -1
+    assert "kv.base" in ftts.lib().ftts_last_error().decode()
+    w.head.w = FAKE + 8
+    assert _decode(w) == -4
+    w.head.w = FAKE
+    w.layers[1].fc2.bias = None
+    assert _decode(w) == -1
+
+
+def test_quantised_modes_need_scales():
+    cfg = ftts.make_config(workload.TINY, ftts.W4A16)
+    w = _fake_weights(cfg)
+    w.layers[0].qkv.zero = None
+    assert _decode(w) == -1
+    cfg.group_size = 64
+    w = _fake_weights(cfg)
+    assert _decode(w) == -7
+
+
+def test_prefill_argument_errors():
+    cfg = ftts.make_config(workload.TINY, ftts.F32)
+    w = _fake_weights(cfg)
+    pt = ftts.PageTable(FAKE, None, 1)
+    kv = ftts.KvPool(FAKE, 4)
+    L = ftts.lib()
+
+    def call(lens, B=None):
+        arr = (ctypes.c_int32 * max(len(lens), 1))(*lens)
+        return L.ftts_prefill(ctypes.byref(w), FAKE, arr, len(lens) if B is None else B, ctypes.byref(pt),
+                              ctypes.byref(kv), FAKE, FAKE, 1 << 30, None)
+
+    assert call([0]) == -5
+    assert call([65]) == -5          # more rows than max_pages * 64
+    assert call([], B=0) == -2
+    assert L.ftts_prefill(ctypes.byref(w), FAKE, None, 1, ctypes.byref(pt), ctypes.byref(kv), FAKE, FAKE,
+                          1 << 30, None) == -1
+
+
+def test_quantize_and_sample_argument_errors():
+    L = ftts.lib()
+    assert L.ftts_quantize_weights(7, FAKE, 4, 128, 128, FAKE, FAKE, FAKE, None) == -3
+    assert L.ftts_quantize_weights(ftts.W4A16, FAKE, 4, 100, 128, FAKE, FAKE, FAKE, None) == -2
+    assert L.ftts_quantize_weights(ftts.W4A16, FAKE, 4, 256, 64, FAKE, FAKE, FAKE, None) == -7
+    assert L.ftts_quantize_weights(ftts.W4A16, FAKE, 4, 256, 128, FAKE, FAKE, None, None) == -1
+    assert L.ftts_quantize_weights(ftts.W8A16, FAKE, 4, 24, 128, FAKE, FAKE, None, None) == -2
+    assert L.ftts_quantize_weights(ftts.W8A16, None, 4, 32, 128, FAKE, FAKE, None, None) == -1
+    s = ftts.Sampling(1.0, 10, 0.9)
+    assert L.ftts_sample(FAKE, 1, 5, ctypes.byref(s), FAKE, FAKE, None) == -5   # top_k > V
+    assert L.ftts_sample(FAKE, 0, 50, ctypes.byref(s), FAKE, FAKE, None) == -2
+    assert L.ftts_sample(FAKE, 1, 50000, ctypes.byref(s), FAKE, FAKE, None) == -2
+    assert L.ftts_sample(None, 1, 50, ctypes.byref(s), FAKE, FAKE, None) == -1
+
+
+def test_page_pool_allocator():
+    p = ftts.PagePool(4)
+    a = p.alloc(3)
+    assert sorted(a) == [0, 1, 2]
+    with pytest.raises(ftts.FTTSError):
+        p.alloc(2)
+    p.release(a)
+    assert len(p.alloc(4)) == 4

@@ -1,0 +1,271 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.
+
+Bars: quantised codes, scales, zero-points and packed words bit-exact; greedy
+and sampled choices equal (sampled ones except where the draw sits within
+1e-5 of a cumulative-sum boundary); fp32 logits within 1e-4 normwise; bf16-
+storage logits within 3e-2 absolute of the fp32 oracle on the same
+dequantised weights; argmax equal away from near-ties; page placement
+bit-for-bit irrelevant.
+"""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import gpt as ogpt
+from oracle import quant as oquant
+from oracle import sample as osample
+from paper_2607_21042_amd import workload
+from tests import helpers
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+MODES = ["f32", "bf16", "w8a16", "w4a16"]
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available()
+    return torch
+
+
+def wd(name):
+    from paper_2607_21042_amd import ftts
+    return {"f32": ftts.F32, "bf16": ftts.BF16, "w8a16": ftts.W8A16, "w4a16": ftts.W4A16}[name]
+
+
+def model_inputs(shape, mode, master):
+    if mode == "f32":
+        return master
+    if mode == "bf16":
+        return workload.bf16_weights(master)
+    return workload.quantisable_weights(master)
+
+
+# ------------------------------------------------------------------------------ quantiser
+def gpu_quantize(torch, w, mode):
+    from paper_2607_21042_amd import ftts
+    N, K = w.shape
+    wt = torch.from_numpy(np.ascontiguousarray(w, np.float32)).cuda()
+    if mode == "w8a16":
+        codes = torch.empty((N, K), dtype=torch.int8, device="cuda")
+        scales = torch.empty((N,), dtype=torch.int16, device="cuda")
+        ftts.quantize_weights(ftts.W8A16, wt, codes, scales)
+        torch.cuda.synchronize()
+        return codes.cpu().numpy(), scales.cpu().numpy().view(np.uint16), None
+    codes = torch.empty((N, K // 8), dtype=torch.int32, device="cuda")
+    scales = torch.empty((N, K // 128), dtype=torch.int16, device="cuda")
+    zeros = torch.empty((N, K // 128), dtype=torch.int16, device="cuda")
+    ftts.quantize_weights(ftts.W4A16, wt, codes, scales, zeros)
+    torch.cuda.synchronize()
+    return codes.cpu().numpy(), scales.cpu().numpy().view(np.uint16), zeros.cpu().numpy().view(np.uint16)
+
+
+def special_rows(K, rng):
+    """Rows that exercise the corner cases: all zero, constant, one spike, ties."""
+    rows = [np.zeros(K), np.full(K, 0.5), np.full(K, -0.25), np.zeros(K), rng.standard_normal(K) * 1e-30]
+    rows[3][K // 3] = 3.0
+    t = np.round(rng.standard_normal(K) * 4) / 2  # many exact .5 multiples -> rint ties
+    t[0] = 127.0
+    rows.append(t)
+    return np.array(rows, dtype=np.float32)
+
+
+@pytest.mark.parametrize("mode", ["w8a16", "w4a16"])
+def test_quantiser_bit_exact(torch_cuda, mode):
+    torch = torch_cuda
+    rng = np.random.default_rng(40)
+    g = json.load(open(os.path.join(GOLDEN, "quant_examples.json")))
+    cases = []
+    if mode == "w8a16":
+        w = np.zeros((3, 16), np.float32)
+        w[:, :4] = np.array(g["w8"]["rows"], np.float32)
+        cases.append(("golden", w))
+    else:
+        G = 128
+        w = np.zeros((2, 2 * G), np.float32)
+        for blk in g["w4"]["rows_sparse"]:
+            a, b = blk["cols"]
+            w[blk["row"], a:b] = blk["fill"]
+            for k, v in blk["values"].items():
+                w[blk["row"], a + int(k)] = v
+        cases.append(("golden", w))
+    for N, K in [(3840, 1280), (1280, 5120), (7, 384)]:
+        w = rng.standard_normal((N, K)).astype(np.float32) * 0.02
+        w[:6] = special_rows(K, rng)
+        cases.append((f"{N}x{K}", w))
+    for name, w in cases:
+        say(f"quantiser {mode} {name}")
+        codes, sbits, zbits = gpu_quantize(torch, w, mode)
+        if mode == "w8a16":
+            q, s = oquant.quantize_w8(w)
+            np.testing.assert_array_equal(codes, q, err_msg=name)
+            np.testing.assert_array_equal(sbits, oquant.to_bits(s), err_msg=name)
+        else:
+            q, s, z = oquant.quantize_w4(w)
+            np.testing.assert_array_equal(codes, oquant.pack_w4(q), err_msg=name)
+            np.testing.assert_array_equal(sbits, oquant.to_bits(s), err_msg=name)
+            np.testing.assert_array_equal(zbits, oquant.to_bits(z), err_msg=name)
+    if mode == "w8a16":
+        np.testing.assert_array_equal(gpu_quantize(torch, cases[0][1], mode)[0][:, :4], g["w8"]["codes"])
+
+
+# ------------------------------------------------------------------------------ sampler
+def test_sampler_matches_oracle(torch_cuda):
+    torch = torch_cuda
+    from paper_2607_21042_amd import ftts
+    V = workload.INDEXTTS2.vocab
+    B = 256
+    logits = workload.random_logits(B, V, seed=41)
+    logits[:8, 100:110] = logits[:8, 100:101]       # exact ties across several indices
+    logits[8:16, :] = np.float32(-1.0)
+    logits[8:16, 7] = 5.0
+    us = workload.uniforms(1, B, seed=42)[0]
+    lt = torch.from_numpy(logits).cuda()
+    ut = torch.from_numpy(us).cuda()
+    out = torch.empty(B, dtype=torch.int32, device="cuda")
+    near, checked = 0, 0
+    for (T, k, p) in [(1.0, 1, 1.0), (0.8, 30, 0.8), (1.3, 64, 0.95), (0.5, 5, 1.0), (2.0, 64, 0.1)]:
+        say(f"sampler T={T} k={k} p={p}")
+        s = ftts.Sampling(T, k, p)
+        ftts.sample(lt, s, ut, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        for b in range(B):
+            want, det = osample.sample(logits[b], T, k, p, us[b])
+            checked += 1
+            if got[b] != want:
+                assert osample.near_boundary(det), (T, k, p, b, got[b], want)
+                near += 1
+    assert near <= checked * 0.01
+    # hand-worked examples
+    g = json.load(open(os.path.join(GOLDEN, "sampler_examples.json")))
+    for c in g["cases"]:
+        lg = (np.log(np.array(c["logits_log_probs"], np.float64)) * c.get("logit_scale", 1.0)
+              if "logits_log_probs" in c else np.array(c["logits"])).astype(np.float32)
+        for u, want in c["draws"]:
+            s = ftts.Sampling(c["temperature"], c["top_k"], c["top_p"])
+            o = torch.empty(1, dtype=torch.int32, device="cuda")
+            ftts.sample(torch.from_numpy(lg[None]).cuda(), s, torch.tensor([u], dtype=torch.float32).cuda(), o)
+            assert int(o.cpu()[0]) == want, (c, u)
+
+
+# ------------------------------------------------------------------------------ end to end
+def compare_run(res, oracle_model, prefixes, fed, mode, check_sampled=True):
+    """Per-step logits tolerance and greedy agreement for every sequence."""
+    worst, near = 0.0, 0
+    B = len(prefixes)
+    for b in range(B):
+        steps = [t for t in range(fed.shape[0]) if fed[t, b] >= 0]
+        pre, ref = helpers.oracle_teacher_forced(oracle_model, prefixes[b], fed[steps, b])
+        ok, err = helpers.tolerance_ok(res["prefill"][b], pre, mode)
+        assert ok, ("prefill", b, err)
+        for i, t in enumerate(steps):
+            ok, err = helpers.tolerance_ok(res["logits"][t, b], ref[i], mode)
+            worst = max(worst, err)
+            assert ok, ("step", t, "seq", b, err)
+            if check_sampled:
+                agree, is_near = helpers.argmax_agrees(res["sampled"][t, b], ref[i], mode)
+                near += is_near
+                assert agree, ("argmax", t, b, res["sampled"][t, b], int(np.argmax(ref[i])))
+    return worst, near
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_tiny_greedy_decode(torch_cuda, mode):
+    """Tiny decoder, prefix 32, 16 greedy steps teacher-forced on the oracle's tokens."""
+    from paper_2607_21042_amd import ftts
+    shape = workload.TINY
+    master = workload.master_weights(shape, seed=0)
+    inputs = model_inputs(shape, mode, master)
+    prefix = workload.prefix_embeddings([32], shape.d_model, seed=1, bf16=(mode != "f32"))
+    om = ogpt.GPT(helpers.oracle_weights(inputs, mode), shape.n_head, shape.d_head,
+                  dtype=np.float64 if mode == "f32" else np.float32)
+    toks = om.greedy_decode(prefix, 16, shape.start_token)
+    fed = np.concatenate([[shape.start_token], toks[:-1]]).astype(np.int32)[:, None]
+    say(f"tiny greedy {mode}")
+    dm = ftts.DeviceModel(inputs, shape, wd(mode))
+    res = helpers.run_gpu(dm, shape, [prefix], fed)
+    worst, near = compare_run(res, om, [prefix], fed, mode)
+    say(f"  worst err {worst:.3g}, near ties {near}")
+
+
+@pytest.mark.parametrize("mode", ["f32", "bf16", "w4a16"])
+def test_ragged_batch_and_page_placement(torch_cuda, mode):
+    """Three sequences of ragged prefix length (spanning several pages and a partial
+    last page), one of them retired midway; the same run with physical pages
+    permuted gives bit-identical logits, and only the named slots are written."""
+    from paper_2607_21042_amd import ftts
+    import torch
+    shape = workload.TINY
+    inputs = model_inputs(shape, mode, workload.master_weights(shape, seed=0))
+    lens = [70, 1, 129]
+    flat = workload.prefix_embeddings(lens, shape.d_model, seed=1, bf16=(mode != "f32"))
+    prefixes = np.split(flat, np.cumsum(lens)[:-1])
+    T = 12
+    fed = workload.random_tokens(T, 3, shape.vocab, seed=4)
+    fed[0, :] = shape.start_token
+    fed[7:, 1] = -1                                  # sequence 1 retires after 7 steps
+    dm = ftts.DeviceModel(inputs, shape, wd(mode))
+    om = ogpt.GPT(helpers.oracle_weights(inputs, mode), shape.n_head, shape.d_head, dtype=np.float32)
+    say(f"ragged batch {mode}")
+    totals = [n + T for n in lens]
+    bt0, n_pages = helpers.make_block_table(totals, spare=3)
+    r0 = helpers.run_gpu(dm, shape, prefixes, fed, block_table=bt0, n_pages=n_pages, pool_fill=float("nan"))
+    compare_run(r0, om, prefixes, fed, mode, check_sampled=False)
+    assert np.all(r0["sampled"][7:, 1] == -1)
+    # only slots named by the page table hold data; everything else keeps the NaN fill
+    pool = r0["kv"].pool.float().cpu().numpy()
+    written = ~np.isnan(pool)
+    expect = np.zeros_like(written)
+    fed_counts = (fed >= 0).sum(axis=0)
+    for b, n in enumerate(lens):
+        used = n + int(fed_counts[b])
+        for t in range(used):
+            expect[:, bt0[b, t // 64], :, :, t % 64, :] = True
+    np.testing.assert_array_equal(written, expect)
+    say(f"ragged batch {mode} permuted pages")
+    bt1, _ = helpers.make_block_table(totals, seed=7, spare=3)
+    r1 = helpers.run_gpu(dm, shape, prefixes, fed, block_table=bt1, n_pages=n_pages)
+    np.testing.assert_array_equal(r0["logits"], r1["logits"])
+    np.testing.assert_array_equal(r0["prefill"], r1["prefill"])
+    # run-to-run determinism
+    r2 = helpers.run_gpu(dm, shape, prefixes, fed, block_table=bt1, n_pages=n_pages)
+    np.testing.assert_array_equal(r1["logits"], r2["logits"])
+    del torch
+
+
+@pytest.fixture(scope="module")
+def big_master():
+    return workload.master_weights(workload.INDEXTTS2, seed=0)
+
+
+@pytest.mark.parametrize("mode,P,T,B", [("bf16", 256, 32, 1), ("w8a16", 256, 16, 1), ("w4a16", 384, 16, 1),
+                                        ("w8a16", 256, 8, 8)])
+def test_indextts2_shape_teacher_forced(torch_cuda, big_master, mode, P, T, B):
+    """The 24-layer d=1280 GPT at its real shapes: prefill P rows, then T steps
+    teacher-forced on seeded tokens, every logit checked against the oracle."""
+    from paper_2607_21042_amd import ftts
+    shape = workload.INDEXTTS2
+    inputs = model_inputs(shape, mode, big_master)
+    flat = workload.prefix_embeddings([P] * B, shape.d_model, seed=1)
+    prefixes = np.split(flat, B)
+    fed = workload.random_tokens(T, B, shape.vocab, seed=4)
+    fed[0, :] = shape.start_token
+    say(f"indextts2 {mode} P={P} T={T} B={B}: upload")
+    dm = ftts.DeviceModel(inputs, shape, wd(mode))
+    say("  gpu run")
+    res = helpers.run_gpu(dm, shape, prefixes, fed)
+    say("  oracle")
+    om = ogpt.GPT(helpers.oracle_weights(inputs, mode), shape.n_head, shape.d_head, dtype=np.float32)
+    worst, near = compare_run(res, om, prefixes, fed, mode)
+    say(f"  worst abs err {worst:.3g}, near ties {near}")
