@@ -18,7 +18,9 @@ consecutive k (G = 128):
     mn = min(0, min of the group),  mx = max(0, max of the group)
          (the range always holds zero, so the zero-point lies in 0..15)
     s    = bf16((mx - mn) / 15)         (s = 1 if that is 0)
-    z    = clamp(rint(-mn / s), 0, 15)  stored as a bf16 (an integer, exact)
+    z    = clamp(rint(-mn / s), 0, 15)  stored as a bf16 (an integer, exact;
+                                         zero is +0, never the negative zero
+                                         that rint(-0 / s) yields)
     q    = clamp(rint(W[n,k] / s) + z, 0, 15)
     dequantised weight = (q - z) * s    (exact in fp32)
     packing: word[n][k // 8] holds q of column k in bits 4*(k%8) .. 4*(k%8)+3.
@@ -80,7 +82,7 @@ def quantize_w4(w, group=128):
     mx = np.maximum(g.max(axis=2), np.float32(0.0))
     s = bf16_rne((mx - mn) / np.float32(15.0))
     s = np.where(s == 0, np.float32(1.0), s).astype(np.float32)
-    z = np.clip(np.rint(-mn / s), 0, 15).astype(np.float32)
+    z = np.clip(np.rint(-mn / s), 0, 15).astype(np.float32) + np.float32(0.0)  # -0 -> +0
     q = np.rint(g / s[:, :, None]) + z[:, :, None]
     q = np.clip(q, 0, 15).astype(np.uint8).reshape(N, K)
     return q, s, z

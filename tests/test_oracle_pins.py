@@ -256,6 +256,8 @@ def test_w4_golden():
     np.testing.assert_array_equal(s, np.array(g["scales"], dtype=np.float32))
     np.testing.assert_array_equal(quant.to_bits(s), [[int(b, 16) for b in r] for r in g["scale_bits"]])
     np.testing.assert_array_equal(z, np.array(g["zeros"], dtype=np.float32))
+    # zero-points are non-negative integers: +0 is the only encoding of zero
+    np.testing.assert_array_equal(quant.to_bits(z), [[0x4040, 0x0000], [0x4170, 0x0000]])
     h = g["codes_head"]
     np.testing.assert_array_equal(q[0, :8], h["row0_group0"])
     np.testing.assert_array_equal(q[0, G:G + 4], h["row0_group1"])
