@@ -90,12 +90,16 @@ __global__ __launch_bounds__(64) void attn_decode_split(const AttnDecodeArgs a) 
         for (int j = 0; j < 8; ++j) o[j] *= alpha;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            const float pr = expf(sc[i] - m);
-            float vv[8];
-            load8<F32>(a.kv_base, vbase + (size_t)(i * 64 + lane) * 8, vv);
-            l += pr;
+            // Slots past the context hold whatever the pool held: never let them
+            // into the sum (0 * NaN would poison it).
+            if (p * kPage + i * 8 + grp < ctx) {
+                const float pr = expf(sc[i] - m);
+                float vv[8];
+                load8<F32>(a.kv_base, vbase + (size_t)(i * 64 + lane) * 8, vv);
+                l += pr;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) o[j] = fmaf(pr, vv[j], o[j]);
+                for (int j = 0; j < 8; ++j) o[j] = fmaf(pr, vv[j], o[j]);
+            }
         }
     }
     // Sum over the 8 token groups (lanes with equal l % 8 hold the same dims).
