@@ -37,6 +37,7 @@ def parse():
     p.add_argument("--prefix", type=int, default=256)
     p.add_argument("--decode", type=int, default=512)
     p.add_argument("--cpu-steps", type=int, default=16, help="decode steps timed for the CPU oracle baseline")
+    p.add_argument("--graph-steps", type=int, default=32, help="decode steps captured per HIP graph")
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
 
@@ -109,29 +110,52 @@ def main():
     n_pages = B * max_pages
     bt = torch.arange(n_pages, dtype=torch.int32, device="cuda").reshape(B, max_pages)
     kv = ftts.KVCache(shape, wdtype, n_pages)
-    steps = torch.arange(T, dtype=torch.int32, device="cuda")
-    positions = steps[:, None].repeat(1, B).contiguous()              # [T][B]
-    seq_lens = (steps[:, None] + P).repeat(1, B).contiguous()         # [T][B]
-    toks = torch.full((T + 1, B), shape.start_token, dtype=torch.int32, device="cuda")
     logits = torch.empty((B, shape.vocab), dtype=torch.float32, device="cuda")
     last = torch.empty((B, shape.vocab), dtype=torch.float32, device="cuda")
     ws = torch.empty(ftts.workspace_bytes(dm.cfg, B, B * P), dtype=torch.uint8, device="cuda")
     greedy = ftts.Sampling(1.0, 1, 1.0)
+    # Generation state; every decode step reads and updates it on the device.
+    tokens = torch.empty(B, dtype=torch.int32, device="cuda")
+    positions = torch.empty(B, dtype=torch.int32, device="cuda")
+    seq_lens = torch.empty(B, dtype=torch.int32, device="cuda")
+    sampled = torch.empty(B, dtype=torch.int32, device="cuda")
+    history = torch.empty((T, B), dtype=torch.int32, device="cuda")
+    counter = torch.empty(1, dtype=torch.int32, device="cuda")
+    pt = ftts.PageTableView(bt, seq_lens)
+    pt.seq_lens = seq_lens  # keep the same storage: the graph reads these pointers
+    pt.c = ftts.PageTable(bt.data_ptr(), seq_lens.data_ptr(), max_pages)
 
-    class _PT:  # page-table view of one step (block table shared, seq_lens row t)
-        def __init__(self, t):
-            self.c = ftts.PageTable(bt.data_ptr(), seq_lens[t].data_ptr(), max_pages)
-    pts = [_PT(t) for t in range(T)]
-    pt_prefill = _PT(0)
+    def reset():
+        tokens.fill_(shape.start_token)
+        positions.zero_()
+        seq_lens.fill_(P)
+        counter.zero_()
 
+    def one_step():
+        ftts.decode_step(dm, tokens, positions, pt, kv, logits, sampled, None, greedy, ws)
+        ftts.advance(tokens, positions, seq_lens, sampled, None, shape.stop_token, history, counter)
+
+    S = args.graph_steps if T % args.graph_steps == 0 else 1
     stream = torch.cuda.current_stream()
+    # eager warm-up (sets kernel attributes), then capture S steps into one graph
+    reset()
+    ftts.prefill(dm, prefix, [P] * B, pt, kv, last, ws)
+    for _ in range(2):
+        one_step()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(S):
+            one_step()
+    torch.cuda.synchronize()
 
     def job(ev=None):
-        ftts.prefill(dm, prefix, [P] * B, pt_prefill, kv, last, ws)
+        reset()
+        ftts.prefill(dm, prefix, [P] * B, pt, kv, last, ws)
         if ev is not None:
             ev[0].record(stream)
-        for t in range(T):
-            ftts.decode_step(dm, toks[t], positions[t], pts[t], kv, logits, toks[t + 1], None, greedy, ws)
+        for _ in range(T // S):
+            graph.replay()
         if ev is not None:
             ev[1].record(stream)
 
@@ -152,8 +176,8 @@ def main():
     total_ms = t_start.elapsed_time(t_end)
     decode_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
     job_ms = total_ms / args.steps
-    tokens = B * T
-    value = tokens / (job_ms / 1e3)
+    tokens_per_job = B * T
+    value = tokens_per_job / (job_ms / 1e3)
 
     kv_elem = 4 if mode == "f32" else 2
     step_bytes = [algorithmic_step_bytes(shape, dm, B, [P + t] * B, kv_elem) for t in range(T)]
@@ -165,7 +189,7 @@ def main():
         "vs_baseline": None, "dtype": {"f32": "f32", "bf16": "bf16", "w8a16": "int8-w/bf16", "w4a16": "int4-w/bf16"}[mode],
         "data": "synthetic: seeded random-init IndexTTS-2-shaped GPT (24x1280, 20 heads, FFN 5120, vocab 8194)",
         "config": {"workload": f"indextts2-gpt {mode} batch={B} prefix={P} greedy decode={T}", "batch": B,
-                   "prefix": P, "decode_tokens": T, "weights": mode},
+                   "prefix": P, "decode_tokens": T, "weights": mode, "graph_steps": S},
         "decode_ms_per_token_step": round(decode_ms / T, 4),
         "prefill_ms": round(job_ms - decode_ms, 3),
         "wall_s": round(wall, 3),

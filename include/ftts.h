@@ -226,6 +226,25 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
                      int32_t B, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Bookkeeping between two decode steps, done on the device so that a step can
+ * be replayed from a captured HIP graph with fixed pointers (the generation loop
+ * of the serving engine: one token per sequence per step, Sec. II-C).  For each
+ * sequence b with tokens[b] >= 0:
+ *   seq_lens[b] += 1 and positions[b] += 1 (the slot and position just used);
+ *   if remaining != NULL, remaining[b] -= 1, and when it reaches 0 the sampled id
+ *   is replaced by stop_token (in sampled[b] too) and the sequence retires:
+ *   tokens[b] = -1; otherwise tokens[b] = sampled[b];
+ *   if history != NULL and *step_counter < max_steps,
+ *   history[*step_counter][b] = sampled[b].
+ * Sequences with tokens[b] < 0 are left unchanged (history entry -1).  When
+ * step_counter != NULL it is incremented once.  All pointers are device int32
+ * arrays of B entries (history: [max_steps][B]); 1 <= B <= 1024.
+ */
+int ftts_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled,
+                 int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,
+                 int32_t max_steps, int32_t B, void* stream);
+
+/*
  * The sampler of ftts_decode_step on its own: logits [B][V] fp32, uniforms [B]
  * (may be NULL when top_k == 1), sampled_out [B] int32.  No workspace.
  */

@@ -2,13 +2,14 @@
 //
 // Decode (one query row per sequence and head, over its paged KV cache):
 //   o_h = softmax(q_h K_h^T / sqrt(64)) V_h over cached slots 0 .. seq_len
-// split over contiguous runs of `pps` logical pages (flash-decoding).  Each
-// split is one wave: a 64x64 K or V page is read as 8 fully coalesced 1 KB
-// wave loads, lane l holding dims (l%8)*8 .. +7 of tokens i*8 + l/8.  Scores
-// are reduced over the 8 lanes of a token, the page's softmax is folded into a
-// running (max, sum, output) triple, and the partial of each split is merged
-// with the log-sum-exp rule by a second kernel.  Splits follow logical pages,
-// so the result does not depend on where the pages live in the pool.
+// One workgroup per (head, sequence) whose 8 waves stride over the logical
+// pages (split-K inside the workgroup).  A 64x64 K or V page is read as 8 fully
+// coalesced 1 KB wave loads, lane l holding dims (l%8)*8 .. +7 of tokens
+// i*8 + l/8; the next page's K and V are loaded while the current one is used.
+// Scores are reduced over the 8 lanes of a token, each page's softmax is
+// folded into a running (max, sum, output) triple, and the 8 wave partials
+// are merged in LDS with the log-sum-exp rule.  The walk follows logical
+// pages, so the result does not depend on where pages live in the pool.
 //
 // Prefill (causal attention over each prefix, queries in tiles of 64): one
 // thread per query row keeps q and the output in registers and streams 64-key
@@ -31,18 +32,70 @@ __device__ __forceinline__ void load8(const void* base, size_t elem, float (&v)[
     }
 }
 
-template <bool F32>
-__global__ __launch_bounds__(64) void attn_decode_split(const AttnDecodeArgs a) {
-    const int s = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-    const int lane = threadIdx.x;
-    if (!a.active[b]) return;
-    const int ctx = a.seq_lens[b] + 1;                 // cached slots incl. the new token
-    const int n_pages_ctx = (ctx + kPage - 1) / kPage;
-    const int p0 = s * a.pps;
-    if (p0 >= n_pages_ctx) return;
-    const int p1 = min(p0 + a.pps, n_pages_ctx);
+// One page of K or V as seen by one lane: 8 chunks, each 8 consecutive dims of one token.
+template <bool F32> struct PageRegs;
+template <> struct PageRegs<false> { uint4 k[8], v[8]; };
+template <> struct PageRegs<true> { float4 k[16], v[16]; };
 
-    const int grp = lane >> 3, sub = lane & 7;         // token within 8-token row, dim block
+template <bool F32>
+__device__ __forceinline__ void load_page(const void* base, size_t kbase, size_t vbase, int lane, PageRegs<F32>& r) {
+    if constexpr (F32) {
+        const float4* K = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(base) + kbase);
+        const float4* V = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(base) + vbase);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            r.k[2 * i] = K[(i * 64 + lane) * 2];
+            r.k[2 * i + 1] = K[(i * 64 + lane) * 2 + 1];
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            r.v[2 * i] = V[(i * 64 + lane) * 2];
+            r.v[2 * i + 1] = V[(i * 64 + lane) * 2 + 1];
+        }
+    } else {
+        const uint4* K = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(base) + kbase);
+        const uint4* V = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(base) + vbase);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) r.k[i] = K[i * 64 + lane];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) r.v[i] = V[i * 64 + lane];
+    }
+}
+
+template <bool F32>
+__device__ __forceinline__ void unpack8(const PageRegs<F32>& r, bool is_v, int i, float (&x)[8]) {
+    if constexpr (F32) {
+        const float4 a = is_v ? r.v[2 * i] : r.k[2 * i];
+        const float4 b = is_v ? r.v[2 * i + 1] : r.k[2 * i + 1];
+        x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+    } else {
+        const uint4 w = is_v ? r.v[i] : r.k[i];
+        x[0] = bf16lo(w.x); x[1] = bf16hi(w.x); x[2] = bf16lo(w.y); x[3] = bf16hi(w.y);
+        x[4] = bf16lo(w.z); x[5] = bf16hi(w.z); x[6] = bf16lo(w.w); x[7] = bf16hi(w.w);
+    }
+}
+
+constexpr int kAttnWaves = 8;
+
+// One workgroup per (head, sequence); wave w walks logical pages w, w + 8, ...
+template <bool F32>
+__global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_kernel(const AttnDecodeArgs a) {
+    __shared__ float s_m[kAttnWaves], s_l[kAttnWaves];
+    __shared__ float s_o[kAttnWaves][kHeadDim];
+    const int h = blockIdx.x, b = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    float* out = a.o + (size_t)b * a.o_stride + h * kHeadDim;
+    if (!a.active[b]) {
+        if (tid < kHeadDim) out[tid] = 0.f;
+        return;
+    }
+    const int ctx = a.seq_lens[b] + 1;                 // cached slots incl. the new token
+    const int npg = (ctx + kPage - 1) / kPage;
+    const int grp = lane >> 3, sub = lane & 7;
+
+    // This wave's page ids: lane j holds the id of its j-th page (logical page w + 8 j).
+    const int lp = w + kAttnWaves * lane;
+    int my_phys = lp < npg ? a.block_table[(size_t)b * a.max_pages + lp] : -1;
     float q[8];
     {
         const float* qp = a.qkv + (size_t)b * a.qkv_stride + h * kHeadDim + sub * 8;
@@ -53,109 +106,121 @@ __global__ __launch_bounds__(64) void attn_decode_split(const AttnDecodeArgs a) 
 #pragma unroll
     for (int j = 0; j < 8; ++j) o[j] = 0.f;
 
-    for (int p = p0; p < p1; ++p) {
-        const int phys = a.block_table[(size_t)b * a.max_pages + p];
-        if (phys < 0 || phys >= a.n_pages) continue;
-        const size_t kbase = kv_offset(a.layer, a.n_pages, phys, 0, a.n_head, h, 0);
-        const size_t vbase = kv_offset(a.layer, a.n_pages, phys, 1, a.n_head, h, 0);
-        float sc[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            float kv[8];
-            load8<F32>(a.kv_base, kbase + (size_t)(i * 64 + lane) * 8, kv);
-            float t = 0.f;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) t = fmaf(q[j], kv[j], t);
-            sc[i] = t;
+    auto page_base = [&](int j, size_t& kb, size_t& vb) {
+        int phys = __shfl(my_phys, j, kWave);
+        const bool ok = phys >= 0 && phys < a.n_pages;
+        phys = ok ? phys : 0;
+        kb = kv_offset(a.layer, a.n_pages, phys, 0, a.n_head, h, 0);
+        vb = kv_offset(a.layer, a.n_pages, phys, 1, a.n_head, h, 0);
+        return ok;
+    };
+
+    const int my_pages = npg > w ? (npg - w + kAttnWaves - 1) / kAttnWaves : 0;
+    PageRegs<F32> cur, nxt;
+    size_t kb, vb;
+    bool ok_cur = false, ok_nxt = false;
+    if (my_pages > 0) {
+        ok_cur = page_base(0, kb, vb);
+        load_page<F32>(a.kv_base, kb, vb, lane, cur);
+    }
+    for (int j = 0; j < my_pages; ++j) {
+        const int p = w + kAttnWaves * j;
+        if (!F32 && j + 1 < my_pages) {                 // prefetch the next page (bf16 only)
+            ok_nxt = page_base(j + 1, kb, vb);
+            load_page<F32>(a.kv_base, kb, vb, lane, nxt);
         }
+        float sc[8];
         float pm = -INFINITY;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            float t = sc[i];
+            float kv[8];
+            unpack8<F32>(cur, false, i, kv);
+            float t = 0.f;
+#pragma unroll
+            for (int d = 0; d < 8; ++d) t = fmaf(q[d], kv[d], t);
             t += __shfl_xor(t, 1, kWave);
             t += __shfl_xor(t, 2, kWave);
             t += __shfl_xor(t, 4, kWave);
             const int tok = p * kPage + i * 8 + grp;
-            sc[i] = tok < ctx ? t : -INFINITY;
+            sc[i] = (ok_cur && tok < ctx) ? t : -INFINITY;
             pm = fmaxf(pm, sc[i]);
         }
         pm = fmaxf(pm, __shfl_xor(pm, 8, kWave));
         pm = fmaxf(pm, __shfl_xor(pm, 16, kWave));
         pm = fmaxf(pm, __shfl_xor(pm, 32, kWave));
-        const float mn = fmaxf(m, pm);
-        const float alpha = expf(m - mn);              // 0 on the first page (m = -inf)
-        m = mn;
-        l *= alpha;
+        if (pm > -INFINITY) {
+            const float mn = fmaxf(m, pm);
+            const float alpha = expf(m - mn);          // 0 on this wave's first valid page
+            m = mn;
+            l *= alpha;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) o[j] *= alpha;
+            for (int d = 0; d < 8; ++d) o[d] *= alpha;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            // Slots past the context hold whatever the pool held: never let them
-            // into the sum (0 * NaN would poison it).
-            if (p * kPage + i * 8 + grp < ctx) {
-                const float pr = expf(sc[i] - m);
-                float vv[8];
-                load8<F32>(a.kv_base, vbase + (size_t)(i * 64 + lane) * 8, vv);
-                l += pr;
+            for (int i = 0; i < 8; ++i) {
+                // Slots past the context (or of an invalid page) hold whatever the pool
+                // held: keep them out of the sum (0 * NaN would poison it).
+                if (sc[i] > -INFINITY) {
+                    const float pr = expf(sc[i] - m);
+                    float vv[8];
+                    unpack8<F32>(cur, true, i, vv);
+                    l += pr;
 #pragma unroll
-                for (int j = 0; j < 8; ++j) o[j] = fmaf(pr, vv[j], o[j]);
+                    for (int d = 0; d < 8; ++d) o[d] = fmaf(pr, vv[d], o[d]);
+                }
+            }
+        }
+        if (j + 1 < my_pages) {
+            if constexpr (F32) {
+                ok_cur = page_base(j + 1, kb, vb);
+                load_page<F32>(a.kv_base, kb, vb, lane, cur);
+            } else {
+                cur = nxt;
+                ok_cur = ok_nxt;
             }
         }
     }
     // Sum over the 8 token groups (lanes with equal l % 8 hold the same dims).
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        float t = o[j];
+    for (int d = 0; d < 8; ++d) {
+        float t = o[d];
         t += __shfl_xor(t, 8, kWave);
         t += __shfl_xor(t, 16, kWave);
         t += __shfl_xor(t, 32, kWave);
-        o[j] = t;
+        o[d] = t;
     }
     l += __shfl_xor(l, 8, kWave);
     l += __shfl_xor(l, 16, kWave);
     l += __shfl_xor(l, 32, kWave);
-    float* part = a.part + (((size_t)b * a.n_head + h) * a.n_splits + s) * kPartStride;
     if (lane < 8) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) part[lane * 8 + j] = o[j];
+        for (int d = 0; d < 8; ++d) s_o[w][lane * 8 + d] = o[d];
     }
     if (lane == 0) {
-        part[64] = m;
-        part[65] = l;
+        s_m[w] = m;
+        s_l[w] = l;
     }
-}
-
-__global__ __launch_bounds__(64) void attn_decode_merge(const AttnDecodeArgs a) {
-    const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
-    float* out = a.o + (size_t)b * a.o_stride + h * kHeadDim + d;
-    if (!a.active[b]) {
-        *out = 0.f;
-        return;
+    __syncthreads();
+    if (tid < kHeadDim) {                               // log-sum-exp merge of the wave partials
+        float M = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < kAttnWaves; ++i) M = fmaxf(M, s_m[i]);
+        float L = 0.f, acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < kAttnWaves; ++i) {
+            if (s_m[i] > -INFINITY) {
+                const float wgt = expf(s_m[i] - M);
+                L = fmaf(s_l[i], wgt, L);
+                acc = fmaf(s_o[i][tid], wgt, acc);
+            }
+        }
+        out[tid] = L > 0.f ? acc / L : 0.f;
     }
-    const int ctx = a.seq_lens[b] + 1;
-    const int n_pages_ctx = (ctx + kPage - 1) / kPage;
-    const int ns = (n_pages_ctx + a.pps - 1) / a.pps;
-    const float* part = a.part + ((size_t)b * a.n_head + h) * a.n_splits * kPartStride;
-    float M = -INFINITY;
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, part[s * kPartStride + 64]);
-    float L = 0.f, acc = 0.f;
-    for (int s = 0; s < ns; ++s) {
-        const float ms = part[s * kPartStride + 64];
-        if (ms == -INFINITY) continue;                 // split held no valid page
-        const float w = expf(ms - M);
-        L = fmaf(part[s * kPartStride + 65], w, L);
-        acc = fmaf(part[s * kPartStride + d], w, acc);
-    }
-    *out = L > 0.f ? acc / L : 0.f;
 }
 
 hipError_t launch_attn_decode(int wdtype, const AttnDecodeArgs& a, int B, hipStream_t st) {
-    const dim3 g1(a.n_splits, a.n_head, B);
-    if (wdtype == FTTS_F32) hipLaunchKernelGGL(attn_decode_split<true>, g1, dim3(64), 0, st, a);
-    else hipLaunchKernelGGL(attn_decode_split<false>, g1, dim3(64), 0, st, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_decode_merge, dim3(a.n_head, B), dim3(64), 0, st, a);
+    const dim3 g(a.n_head, B);
+    if (wdtype == FTTS_F32) hipLaunchKernelGGL(attn_decode_kernel<true>, g, dim3(kAttnWaves * 64), 0, st, a);
+    else hipLaunchKernelGGL(attn_decode_kernel<false>, g, dim3(kAttnWaves * 64), 0, st, a);
     return hipGetLastError();
 }
 

@@ -45,6 +45,11 @@ int check_config(const ftts_config* c) {
     if (c->wdtype == FTTS_W4A16 && c->group_size != 128)
         return fail(FTTS_E_UNSUPPORTED, "W4A16 group_size must be 128 (got %d)", c->group_size);
     if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return fail(FTTS_E_RANGE, "ln_eps must be finite and > 0");
+    const int head_wt = c->wdtype == FTTS_F32 ? FTTS_F32 : FTTS_BF16;
+    if (!gemv_supported(c->wdtype, c->d_model, true) || !gemv_supported(c->wdtype, c->d_model, false) ||
+        !gemv_supported(c->wdtype, c->d_ff, false) || !gemv_supported(head_wt, c->d_model, true))
+        return fail(FTTS_E_UNSUPPORTED, "no decode tiling for d_model=%d d_ff=%d in this weight mode", c->d_model,
+                    c->d_ff);
     return FTTS_OK;
 }
 
@@ -107,7 +112,8 @@ int check_kv(const ftts_page_table* pt, const ftts_kv_pool* kv, bool need_seq_le
     TRY(check_ptr(kv->base, "kv.base"));
     if (!pt->block_table) return fail(FTTS_E_INVALID_ARG, "block_table is NULL");
     if (need_seq_lens && !pt->seq_lens) return fail(FTTS_E_INVALID_ARG, "seq_lens is NULL");
-    if (pt->max_pages < 1) return fail(FTTS_E_SHAPE, "max_pages must be >= 1");
+    if (pt->max_pages < 1 || pt->max_pages > kMaxPages)
+        return fail(FTTS_E_SHAPE, "max_pages must be in [1, %d]", kMaxPages);
     if (kv->n_pages < 1) return fail(FTTS_E_SHAPE, "n_pages must be >= 1");
     return FTTS_OK;
 }
@@ -128,7 +134,7 @@ int check_sampling(const ftts_sampling* s, int V, const float* uniforms) {
 // Workspace regions (all 256-byte aligned).  Decode and prefill never run at the
 // same time on one workspace, so their regions overlap.
 struct DecodeWs {
-    float *x, *qkv, *o, *h, *part;
+    float *x, *qkv, *o, *h;
     int32_t* active;
 };
 struct PrefillWs {
@@ -147,9 +153,8 @@ size_t decode_bytes(const ftts_config& c, int B, DecodeWs* out, char* base) {
     char* qkv = take((size_t)B * 3 * c.d_model * 4);
     char* o = take((size_t)B * c.d_model * 4);
     char* h = take((size_t)B * c.d_ff * 4);
-    char* part = take((size_t)B * c.n_head * kMaxSplits * kPartStride * 4);
     char* act = take((size_t)B * 4);
-    if (out) *out = DecodeWs{(float*)x, (float*)qkv, (float*)o, (float*)h, (float*)part, (int32_t*)act};
+    if (out) *out = DecodeWs{(float*)x, (float*)qkv, (float*)o, (float*)h, (int32_t*)act};
     return off;
 }
 
@@ -236,6 +241,20 @@ int ftts_sample(const float* logits, int32_t B, int32_t V, const ftts_sampling* 
     return FTTS_OK;
 }
 
+int ftts_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled, int32_t* remaining,
+                 int32_t stop_token, int32_t* history, int32_t* step_counter, int32_t max_steps, int32_t B,
+                 void* stream) {
+    if (!tokens || !positions || !seq_lens || !sampled) return fail(FTTS_E_INVALID_ARG, "advance: NULL pointer");
+    if (B < 1 || B > 1024) return fail(FTTS_E_SHAPE, "advance: B must be in [1, 1024]");
+    if (history && (max_steps < 1 || !step_counter))
+        return fail(FTTS_E_INVALID_ARG, "advance: history needs step_counter and max_steps >= 1");
+    (void)hipGetLastError();
+    hipError_t e = launch_advance(tokens, positions, seq_lens, sampled, remaining, stop_token, history, step_counter,
+                                  max_steps, B, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "advance launch");
+    return FTTS_OK;
+}
+
 int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
                      const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out, int32_t* sampled_out,
                      const float* uniforms, const ftts_sampling* samp, int32_t B, void* ws, size_t ws_bytes,
@@ -255,12 +274,6 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
     DecodeWs W;
     decode_bytes(c, B, &W, reinterpret_cast<char*>(ws));
     const int d = c.d_model, H = c.n_head, F = c.d_ff, V = c.vocab;
-
-    // Split the KV walk so that about 2048 waves share the attention.
-    const int want = (2048 + B * H - 1) / (B * H);
-    const int splits = want < 1 ? 1 : (want > kMaxSplits ? kMaxSplits : want);
-    const int pps = (pt->max_pages + splits - 1) / splits;
-    const int n_splits = (pt->max_pages + pps - 1) / pps;
 
     (void)hipGetLastError();
     hipError_t e = launch_embed(c.wdtype, w->tok_emb, w->pos_emb, V, c.n_pos, d, tokens, positions, pt->seq_lens,
@@ -284,12 +297,9 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
     at.n_pages = kv->n_pages;
     at.n_head = H;
     at.max_pages = pt->max_pages;
-    at.pps = pps;
-    at.n_splits = n_splits;
     at.block_table = pt->block_table;
     at.seq_lens = pt->seq_lens;
     at.active = W.active;
-    at.part = W.part;
     at.o = W.o;
     at.o_stride = d;
 

@@ -13,8 +13,7 @@ namespace ftts {
 constexpr int kWave = 64;        // CDNA wavefront width
 constexpr int kPage = 64;        // KV tokens per page
 constexpr int kHeadDim = 64;     // attention head width
-constexpr int kMaxSplits = 32;   // split-K partitions per (sequence, head) in decode attention
-constexpr int kPartStride = 68;  // floats per split partial: o[64], m, l, pad
+constexpr int kMaxPages = 512;   // logical pages per sequence (32768 tokens)
 
 // ---- bf16 <-> fp32 --------------------------------------------------------------
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
@@ -28,6 +27,19 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     u += 0x7FFFu + ((u >> 16) & 1u);
     return (uint16_t)(u >> 16);
 }
+
+// 16-byte streaming load (weights are read once per call; the hint keeps them from
+// displacing activations in the caches).
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld_stream(const uint4* p) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Workgroup barrier for LDS traffic only.  __syncthreads() also waits for every
+// outstanding global load of the wave; this one leaves the weight stream in
+// flight.  Global data exchanged through it must have been waited for already.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // Activation/parameter element: fp32 in FTTS_F32 mode, bf16 in the 16-bit modes.
 template <bool F32>
@@ -84,7 +96,7 @@ struct GemvArgs {
     const uint16_t* scale;   // W8: [N]; W4: [N][K/128]
     const uint16_t* zero;    // W4: [N][K/128]
     const void* bias;        // [N] activation dtype
-    int N, K, B, lpr;        // lpr: lanes cooperating on one row
+    int N, K, B;
     const float* act;        // [B][K] fp32 input (x when LayerNorm is fused)
     const void* ln_g;        // LayerNorm gain / bias (activation dtype) or null
     const void* ln_b;
@@ -98,12 +110,11 @@ struct AttnDecodeArgs {
     const float* qkv;        // [B][3d] fp32; q of head h at h*64
     int qkv_stride;
     const void* kv_base;
-    int n_pages, layer, n_head, max_pages, pps, n_splits;
+    int n_pages, layer, n_head, max_pages;
     const int32_t* block_table;
     const int32_t* seq_lens;
     const int32_t* active;
-    float* part;             // [B][H][n_splits][kPartStride]
-    float* o;                // [B][o_stride] fp32 merged output
+    float* o;                // [B][o_stride] fp32 attention output
     int o_stride;
 };
 
@@ -139,6 +150,7 @@ hipError_t launch_embed(int wdtype, const void* tok_emb, const void* pos_emb, in
                         const int32_t* block_table, int max_pages, int n_pages, int B, float* x,
                         int32_t* active, hipStream_t st);
 hipError_t launch_gemv(int wdtype, int epi, bool ln, const GemvArgs& a, hipStream_t st);
+bool gemv_supported(int wdtype, int K, bool ln);
 hipError_t launch_attn_decode(int wdtype, const AttnDecodeArgs& a, int B, hipStream_t st);
 hipError_t launch_sample(const float* logits, int B, int V, const ftts_sampling& s, const float* uniforms,
                          const int32_t* active, int32_t* out, hipStream_t st);
@@ -149,6 +161,9 @@ hipError_t launch_ln_rows(int wdtype, const float* x, const void* g, const void*
 hipError_t launch_gemm(int wdtype, int epi, const GemmArgs& a, hipStream_t st);
 hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_tiles, hipStream_t st);
 hipError_t launch_gather_rows(const float* x, int d, const SeqTable& seqs, float* out, hipStream_t st);
+hipError_t launch_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled,
+                          int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,
+                          int max_steps, int B, hipStream_t st);
 hipError_t launch_act_to_f32(int wdtype, const void* src, int rows, int d, float* dst, hipStream_t st);
 
 }  // namespace ftts

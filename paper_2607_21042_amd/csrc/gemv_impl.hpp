@@ -1,19 +1,22 @@
-// Decode-time linear layers: y[b] = act[b] . W^T (+ bias, epilogue) for a small
-// batch of rows, streaming each weight byte from HBM exactly once per call.
+// Decode-time linear layers: y[b] = act[b] . W^T (+ bias, epilogue) for a small batch
+// of rows, streaming each weight byte from HBM once per call.
 //
-// One 256-thread workgroup owns 4 * (64 / lpr) consecutive output rows; `lpr`
-// lanes share a row and walk its K dimension in 16-byte chunks, so each group
-// of lanes issues fully coalesced 16-byte loads.  The fp32 activations of all
-// batch rows are staged in LDS (LayerNorm applied while staging when the
-// layer is preceded by one), and every weight chunk is dequantised in
-// registers and multiplied against all batch rows before the next chunk.
+// A 256-thread workgroup owns 4 * (64 / LPR) consecutive output rows; LPR lanes
+// share a row and each lane owns NCH 16-byte chunks of it per pass over K
+// (K = passes * LPR * NCH * elements-per-chunk).  Every global load a workgroup
+// needs -- its weight chunks, their quantisation parameters and the activations
+// -- is issued at the top, unrolled and branch-free, before the first barrier, so
+// the kernel's latency is one memory round trip plus the streaming time.
+// Activations are staged in LDS as fp32 (LayerNorm applied in place when the
+// layer is preceded by one), every weight chunk is dequantised in registers and
+// multiplied against all batch rows, and the LPR partial sums of a row are
+// reduced with cross-lane shuffles.
 //
-// Weight storage (element size per 16-byte chunk):
-//   FTTS_F32   4 fp32      FTTS_BF16  8 bf16
-//   FTTS_W8A16 16 int8 codes, one bf16 scale per row (applied once at the end)
-//   FTTS_W4A16 32 4-bit codes (one group of 128 spans 4 chunks); each chunk
-//              contributes s * (sum q x - z * sum x), the per-chunk sums of x
-//              being precomputed in LDS.
+// Weight storage (elements per 16-byte chunk):
+//   FTTS_F32 4 fp32 | FTTS_BF16 8 bf16 | FTTS_W8A16 16 int8 codes, one bf16 scale
+//   per row applied once at the end | FTTS_W4A16 32 4-bit codes of one 128-column
+//   group; a chunk contributes s * (sum q x - z * sum x), the per-chunk sums of x
+//   being formed while staging.
 #pragma once
 #include "ftts_internal.hpp"
 
@@ -25,10 +28,7 @@ template <> struct WInfo<FTTS_BF16> { static constexpr int EPC = 8; };
 template <> struct WInfo<FTTS_W8A16> { static constexpr int EPC = 16; };
 template <> struct WInfo<FTTS_W4A16> { static constexpr int EPC = 32; };
 
-constexpr int kActFloats = 12288;  // LDS budget for staged activations (48 KB); a multiple of 128 per batch row
-constexpr int kUnroll = 5;         // weight chunks in flight per lane
-
-__host__ __device__ constexpr int k_chunk(int bmax) { return kActFloats / bmax; }
+constexpr int kGemvLdsFloats = 24576;  // 96 KB of staged fp32 activations per workgroup
 
 template <int WT, int BMAX>
 __device__ __forceinline__ void dot_chunk(const uint4 wv, const float* __restrict__ xs, int stride, int B,
@@ -120,112 +120,143 @@ __device__ __forceinline__ void dot_chunk(const uint4 wv, const float* __restric
     }
 }
 
-template <int WT, int BMAX, int EPI, bool LN>
+// LPR lanes per row, NCH 16-byte chunks per lane per pass, up to BMAX batch rows.
+template <int WT, int BMAX, int EPI, bool LN, int LPR, int NCH>
 __global__ __launch_bounds__(256) void gemv_kernel(const GemvArgs a) {
     constexpr bool F32 = (WT == FTTS_F32);
     constexpr int EPC = WInfo<WT>::EPC;
-    constexpr int KC = k_chunk(BMAX);
-    extern __shared__ float s_act[];              // [BMAX][min(KC, K)]
-    __shared__ float s_xsum[kActFloats / 32];     // W4: per-32-column sums of the activations
+    constexpr int RPW = kWave / LPR;
+    constexpr int PK = LPR * NCH * EPC;          // K columns per pass
+    extern __shared__ float s_act[];              // [BMAX][PK] (+ W4 chunk sums [BMAX][PK/32])
     __shared__ float s_mean[BMAX], s_rstd[BMAX];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int lpr = a.lpr;
-    const int li = lane & (lpr - 1);
-    const int rpw = kWave / lpr;
-    const int row = blockIdx.x * (4 * rpw) + wave * rpw + lane / lpr;
+    const int li = lane & (LPR - 1);
+    const int row = blockIdx.x * (4 * RPW) + wave * RPW + lane / LPR;
     const bool row_ok = row < a.N;
+    const int rr = row_ok ? row : a.N - 1;        // loads stay in bounds; results discarded
     const int B = a.B, K = a.K;
-    const int kcs = K < KC ? K : KC;              // LDS row stride of the staged activations
-
-    if constexpr (LN) {
-        for (int b = wave; b < B; b += 4) {
-            const float* xr = a.act + (size_t)b * K;
-            float s = 0.f;
-            for (int k = lane; k < K; k += kWave) s += xr[k];
-            const float mean = wave_sum(s) / (float)K;
-            float v = 0.f;
-            for (int k = lane; k < K; k += kWave) {
-                const float d = xr[k] - mean;
-                v = fmaf(d, d, v);
-            }
-            v = wave_sum(v) / (float)K;
-            if (lane == 0) {
-                s_mean[b] = mean;
-                s_rstd[b] = 1.0f / sqrtf(v + a.eps);
-            }
-        }
-    }
-
-    float acc[BMAX];
-#pragma unroll
-    for (int b = 0; b < BMAX; ++b) acc[b] = 0.f;
+    const int n_groups = K / 128;
+    float* s_xsum = s_act + BMAX * PK;
 
     size_t row_bytes;
     if constexpr (WT == FTTS_W4A16) row_bytes = (size_t)K / 2;
     else if constexpr (WT == FTTS_W8A16) row_bytes = (size_t)K;
     else row_bytes = (size_t)K * (F32 ? 4 : 2);
-    const uint4* wrow = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(a.w) +
-                                                       row_bytes * (size_t)(row_ok ? row : 0));
-    const int n_groups = K / 128;
+    const uint4* wrow = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(a.w) + row_bytes * rr);
 
-    for (int kc = 0; kc < K; kc += KC) {
-        const int kn = (K - kc) < KC ? (K - kc) : KC;
-        __syncthreads();
-        for (int i = tid; i < B * kn; i += 256) {
-            const int b = i / kn, k = i - b * kn;
-            float v = a.act[(size_t)b * K + kc + k];
-            if constexpr (LN)
-                v = (v - s_mean[b]) * s_rstd[b] * ld_act<F32>(a.ln_g, kc + k) + ld_act<F32>(a.ln_b, kc + k);
-            s_act[b * kcs + k] = v;
+    float acc[BMAX];
+#pragma unroll
+    for (int b = 0; b < BMAX; ++b) acc[b] = 0.f;
+
+    constexpr int PK4 = PK / 4;                   // float4s of one staged batch row
+    constexpr int NV = (BMAX * PK4 + 255) / 256;  // staged float4s per thread (<= 24 by the LDS budget)
+    constexpr int NLN = LN ? (PK + 255) / 256 : 1;
+    const float4* act4 = reinterpret_cast<const float4*>(a.act);
+    float4* dst4 = reinterpret_cast<float4*>(s_act);
+    const int total = B * PK4;
+
+    for (int k0 = 0; k0 < K; k0 += PK) {
+        // The vector-memory counter retires loads in issue order, so everything
+        // the prologue waits for (activations, LayerNorm and quantisation
+        // parameters) is issued before the weight stream, which then stays in
+        // flight while the activations are staged and normalised (the barriers
+        // below wait for LDS traffic only).
+        if (k0 > 0) lds_barrier();
+        float4 v[NV];
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int j = min(tid + 256 * i, total - 1);
+            const int b = j / PK4;
+            v[i] = act4[((size_t)b * K + k0) / 4 + (j - b * PK4)];
+        }
+        float lg[NLN], lb[NLN];
+        if constexpr (LN) {
+#pragma unroll
+            for (int i = 0; i < NLN; ++i) {
+                const int k = min(tid + 256 * i, PK - 1);
+                lg[i] = ld_act<F32>(a.ln_g, k);
+                lb[i] = ld_act<F32>(a.ln_b, k);
+            }
+        }
+        float s4[NCH], z4[NCH];
+        if constexpr (WT == FTTS_W4A16) {
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) {
+                const int g = (k0 + (li + i * LPR) * 32) >> 7;
+                s4[i] = bf16_to_f32(a.scale[(size_t)rr * n_groups + g]);
+                z4[i] = bf16_to_f32(a.zero[(size_t)rr * n_groups + g]);
+            }
+        }
+        // the weight stream of this pass
+        uint4 wv[NCH];
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) wv[i] = ld_stream(wrow + k0 / EPC + li + i * LPR);
+        // Unconditional stores (clamped lanes rewrite the last element with its own
+        // value) so the compiler keeps the loads above the weight stream.
+#pragma unroll
+        for (int i = 0; i < NV; ++i) dst4[min(tid + 256 * i, total - 1)] = v[i];
+        lds_barrier();
+        if constexpr (LN) {  // LN rows are single-pass (PK == K): stats from LDS, then normalise
+            for (int b = wave; b < B; b += 4) {
+                const float* xr = s_act + b * PK;
+                float s = 0.f;
+#pragma unroll
+                for (int i = 0; i < PK / kWave; ++i) s += xr[lane + kWave * i];
+                const float mean = wave_sum(s) / (float)PK;
+                float var = 0.f;
+#pragma unroll
+                for (int i = 0; i < PK / kWave; ++i) {
+                    const float d = xr[lane + kWave * i] - mean;
+                    var = fmaf(d, d, var);
+                }
+                var = wave_sum(var) / (float)PK;
+                if (lane == 0) {
+                    s_mean[b] = mean;
+                    s_rstd[b] = 1.0f / sqrtf(var + a.eps);
+                }
+            }
+            lds_barrier();
+#pragma unroll
+            for (int i = 0; i < NLN; ++i) {
+                const int k = tid + 256 * i;
+                if (k < PK) {
+#pragma unroll
+                    for (int b = 0; b < BMAX; ++b)
+                        if (b < B) s_act[b * PK + k] = (s_act[b * PK + k] - s_mean[b]) * s_rstd[b] * lg[i] + lb[i];
+                }
+            }
+            lds_barrier();
         }
         if constexpr (WT == FTTS_W4A16) {
-            __syncthreads();
-            const int nc = kn / 32;
-            for (int i = tid; i < B * nc; i += 256) {
-                const int b = i / nc, c = i - b * nc;
-                const float* p = s_act + b * kcs + c * 32;
+            constexpr int NC = PK / 32;
+            for (int i = tid; i < B * NC; i += 256) {
+                const int b = i / NC, c = i - b * NC;
+                const float* p = s_act + b * PK + c * 32;
                 float s = 0.f;
 #pragma unroll
                 for (int j = 0; j < 32; ++j) s += p[j];
-                s_xsum[b * (kcs / 32) + c] = s;
+                s_xsum[b * NC + c] = s;
             }
+            lds_barrier();
         }
-        __syncthreads();
-        if (row_ok) {
-            const int nch = kn / EPC;
-            const uint4* wp = wrow + kc / EPC;
-            for (int c0 = li; c0 < nch; c0 += lpr * kUnroll) {
-                uint4 wv[kUnroll];
+        // multiply
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
-                    const int c = c0 + u * lpr;
-                    if (c < nch) wv[u] = wp[c];
-                }
-#pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
-                    const int c = c0 + u * lpr;
-                    if (c < nch) {
-                        float s4 = 0.f, z4 = 0.f;
-                        if constexpr (WT == FTTS_W4A16) {
-                            const int g = (kc + c * 32) >> 7;
-                            s4 = bf16_to_f32(a.scale[(size_t)row * n_groups + g]);
-                            z4 = bf16_to_f32(a.zero[(size_t)row * n_groups + g]);
-                        }
-                        dot_chunk<WT, BMAX>(wv[u], s_act + c * EPC, kcs, B, acc, s4, z4, s_xsum + c,
-                                            kcs / 32);
-                    }
-                }
-            }
+        for (int i = 0; i < NCH; ++i) {
+            const int c = li + i * LPR;
+            float sv = 0.f, zv = 0.f;
+            if constexpr (WT == FTTS_W4A16) { sv = s4[i]; zv = z4[i]; }
+            dot_chunk<WT, BMAX>(wv[i], s_act + c * EPC, PK, B, acc, sv, zv, s_xsum + c, PK / 32);
         }
     }
 
-    // Reduce over the lanes of a row; every lane ends with the full sums.
+    // Reduce over the LPR lanes of a row; every lane ends with the full sums.
 #pragma unroll
     for (int b = 0; b < BMAX; ++b) {
         if (b < B) {
             float v = acc[b];
-            for (int o = lpr >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+#pragma unroll
+            for (int o = LPR >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
             acc[b] = v;
         }
     }
@@ -236,7 +267,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvArgs a) {
     const float bias = ld_act<F32>(a.bias, row);
 #pragma unroll
     for (int b = 0; b < BMAX; ++b) {
-        if (b < B && (b & (lpr - 1)) == li) {
+        if (b < B && (b & (LPR - 1)) == li) {
             const float v = fmaf(acc[b], rs, bias);
             float* o = a.out + (size_t)b * a.out_stride + row;
             if constexpr (EPI == EPI_STORE) {
@@ -262,39 +293,74 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvArgs a) {
     }
 }
 
-template <int WT, int BMAX, int EPI, bool LN>
-static hipError_t launch_one(const GemvArgs& a, hipStream_t st) {
-    const int rows_per_block = 4 * (kWave / a.lpr);
-    const int blocks = (a.N + rows_per_block - 1) / rows_per_block;
-    const int kcs = a.K < k_chunk(BMAX) ? a.K : k_chunk(BMAX);
-    const size_t lds = (size_t)BMAX * kcs * sizeof(float);
-    hipLaunchKernelGGL((gemv_kernel<WT, BMAX, EPI, LN>), dim3(blocks), dim3(256), lds, st, a);
+// (LPR, NCH) tilings of one pass over K that the launchers instantiate.
+struct Tiling {
+    int lpr, nch;
+};
+
+template <int WT, int BMAX, int EPI, bool LN, int LPR, int NCH>
+static hipError_t launch_tiled(const GemvArgs& a, hipStream_t st) {
+    constexpr int RPB = 4 * (kWave / LPR);
+    constexpr int PK = LPR * NCH * WInfo<WT>::EPC;
+    const int blocks = (a.N + RPB - 1) / RPB;
+    const size_t lds = (size_t)BMAX * PK * sizeof(float) + (WT == FTTS_W4A16 ? (size_t)BMAX * (PK / 32) * 4 : 0);
+    if (lds > 65536) {
+        static bool raised = false;  // once per instantiation
+        if (!raised) {
+            const hipError_t e = hipFuncSetAttribute(
+                reinterpret_cast<const void*>(&gemv_kernel<WT, BMAX, EPI, LN, LPR, NCH>),
+                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) return e;
+            raised = true;
+        }
+    }
+    hipLaunchKernelGGL((gemv_kernel<WT, BMAX, EPI, LN, LPR, NCH>), dim3(blocks), dim3(256), lds, st, a);
     return hipGetLastError();
 }
 
+#define FTTS_TILE_CASE(L, C) \
+    if (t.lpr == L && t.nch == C) return launch_tiled<WT, BMAX, EPI, LN, L, C>(a, st);
+
+template <int WT, int BMAX, int EPI, bool LN>
+static hipError_t by_tiling(const GemvArgs& a, Tiling t, hipStream_t st) {
+    FTTS_TILE_CASE(64, 10) FTTS_TILE_CASE(64, 5) FTTS_TILE_CASE(64, 4) FTTS_TILE_CASE(32, 5)
+    FTTS_TILE_CASE(32, 4) FTTS_TILE_CASE(16, 5) FTTS_TILE_CASE(16, 4) FTTS_TILE_CASE(16, 2)
+    FTTS_TILE_CASE(8, 5) FTTS_TILE_CASE(8, 4) FTTS_TILE_CASE(8, 2) FTTS_TILE_CASE(8, 1)
+    return hipErrorInvalidValue;
+}
+#undef FTTS_TILE_CASE
+
 template <int WT, int EPI, bool LN>
-static hipError_t by_batch(const GemvArgs& a, hipStream_t st) {
-    if (a.B <= 1) return launch_one<WT, 1, EPI, LN>(a, st);
-    if (a.B <= 2) return launch_one<WT, 2, EPI, LN>(a, st);
-    if (a.B <= 4) return launch_one<WT, 4, EPI, LN>(a, st);
-    if (a.B <= 8) return launch_one<WT, 8, EPI, LN>(a, st);
-    return launch_one<WT, 16, EPI, LN>(a, st);
+static hipError_t by_batch(const GemvArgs& a, Tiling t, hipStream_t st) {
+    if (a.B <= 1) return by_tiling<WT, 1, EPI, LN>(a, t, st);
+    if (a.B <= 4) return by_tiling<WT, 4, EPI, LN>(a, t, st);
+    return by_tiling<WT, 16, EPI, LN>(a, t, st);
 }
 
-// Instantiates the launchers of one weight type (one translation unit each).
-#define FTTS_GEMV_INSTANCE(WT, NAME)                                                        \
-    hipError_t NAME(int epi, bool ln, const GemvArgs& a, hipStream_t st) {                   \
-        if (epi == EPI_QKV && ln) return by_batch<WT, EPI_QKV, true>(a, st);                 \
-        if (epi == EPI_GELU && ln) return by_batch<WT, EPI_GELU, true>(a, st);               \
-        if (epi == EPI_RESID && !ln) return by_batch<WT, EPI_RESID, false>(a, st);           \
-        if (epi == EPI_STORE && ln && (WT == FTTS_F32 || WT == FTTS_BF16))                   \
-            return by_batch<WT, EPI_STORE, true>(a, st);                                     \
-        return hipErrorInvalidValue;                                                         \
-    }
+// LayerNorm-fused layers (q/k/v, FC1 + GELU, LM head) and residual layers (out-proj,
+// FC2) are instantiated in separate translation units per weight type.
+template <int WT>
+static hipError_t gemv_dispatch_ln(int epi, const GemvArgs& a, Tiling t, hipStream_t st) {
+    if (epi == EPI_QKV) return by_batch<WT, EPI_QKV, true>(a, t, st);
+    if (epi == EPI_GELU) return by_batch<WT, EPI_GELU, true>(a, t, st);
+    if constexpr (WT == FTTS_F32 || WT == FTTS_BF16)
+        if (epi == EPI_STORE) return by_batch<WT, EPI_STORE, true>(a, t, st);
+    return hipErrorInvalidValue;
+}
 
-hipError_t gemv_f32(int epi, bool ln, const GemvArgs& a, hipStream_t st);
-hipError_t gemv_bf16(int epi, bool ln, const GemvArgs& a, hipStream_t st);
-hipError_t gemv_w8(int epi, bool ln, const GemvArgs& a, hipStream_t st);
-hipError_t gemv_w4(int epi, bool ln, const GemvArgs& a, hipStream_t st);
+template <int WT>
+static hipError_t gemv_dispatch_res(int epi, const GemvArgs& a, Tiling t, hipStream_t st) {
+    if (epi == EPI_RESID) return by_batch<WT, EPI_RESID, false>(a, t, st);
+    return hipErrorInvalidValue;
+}
+
+hipError_t gemv_ln_f32(int epi, const GemvArgs& a, Tiling t, hipStream_t st);
+hipError_t gemv_ln_bf16(int epi, const GemvArgs& a, Tiling t, hipStream_t st);
+hipError_t gemv_ln_w8(int epi, const GemvArgs& a, Tiling t, hipStream_t st);
+hipError_t gemv_ln_w4(int epi, const GemvArgs& a, Tiling t, hipStream_t st);
+hipError_t gemv_res_f32(int epi, const GemvArgs& a, Tiling t, hipStream_t st);
+hipError_t gemv_res_bf16(int epi, const GemvArgs& a, Tiling t, hipStream_t st);
+hipError_t gemv_res_w8(int epi, const GemvArgs& a, Tiling t, hipStream_t st);
+hipError_t gemv_res_w4(int epi, const GemvArgs& a, Tiling t, hipStream_t st);
 
 }  // namespace ftts

@@ -235,6 +235,45 @@ hipError_t launch_sample(const float* logits, int B, int V, const ftts_sampling&
     return hipGetLastError();
 }
 
+// ---- generation-loop bookkeeping -----------------------------------------------------------
+__global__ __launch_bounds__(1024) void advance_kernel(int32_t* tokens, int32_t* positions, int32_t* seq_lens,
+                                                       int32_t* sampled, int32_t* remaining, int32_t stop_token,
+                                                       int32_t* history, int32_t* step_counter, int max_steps,
+                                                       int B) {
+    const int step = step_counter ? *step_counter : 0;
+    __syncthreads();  // every thread has read the counter before it moves
+    for (int b = threadIdx.x; b < B; b += blockDim.x) {
+        int h = -1;
+        if (tokens[b] >= 0) {
+            seq_lens[b] += 1;
+            positions[b] += 1;
+            int next = sampled[b];
+            if (remaining) {
+                const int r = remaining[b] - 1;
+                remaining[b] = r;
+                if (r <= 0) {
+                    next = stop_token;
+                    sampled[b] = stop_token;
+                }
+                tokens[b] = r <= 0 ? -1 : next;
+            } else {
+                tokens[b] = next;
+            }
+            h = next;
+        }
+        if (history && step < max_steps) history[(size_t)step * B + b] = h;
+    }
+    if (step_counter && threadIdx.x == 0) *step_counter = step + 1;
+}
+
+hipError_t launch_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled,
+                          int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,
+                          int max_steps, int B, hipStream_t st) {
+    hipLaunchKernelGGL(advance_kernel, dim3(1), dim3(B < 64 ? 64 : (B + 63) / 64 * 64), 0, st, tokens, positions,
+                       seq_lens, sampled, remaining, stop_token, history, step_counter, max_steps, B);
+    return hipGetLastError();
+}
+
 // ---- weight quantiser ----------------------------------------------------------------------
 // W8A16: one block per row.  s = bf16(amax / 127) (1 if 0); code = clamp(rint(w / s), -127, 127).
 __global__ __launch_bounds__(256) void quant_w8_kernel(const float* w, int64_t K, int8_t* codes,

@@ -89,6 +89,8 @@ def lib():
         L.ftts_decode_step.restype = _c.c_int
         L.ftts_decode_step.argtypes = [P(Weights), vp, vp, P(PageTable), P(KvPool), vp, vp, vp, P(Sampling), i32,
                                        vp, _c.c_size_t, vp]
+        L.ftts_advance.restype = _c.c_int
+        L.ftts_advance.argtypes = [vp, vp, vp, vp, vp, i32, vp, vp, i32, i32, vp]
         L.ftts_sample.restype = _c.c_int
         L.ftts_sample.argtypes = [vp, i32, i32, P(Sampling), vp, vp, vp]
         _lib = L
@@ -171,6 +173,15 @@ def decode_step(model, tokens, positions, page_table, kv, logits_out, sampled_ou
                                   _c.byref(kv.c), _ptr(logits_out), _ptr(sampled_out), _ptr(uniforms),
                                   _c.byref(sampling), B, _ptr(ws), ws.numel() * ws.element_size(),
                                   _stream(stream)))
+
+
+def advance(tokens, positions, seq_lens, sampled, remaining=None, stop_token=0, history=None, step_counter=None,
+            stream=None):
+    """ftts_advance: device-side bookkeeping between decode steps."""
+    B = tokens.numel()
+    max_steps = history.shape[0] if history is not None else 0
+    _check(lib().ftts_advance(_ptr(tokens), _ptr(positions), _ptr(seq_lens), _ptr(sampled), _ptr(remaining),
+                              stop_token, _ptr(history), _ptr(step_counter), max_steps, B, _stream(stream)))
 
 
 # --------------------------------------------------------------------------- device state

@@ -269,3 +269,111 @@ def test_indextts2_shape_teacher_forced(torch_cuda, big_master, mode, P, T, B):
     om = ogpt.GPT(helpers.oracle_weights(inputs, mode), shape.n_head, shape.d_head, dtype=np.float32)
     worst, near = compare_run(res, om, prefixes, fed, mode)
     say(f"  worst abs err {worst:.3g}, near ties {near}")
+
+
+# ------------------------------------------------------------------------------ step loop
+def test_advance_bookkeeping(torch_cuda):
+    """Device-side loop bookkeeping: exact integer semantics, STOP forcing, retirement."""
+    torch = torch_cuda
+    from paper_2607_21042_amd import ftts
+    B, T, STOP = 5, 6, 1023
+    tok = torch.tensor([3, 4, -1, 6, 7], dtype=torch.int32, device="cuda")
+    pos = torch.tensor([0, 5, 9, 1, 2], dtype=torch.int32, device="cuda")
+    lens = torch.tensor([10, 20, 30, 40, 50], dtype=torch.int32, device="cuda")
+    rem = torch.tensor([2, 1, 4, 9, 3], dtype=torch.int32, device="cuda")
+    hist = torch.full((T, B), 77, dtype=torch.int32, device="cuda")
+    ctr = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ref = dict(tok=[3, 4, -1, 6, 7], pos=[0, 5, 9, 1, 2], lens=[10, 20, 30, 40, 50], rem=[2, 1, 4, 9, 3])
+    ref_hist = []
+    for step in range(3):
+        samp_vals = [100 + 10 * step + b for b in range(B)]
+        samp = torch.tensor(samp_vals, dtype=torch.int32, device="cuda")
+        ftts.advance(tok, pos, lens, samp, rem, STOP, hist, ctr)
+        row = []
+        for b in range(B):
+            if ref["tok"][b] < 0:
+                row.append(-1)
+                continue
+            ref["lens"][b] += 1
+            ref["pos"][b] += 1
+            ref["rem"][b] -= 1
+            nxt = samp_vals[b] if ref["rem"][b] > 0 else STOP
+            ref["tok"][b] = nxt if ref["rem"][b] > 0 else -1
+            row.append(nxt)
+        ref_hist.append(row)
+        torch.cuda.synchronize()
+        assert tok.cpu().tolist() == ref["tok"]
+        assert pos.cpu().tolist() == ref["pos"]
+        assert lens.cpu().tolist() == ref["lens"]
+        assert rem.cpu().tolist() == ref["rem"]
+    assert int(ctr.cpu()[0]) == 3
+    assert hist[:3].cpu().tolist() == ref_hist
+    assert hist[3:].cpu().eq(77).all()
+
+
+def test_graph_replay_matches_eager(torch_cuda):
+    """A captured HIP graph of decode+advance steps, replayed several times with
+    eager work in between, reproduces the eager run bit for bit on every replay."""
+    torch = torch_cuda
+    from paper_2607_21042_amd import ftts
+    shape = workload.TINY
+    inputs = model_inputs(shape, "bf16", workload.master_weights(shape, seed=0))
+    lens = [40, 70]
+    B, T = 2, 8
+    flat = workload.prefix_embeddings(lens, shape.d_model, seed=1)
+    dm = ftts.DeviceModel(inputs, shape, ftts.BF16)
+    bt_np, n_pages = helpers.make_block_table([n + T for n in lens], seed=3)
+    bt = torch.from_numpy(bt_np).cuda()
+    kv = ftts.KVCache(shape, ftts.BF16, n_pages)
+    tokens = torch.empty(B, dtype=torch.int32, device="cuda")
+    positions = torch.empty(B, dtype=torch.int32, device="cuda")
+    seq_lens = torch.empty(B, dtype=torch.int32, device="cuda")
+    sampled = torch.empty(B, dtype=torch.int32, device="cuda")
+    hist = torch.empty((T, B), dtype=torch.int32, device="cuda")
+    ctr = torch.empty(1, dtype=torch.int32, device="cuda")
+    rem = torch.empty(B, dtype=torch.int32, device="cuda")
+    u = torch.from_numpy(workload.uniforms(1, B, seed=2)[0]).cuda()
+    logits = torch.empty((B, shape.vocab), dtype=torch.float32, device="cuda")
+    last = torch.empty((B, shape.vocab), dtype=torch.float32, device="cuda")
+    ws = torch.empty(ftts.workspace_bytes(dm.cfg, B, sum(lens)), dtype=torch.uint8, device="cuda")
+    prefix = torch.from_numpy(flat).cuda().to(torch.bfloat16)
+    pt = ftts.PageTableView(bt, seq_lens)
+    pt.c = ftts.PageTable(bt.data_ptr(), seq_lens.data_ptr(), bt.shape[1])
+    samp = ftts.Sampling(0.8, 30, 0.8)
+
+    def reset_and_prefill():
+        tokens.fill_(shape.start_token)
+        positions.zero_()
+        seq_lens.copy_(torch.tensor(lens, dtype=torch.int32))
+        ctr.zero_()
+        rem.copy_(torch.tensor([T, 5], dtype=torch.int32))   # sequence 1 stops after 5 tokens
+        ftts.prefill(dm, prefix, lens, pt, kv, last, ws)
+
+    def step():
+        ftts.decode_step(dm, tokens, positions, pt, kv, logits, sampled, u, samp, ws)
+        ftts.advance(tokens, positions, seq_lens, sampled, rem, shape.stop_token, hist, ctr)
+
+    say("graph replay: eager reference")
+    reset_and_prefill()
+    eager_logits = []
+    for _ in range(T):
+        step()
+        eager_logits.append(logits.clone())
+    torch.cuda.synchronize()
+    eager_hist = hist.clone()
+    assert eager_hist[4:, 1].cpu().tolist() == [shape.stop_token] + [-1] * (T - 5)
+    reset_and_prefill()
+    step()                               # warm-up before capture
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(3):
+        say(f"graph replay {rep}")
+        reset_and_prefill()
+        for t in range(T):
+            graph.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(logits, eager_logits[t]), (rep, t)
+            _ = (prefix.float() * 2).sum()  # unrelated eager work between replays
+        assert torch.equal(hist, eager_hist), rep
