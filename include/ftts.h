@@ -166,6 +166,19 @@ const char* ftts_last_error(void);
 /* Library version string. */
 const char* ftts_version(void);
 
+/* Decode implementation for later ftts_decode_step calls of this process:
+ * 0 automatic (the persistent single-launch step when the model and batch
+ * qualify -- d_model 1280, 20 heads, d_ff 5120, 256 <= vocab <= 16384, at most
+ * 50 layers, 16-bit or quantised weights, batch <= 2, per-layer tensors of each
+ * kind at a fixed stride, a 256-CU device -- otherwise one kernel per phase), 1 always one kernel per phase, 2 always
+ * the persistent step (calls that do not qualify return FTTS_E_UNSUPPORTED). */
+int ftts_set_decode_path(int32_t path);
+
+/* Synchronises `stream`, then reports FTTS_E_HIP if a persistent decode step on
+ * this workspace gave up waiting for one of its inputs (its bounded wait ran
+ * out), FTTS_OK otherwise.  ftts_prefill clears the condition. */
+int ftts_check_workspace(const void* ws, size_t ws_bytes, void* stream);
+
 /*
  * Weight-only quantisation of one fp32 matrix w [N][K] (Table I caption and
  * Sec. III-B: only the GPT's weights are quantised; activations stay 16-bit).
@@ -216,7 +229,10 @@ int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* l
  *   sampled_out [B] int32 chosen ids (-1 for inactive slots).
  *   uniforms    [B] fp32 in [0, 1); may be NULL when samp->top_k == 1.
  *   samp        [host] sampling parameters, shared by the batch.
- *   ws          workspace of at least ftts_workspace_bytes(cfg, B, 0).
+ *   ws          workspace of at least ftts_workspace_bytes(cfg, B, 0); it must
+ *               have been zero-filled or passed through ftts_prefill before
+ *               the first step (the persistent step keeps its step counter
+ *               and exchange buffers there).
  * Safe to capture in a HIP graph: no host synchronisation, no memset, and all
  * per-step inputs are read through device pointers.
  */

@@ -146,8 +146,30 @@ struct PrefillWs {
     int32_t* active; // [B] all ones (head GEMV reads no flags; kept for symmetry)
 };
 
-size_t decode_bytes(const ftts_config& c, int B, DecodeWs* out, char* base) {
+// The persistent decode step's control words and exchange buffers sit at the
+// start of every workspace, at a fixed size, so that decode and prefill calls
+// with different batch sizes agree on where they are.
+struct MegaWs {
+    uint32_t* ctl;
+    uint64_t *x, *qkv, *o, *h, *arg;
+};
+
+size_t mega_bytes(MegaWs* out, char* base) {
     size_t off = 0;
+    auto take = [&](size_t n) { size_t o = off; off += round256(n); return base ? base + o : nullptr; };
+    using namespace ftts::mega;
+    char* ctl = take(256);
+    char* x = take((size_t)BM * D * 8);
+    char* qkv = take((size_t)BM * 3 * D * 8);
+    char* o = take((size_t)BM * D * 8);
+    char* h = take((size_t)BM * FF * 8);
+    char* arg = take((size_t)G * BM * 2 * 8);
+    if (out) *out = MegaWs{(uint32_t*)ctl, (uint64_t*)x, (uint64_t*)qkv, (uint64_t*)o, (uint64_t*)h, (uint64_t*)arg};
+    return off;
+}
+
+size_t decode_bytes(const ftts_config& c, int B, DecodeWs* out, char* base) {
+    size_t off = mega_bytes(nullptr, nullptr);
     auto take = [&](size_t n) { size_t o = off; off += round256(n); return base ? base + o : nullptr; };
     char* x = take((size_t)B * c.d_model * 4);
     char* qkv = take((size_t)B * 3 * c.d_model * 4);
@@ -160,7 +182,7 @@ size_t decode_bytes(const ftts_config& c, int B, DecodeWs* out, char* base) {
 
 size_t prefill_bytes(const ftts_config& c, int B, int M, PrefillWs* out, char* base) {
     const size_t e = act_bytes(c);
-    size_t off = 0;
+    size_t off = mega_bytes(nullptr, nullptr);
     auto take = [&](size_t n) { size_t o = off; off += round256(n); return base ? base + o : nullptr; };
     char* x = take((size_t)M * c.d_model * 4);
     char* a = take((size_t)M * c.d_model * e);
@@ -170,6 +192,65 @@ size_t prefill_bytes(const ftts_config& c, int B, int M, PrefillWs* out, char* b
     char* act = take((size_t)B * 4);
     if (out) *out = PrefillWs{(float*)x, a, qkv, h, (float*)xl, (int32_t*)act};
     return off;
+}
+
+int g_decode_path = 0;  // 0 automatic, 1 kernel per phase, 2 persistent step
+
+// Per-layer pointers of one kind, if they sit at a fixed stride.
+template <typename F>
+bool stride_of(const ftts_weights* w, F get, Strided* out) {
+    const char* p0 = reinterpret_cast<const char*>(get(w->layers[0]));
+    const long long st = w->cfg.n_layer > 1 ? reinterpret_cast<const char*>(get(w->layers[1])) - p0 : 0;
+    for (int l = 0; l < w->cfg.n_layer; ++l)
+        if (reinterpret_cast<const char*>(get(w->layers[l])) != p0 + (long long)l * st) return false;
+    *out = Strided{p0, st};
+    return true;
+}
+
+int device_cus() {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (!cache[dev]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+// Fills the persistent step's arguments when the model and call qualify.
+bool mega_args(const ftts_weights* w, int B, mega::Args* a) {
+    const ftts_config& c = w->cfg;
+    using namespace ftts::mega;
+    if (c.wdtype == FTTS_F32 || c.d_model != D || c.d_ff != FF || c.n_head != NH) return false;
+    if (B < 1 || B > BM || c.n_layer > 50 || c.vocab < G || c.vocab > G * 64) return false;
+    if (device_cus() != G) return false;
+    bool ok = true;
+    ok &= stride_of(w, [](const ftts_layer& L) { return L.ln1_g; }, &a->ln1_g);
+    ok &= stride_of(w, [](const ftts_layer& L) { return L.ln1_b; }, &a->ln1_b);
+    ok &= stride_of(w, [](const ftts_layer& L) { return L.ln2_g; }, &a->ln2_g);
+    ok &= stride_of(w, [](const ftts_layer& L) { return L.ln2_b; }, &a->ln2_b);
+#define FTTS_LIN(NAME)                                                                          \
+    ok &= stride_of(w, [](const ftts_layer& L) { return L.NAME.w; }, &a->NAME##_w);             \
+    ok &= stride_of(w, [](const ftts_layer& L) { return L.NAME.scale; }, &a->NAME##_s);         \
+    ok &= stride_of(w, [](const ftts_layer& L) { return L.NAME.zero; }, &a->NAME##_z);          \
+    ok &= stride_of(w, [](const ftts_layer& L) { return L.NAME.bias; }, &a->NAME##_b);
+    FTTS_LIN(qkv) FTTS_LIN(out) FTTS_LIN(fc1) FTTS_LIN(fc2)
+#undef FTTS_LIN
+    if (!ok) return false;
+    a->n_layer = c.n_layer;
+    a->V = c.vocab;
+    a->n_pos = c.n_pos;
+    a->B = B;
+    a->eps = c.ln_eps;
+    a->tok_emb = w->tok_emb;
+    a->pos_emb = w->pos_emb;
+    a->lnf_g = w->lnf_g;
+    a->lnf_b = w->lnf_b;
+    a->head_w = w->head.w;
+    a->head_b = w->head.bias;
+    return true;
 }
 
 GemvArgs gemv_args(const ftts_linear& L, int N, int K, int B, const float* act, float* out, int out_stride) {
@@ -192,6 +273,24 @@ GemvArgs gemv_args(const ftts_linear& L, int N, int K, int B, const float* act, 
 extern "C" {
 
 const char* ftts_last_error(void) { return g_err; }
+
+int ftts_set_decode_path(int32_t path) {
+    if (path < 0 || path > 2) return fail(FTTS_E_RANGE, "decode path must be 0, 1 or 2");
+    g_decode_path = path;
+    return FTTS_OK;
+}
+
+int ftts_check_workspace(const void* ws, size_t ws_bytes, void* stream) {
+    if (!ws) return fail(FTTS_E_INVALID_ARG, "workspace is NULL");
+    if (ws_bytes < mega_bytes(nullptr, nullptr)) return fail(FTTS_E_WORKSPACE, "workspace too small");
+    hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "check_workspace sync");
+    uint32_t ctl[2] = {0, 0};
+    e = hipMemcpy(ctl, ws, sizeof ctl, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "check_workspace copy");
+    if (ctl[1]) return fail(FTTS_E_HIP, "a persistent decode step timed out waiting for its input (abort word set)");
+    return FTTS_OK;
+}
 
 const char* ftts_version(void) { return "ftts 0.1.0 gfx950"; }
 
@@ -274,6 +373,40 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
     DecodeWs W;
     decode_bytes(c, B, &W, reinterpret_cast<char*>(ws));
     const int d = c.d_model, H = c.n_head, F = c.d_ff, V = c.vocab;
+
+    mega::Args ma{};
+    const bool mega_ok = g_decode_path != 1 && mega_args(w, B, &ma);
+    if (g_decode_path == 2 && !mega_ok)
+        return fail(FTTS_E_UNSUPPORTED, "the persistent decode step does not take this model/batch/device");
+    if (mega_ok) {
+        MegaWs M;
+        mega_bytes(&M, reinterpret_cast<char*>(ws));
+        ma.max_pages = pt->max_pages;
+        ma.n_pages = kv->n_pages;
+        ma.greedy = samp->top_k == 1;
+        ma.tokens = tokens;
+        ma.positions = positions;
+        ma.seq_lens = pt->seq_lens;
+        ma.block_table = pt->block_table;
+        ma.kv = kv->base;
+        ma.logits = logits_out;
+        ma.sampled = sampled_out;
+        ma.active_out = W.active;
+        ma.ex_x = M.x;
+        ma.ex_qkv = M.qkv;
+        ma.ex_o = M.o;
+        ma.ex_h = M.h;
+        ma.ex_arg = M.arg;
+        ma.ctl = M.ctl;
+        (void)hipGetLastError();
+        hipError_t e = launch_decode_mega(c.wdtype, ma, st);
+        if (e != hipSuccess) return hip_fail(e, "persistent decode step");
+        if (samp->top_k != 1) {
+            e = launch_sample(logits_out, B, V, *samp, uniforms, W.active, sampled_out, st);
+            if (e != hipSuccess) return hip_fail(e, "sampler");
+        }
+        return FTTS_OK;
+    }
 
     (void)hipGetLastError();
     hipError_t e = launch_embed(c.wdtype, w->tok_emb, w->pos_emb, V, c.n_pos, d, tokens, positions, pt->seq_lens,
@@ -433,6 +566,11 @@ int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* l
         g.out = P.x;
         if ((e = launch_gemm(c.wdtype, EPI_RESID, g, st)) != hipSuccess) return hip_fail(e, "fc2 gemm");
     }
+    // A new generation starts: clear the persistent step's control words and
+    // exchange buffers (epoch 0 never matches a live epoch).
+    if ((e = launch_fill_u32(reinterpret_cast<uint32_t*>(ws), mega_bytes(nullptr, nullptr) / 4, 0u, st)) !=
+        hipSuccess)
+        return hip_fail(e, "workspace reset");
     if (last_logits) {
         if ((e = launch_gather_rows(P.x, d, seqs, P.xlast, st)) != hipSuccess) return hip_fail(e, "gather");
         GemvArgs g = gemv_args(w->head, V, d, B, P.xlast, last_logits, V);

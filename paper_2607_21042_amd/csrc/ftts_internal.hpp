@@ -81,6 +81,13 @@ __device__ __forceinline__ size_t kv_offset(int layer, int n_pages, int phys, in
 }
 
 // ---- launch arguments -------------------------------------------------------------
+// A per-layer tensor stored at a fixed stride: layer l lives at p + l * s bytes.
+struct Strided {
+    const char* p;
+    long long s;
+    __host__ __device__ const void* at(int l) const { return p ? p + (long long)l * s : nullptr; }
+};
+
 enum Epi { EPI_STORE = 0, EPI_QKV = 1, EPI_GELU = 2, EPI_RESID = 3 };
 
 struct KvAppend {            // where the QKV epilogue writes keys and values
@@ -164,6 +171,30 @@ hipError_t launch_gather_rows(const float* x, int d, const SeqTable& seqs, float
 hipError_t launch_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled,
                           int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,
                           int max_steps, int B, hipStream_t st);
+hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t st);
 hipError_t launch_act_to_f32(int wdtype, const void* src, int rows, int d, float* dst, hipStream_t st);
+
+namespace mega {
+constexpr int D = 1280, FF = 5120, NH = 20;
+constexpr int G = 256;   // workgroups of the persistent decode step, one per CU
+constexpr int BM = 2;    // largest batch it takes
+struct Args {
+    int n_layer, V, n_pos, B, max_pages, n_pages, greedy;
+    float eps;
+    Strided ln1_g, ln1_b, ln2_g, ln2_b;
+    Strided qkv_w, qkv_s, qkv_z, qkv_b, out_w, out_s, out_z, out_b;
+    Strided fc1_w, fc1_s, fc1_z, fc1_b, fc2_w, fc2_s, fc2_z, fc2_b;
+    const void *tok_emb, *pos_emb, *lnf_g, *lnf_b, *head_w, *head_b;
+    const int32_t *tokens, *positions, *seq_lens, *block_table;
+    void* kv;
+    float* logits;
+    int32_t* sampled;
+    int32_t* active_out;
+    uint64_t *ex_x, *ex_qkv, *ex_o, *ex_h, *ex_arg;
+    uint32_t* ctl;  // [0] step counter, [1] abort
+};
+
+}
+hipError_t launch_decode_mega(int wdtype, const mega::Args& a, hipStream_t st);
 
 }  // namespace ftts

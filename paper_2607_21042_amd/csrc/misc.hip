@@ -80,6 +80,17 @@ hipError_t launch_ln_rows(int wdtype, const float* x, const void* g, const void*
     return hipGetLastError();
 }
 
+// ---- fill (graph-safe replacement for a memset) -------------------------------------------------
+__global__ void fill_u32_kernel(uint32_t* p, size_t n, uint32_t v) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
+}
+
+hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t st) {
+    const int blocks = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(blocks > 0 ? blocks : 1), dim3(256), 0, st, p, n, v);
+    return hipGetLastError();
+}
+
 // ---- row copies ----------------------------------------------------------------------------
 __global__ void gather_last_kernel(const float* x, int d, SeqTable seqs, float* out) {
     const int b = blockIdx.x;

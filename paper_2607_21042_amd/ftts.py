@@ -89,6 +89,10 @@ def lib():
         L.ftts_decode_step.restype = _c.c_int
         L.ftts_decode_step.argtypes = [P(Weights), vp, vp, P(PageTable), P(KvPool), vp, vp, vp, P(Sampling), i32,
                                        vp, _c.c_size_t, vp]
+        L.ftts_set_decode_path.restype = _c.c_int
+        L.ftts_set_decode_path.argtypes = [i32]
+        L.ftts_check_workspace.restype = _c.c_int
+        L.ftts_check_workspace.argtypes = [vp, _c.c_size_t, vp]
         L.ftts_advance.restype = _c.c_int
         L.ftts_advance.argtypes = [vp, vp, vp, vp, vp, i32, vp, vp, i32, i32, vp]
         L.ftts_sample.restype = _c.c_int
@@ -175,6 +179,19 @@ def decode_step(model, tokens, positions, page_table, kv, logits_out, sampled_ou
                                   _stream(stream)))
 
 
+PATH_AUTO, PATH_KERNELS, PATH_PERSISTENT = 0, 1, 2
+
+
+def set_decode_path(path: int):
+    """ftts_set_decode_path: 0 automatic, 1 one kernel per phase, 2 the persistent step."""
+    _check(lib().ftts_set_decode_path(path))
+
+
+def check_workspace(ws, stream=None):
+    """ftts_check_workspace: raises if a persistent step on `ws` timed out waiting."""
+    _check(lib().ftts_check_workspace(_ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
 def advance(tokens, positions, seq_lens, sampled, remaining=None, stop_token=0, history=None, step_counter=None,
             stream=None):
     """ftts_advance: device-side bookkeeping between decode steps."""
@@ -200,78 +217,87 @@ class DeviceModel:
     `weights` is the numpy dict of the seeded input generator (fp32 arrays; in
     the 16-bit modes their values must be bf16-representable).  For W8A16 and
     W4A16 the four per-layer matrices are quantised on the GPU by
-    ftts_quantize_weights from the fp32 values given here.
+    ftts_quantize_weights from the fp32 values given here.  Every per-layer
+    tensor kind is one stacked allocation [n_layer, ...], so layer l of a kind
+    sits at a fixed stride (what the persistent decode step requires).
     """
+
+    LN_KINDS = ("ln1_g", "ln1_b", "ln2_g", "ln2_b")
+    LINEARS = ("qkv", "out", "fc1", "fc2")
 
     def __init__(self, weights: dict, shape, wdtype: int, device="cuda", stream=None):
         self.shape, self.wdtype = shape, wdtype
         self.cfg = make_config(shape, wdtype)
         adt = act_dtype(wdtype)
-        self._keep = []
+        L = shape.n_layer
+        self.tensors = {}
 
         def up(a, dtype=adt):
             t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
-            if dtype != torch.float32:
-                t = t.to(dtype)
-            self._keep.append(t)
-            return t
+            return t if dtype == torch.float32 else t.to(dtype)
 
-        def linear(w, b, quantise: bool):
-            L = Linear()
-            L.bias = up(b).data_ptr()
-            if not quantise or wdtype in (F32, BF16):
-                L.w = up(w).data_ptr()
-                return L
-            N, K = w.shape
-            w32 = torch.from_numpy(np.ascontiguousarray(w, dtype=np.float32)).to(device)
+        def stacked(key):
+            return up(np.stack([lw[key] for lw in weights["layers"]]))
+
+        for k in self.LN_KINDS:
+            self.tensors[k] = stacked(k)
+        for name in self.LINEARS:
+            self.tensors["b_" + name] = stacked("b_" + name)
+            N, K = weights["layers"][0]["w_" + name].shape
+            if wdtype in (F32, BF16):
+                self.tensors["w_" + name] = stacked("w_" + name)
+                continue
             if wdtype == W8A16:
-                codes = torch.empty((N, K), dtype=torch.int8, device=device)
-                scales = torch.empty((N,), dtype=torch.int16, device=device)
-                quantize_weights(W8A16, w32, codes, scales, None, stream=stream)
+                codes = torch.empty((L, N, K), dtype=torch.int8, device=device)
+                scales = torch.empty((L, N), dtype=torch.int16, device=device)
                 zeros = None
             else:
-                codes = torch.empty((N, K // 8), dtype=torch.int32, device=device)
-                scales = torch.empty((N, K // 128), dtype=torch.int16, device=device)
-                zeros = torch.empty((N, K // 128), dtype=torch.int16, device=device)
-                quantize_weights(W4A16, w32, codes, scales, zeros, stream=stream)
-            self._keep += [codes, scales] + ([zeros] if zeros is not None else [])
-            torch.cuda.current_stream().synchronize()
-            del w32
-            L.w, L.scale = codes.data_ptr(), scales.data_ptr()
-            L.zero = zeros.data_ptr() if zeros is not None else None
-            L._tensors = (codes, scales, zeros)
-            return L
+                codes = torch.empty((L, N, K // 8), dtype=torch.int32, device=device)
+                scales = torch.empty((L, N, K // 128), dtype=torch.int16, device=device)
+                zeros = torch.empty((L, N, K // 128), dtype=torch.int16, device=device)
+            for l, lw in enumerate(weights["layers"]):
+                w32 = up(lw["w_" + name], torch.float32)
+                quantize_weights(wdtype, w32, codes[l], scales[l], zeros[l] if zeros is not None else None,
+                                 stream=stream)
+                torch.cuda.current_stream().synchronize()
+                del w32
+            self.tensors["w_" + name] = codes
+            self.tensors["s_" + name] = scales
+            if zeros is not None:
+                self.tensors["z_" + name] = zeros
+        for k in ("tok_emb", "pos_emb", "lnf_g", "lnf_b", "b_head"):
+            self.tensors[k] = up(weights[k])
+        self.tensors["w_head"] = up(weights["w_head"])  # never quantised
 
-        n = shape.n_layer
-        self.layers = (Layer * n)()
-        self.quantised = []
-        for l, lw in enumerate(weights["layers"]):
+        def ptr(key, l):
+            t = self.tensors.get(key)
+            return None if t is None else t[l].data_ptr()
+
+        self.layers = (Layer * L)()
+        for l in range(L):
             Ly = self.layers[l]
-            Ly.ln1_g, Ly.ln1_b = up(lw["ln1_g"]).data_ptr(), up(lw["ln1_b"]).data_ptr()
-            Ly.ln2_g, Ly.ln2_b = up(lw["ln2_g"]).data_ptr(), up(lw["ln2_b"]).data_ptr()
-            lins = {}
-            for name in ("qkv", "out", "fc1", "fc2"):
-                L = linear(lw["w_" + name], lw["b_" + name], True)
-                setattr(Ly, name, L)
-                lins[name] = getattr(L, "_tensors", None)
-            self.quantised.append(lins)
+            Ly.ln1_g, Ly.ln1_b = ptr("ln1_g", l), ptr("ln1_b", l)
+            Ly.ln2_g, Ly.ln2_b = ptr("ln2_g", l), ptr("ln2_b", l)
+            for name in self.LINEARS:
+                setattr(Ly, name, Linear(ptr("w_" + name, l), ptr("s_" + name, l), ptr("z_" + name, l),
+                                         ptr("b_" + name, l)))
         c = Weights()
         c.cfg = self.cfg
-        c.tok_emb = up(weights["tok_emb"]).data_ptr()
-        c.pos_emb = up(weights["pos_emb"]).data_ptr()
+        c.tok_emb = self.tensors["tok_emb"].data_ptr()
+        c.pos_emb = self.tensors["pos_emb"].data_ptr()
         c.layers = self.layers
-        c.lnf_g, c.lnf_b = up(weights["lnf_g"]).data_ptr(), up(weights["lnf_b"]).data_ptr()
-        c.head = linear(weights["w_head"], weights["b_head"], False)
+        c.lnf_g, c.lnf_b = self.tensors["lnf_g"].data_ptr(), self.tensors["lnf_b"].data_ptr()
+        c.head = Linear(self.tensors["w_head"].data_ptr(), None, None, self.tensors["b_head"].data_ptr())
         self.c = c
+
+    def quantised(self, name, l):
+        """(codes, scales, zeros) device tensors of linear `name` in layer l (quantised modes)."""
+        z = self.tensors.get("z_" + name)
+        return self.tensors["w_" + name][l], self.tensors["s_" + name][l], None if z is None else z[l]
 
     def weight_bytes(self) -> int:
         """Bytes of every parameter tensor held on the device."""
-        seen, total = set(), 0
-        for t in self._keep:
-            if t.data_ptr() not in seen:
-                seen.add(t.data_ptr())
-                total += t.numel() * t.element_size()
-        return total
+        return sum(t.numel() * t.element_size() for t in self.tensors.values())
 
 
 class PagePool:

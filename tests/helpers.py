@@ -117,4 +117,4 @@ def run_gpu(dev_model, shape, prefixes, fed, sampling=None, uniforms=None, block
         pt.seq_lens.add_((fed_d[t] >= 0).to(torch.int32))
     torch.cuda.synchronize()
     return {"prefill": last.cpu().numpy(), "logits": logits.cpu().numpy(), "sampled": sampled.cpu().numpy(),
-            "kv": kv, "pt": pt, "lens": lens}
+            "kv": kv, "pt": pt, "lens": lens, "ws": ws}

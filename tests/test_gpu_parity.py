@@ -377,3 +377,80 @@ def test_graph_replay_matches_eager(torch_cuda):
             assert torch.equal(logits, eager_logits[t]), (rep, t)
             _ = (prefix.float() * 2).sum()  # unrelated eager work between replays
         assert torch.equal(hist, eager_hist), rep
+
+
+# ------------------------------------------------------------------------------ persistent step
+# The persistent single-launch step serves the 1280/20x64/5120 shape; two layers
+# keep the oracle fast while exercising every phase (embedding, cross-layer
+# residual exchange, attention over several pages, head, argmax).
+MID = workload.ModelShape(n_layer=2, d_model=1280, n_head=20, d_head=64, d_ff=5120, vocab=1024)
+
+
+@pytest.fixture
+def decode_path():
+    from paper_2607_21042_amd import ftts
+
+    def use(path):
+        ftts.set_decode_path(path)
+    yield use
+    ftts.set_decode_path(ftts.PATH_AUTO)
+
+
+@pytest.fixture(scope="module")
+def mid_master():
+    return workload.master_weights(MID, seed=0)
+
+
+@pytest.mark.parametrize("mode", ["bf16", "w8a16", "w4a16"])
+@pytest.mark.parametrize("B", [1, 2])
+def test_persistent_step_matches_oracle(torch_cuda, decode_path, mid_master, mode, B):
+    from paper_2607_21042_amd import ftts
+    decode_path(ftts.PATH_PERSISTENT)
+    inputs = model_inputs(MID, mode, mid_master)
+    lens = [70, 130][:B]
+    flat = workload.prefix_embeddings(lens, MID.d_model, seed=1)
+    prefixes = np.split(flat, np.cumsum(lens)[:-1])
+    T = 12
+    fed = workload.random_tokens(T, B, MID.vocab, seed=4)
+    fed[0, :] = MID.start_token
+    if B == 2:
+        fed[7:, 0] = -1                           # sequence 0 retires after 7 steps
+    say(f"persistent step {mode} B={B}")
+    dm = ftts.DeviceModel(inputs, MID, wd(mode))
+    res = helpers.run_gpu(dm, MID, prefixes, fed)
+    ftts.check_workspace(res["ws"])
+    om = ogpt.GPT(helpers.oracle_weights(inputs, mode), MID.n_head, MID.d_head, dtype=np.float32)
+    worst, near = compare_run(res, om, prefixes, fed, mode)
+    say(f"  worst abs err {worst:.3g}, near ties {near}")
+    if B == 2:
+        assert np.all(res["sampled"][7:, 0] == -1)
+
+
+def test_persistent_step_agrees_with_kernel_path(torch_cuda, decode_path, mid_master):
+    """Same inputs through both decode implementations: logits agree to fp32
+    reduction-order noise, and the persistent step is independent of where the
+    pages live and bit-reproducible."""
+    from paper_2607_21042_amd import ftts
+    inputs = model_inputs(MID, "bf16", mid_master)
+    lens = [100, 37]
+    flat = workload.prefix_embeddings(lens, MID.d_model, seed=1)
+    prefixes = np.split(flat, np.cumsum(lens)[:-1])
+    T = 10
+    fed = workload.random_tokens(T, 2, MID.vocab, seed=6)
+    fed[0, :] = MID.start_token
+    dm = ftts.DeviceModel(inputs, MID, ftts.BF16)
+    totals = [n + T for n in lens]
+    bt0, n_pages = helpers.make_block_table(totals)
+    bt1, _ = helpers.make_block_table(totals, seed=11)
+    decode_path(ftts.PATH_KERNELS)
+    say("kernel path")
+    rk = helpers.run_gpu(dm, MID, prefixes, fed, block_table=bt0, n_pages=n_pages)
+    decode_path(ftts.PATH_PERSISTENT)
+    say("persistent path")
+    rp = helpers.run_gpu(dm, MID, prefixes, fed, block_table=bt0, n_pages=n_pages)
+    rq = helpers.run_gpu(dm, MID, prefixes, fed, block_table=bt1, n_pages=n_pages)
+    ftts.check_workspace(rq["ws"])
+    scale = np.max(np.abs(rk["logits"]))
+    assert np.max(np.abs(rk["logits"] - rp["logits"])) <= 1e-4 * scale
+    np.testing.assert_array_equal(rp["logits"], rq["logits"])
+    np.testing.assert_array_equal(rp["sampled"], rq["sampled"])
