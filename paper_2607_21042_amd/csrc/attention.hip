@@ -95,16 +95,12 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_kernel(const Attn
             float t = 0.f;
 #pragma unroll
             for (int d = 0; d < 8; ++d) t = fmaf(q[d], kv[d], t);
-            t += __shfl_xor(t, 1, kWave);
-            t += __shfl_xor(t, 2, kWave);
-            t += __shfl_xor(t, 4, kWave);
+            t = group_sum<8>(t);
             const int tok = p * kPage + i * 8 + grp;
             sc[i] = (ok_cur && tok < ctx) ? t : -INFINITY;
             pm = fmaxf(pm, sc[i]);
         }
-        pm = fmaxf(pm, __shfl_xor(pm, 8, kWave));
-        pm = fmaxf(pm, __shfl_xor(pm, 16, kWave));
-        pm = fmaxf(pm, __shfl_xor(pm, 32, kWave));
+        pm = stride8_max(pm);
         if (pm > -INFINITY) {
             const float mn = fmaxf(m, pm);
             const float alpha = expf(m - mn);          // 0 on this wave's first valid page
@@ -138,16 +134,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_kernel(const Attn
     }
     // Sum over the 8 token groups (lanes with equal l % 8 hold the same dims).
 #pragma unroll
-    for (int d = 0; d < 8; ++d) {
-        float t = o[d];
-        t += __shfl_xor(t, 8, kWave);
-        t += __shfl_xor(t, 16, kWave);
-        t += __shfl_xor(t, 32, kWave);
-        o[d] = t;
-    }
-    l += __shfl_xor(l, 8, kWave);
-    l += __shfl_xor(l, 16, kWave);
-    l += __shfl_xor(l, 32, kWave);
+    for (int d = 0; d < 8; ++d) o[d] = stride8_sum(o[d]);
+    l = stride8_sum(l);
     if (lane < 8) {
 #pragma unroll
         for (int d = 0; d < 8; ++d) s_o[w][lane * 8 + d] = o[d];

@@ -3,15 +3,22 @@
 //
 // Why: at batch 1 one step is about 121 dependent phases (5 per layer plus the
 // head) over 0.97 GB of bf16 weights.  Separate kernels pay a launch gap and a
-// cold memory ramp per phase; here one launch covers the whole step and each
-// workgroup holds the next phase's weight share in registers before it waits
-// for that phase's input, so the weight stream overlaps the synchronisation.
+// cold memory ramp per phase; here one launch covers the whole step, and each
+// workgroup's weight share for a phase is already in LDS when that phase's
+// input arrives.
 //
-// Layout: one 512-thread workgroup per CU (256).  Before waiting for a phase's
-// input every thread issues its share of the NEXT phase's weights; the wait
-// (a poll of the exchange words) then overlaps that stream.  A wave's loads
-// retire in issue order, so the poll also waits for the prefetch, which at
-// <= 51 KB per CU lands well within the exchange latency.
+// Layout: one 512-thread workgroup per CU (256).  Waves 0-6 compute; wave 7 only
+// moves weights: it copies each phase's share of a weight matrix into LDS with
+// direct global->LDS loads one or two phases ahead (none while attention runs:
+// the FC1 share goes out once every attention partial is done).  A wave's vector loads
+// retire in issue order, so keeping the weight stream in a wave of its own is
+// what lets the compute waves' polls, parameter loads and KV page loads return
+// without waiting behind it.  The copy wave takes part in every workgroup
+// barrier (it learns the outcome of each poll round from LDS) and, before the
+// barrier that releases a phase's dot products, waits with an explicit vmcnt for
+// the share that phase needs, leaving the next share in flight.
+// Workgroup barriers are bare s_barrier (plus an LDS wait), never __syncthreads,
+// whose memory fence would wait for every outstanding load of the wave.
 //
 // Exchange: every value crossing workgroups travels as one 64-bit word
 // (fp32 value | epoch << 32) written and read with device-coherent (sc1)
@@ -29,7 +36,7 @@
 //   P2  out-proj rows (5 per group) + residual of the group's own x rows
 //   P3  LN2 + FC1 rows (20 per group) + GELU
 //   P4  FC2 rows (5 per group) + residual
-// then LN_f + LM head rows (<= 64 per group) and, for greedy decoding, the
+// then LN_f + LM head rows (<= 40 per group) and, for greedy decoding, the
 // argmax over all groups' candidates.
 #include "gemv_impl.hpp"
 #include "kv_page.hpp"
@@ -37,12 +44,17 @@
 namespace ftts {
 namespace mega {
 
-constexpr int NT = 512;               // threads per workgroup (8 waves)
+constexpr int NT = 512;                    // threads per workgroup (8 waves)
+constexpr int NC = 448;                    // compute threads (waves 0-6)
+constexpr int NWC = NC / 64;               // compute waves
+constexpr int DW = NWC;                    // the copy wave
 constexpr unsigned kSpinLimit = 1u << 19;  // about a second of polling
+constexpr int kBuf = 51200;                // one LDS weight buffer: 20 x 1280 or 5 x 5120 bf16
+constexpr int kHeadRowsMax = 2 * kBuf / (2 * D);  // LM-head rows a group holds (both buffers)
 
-template <int WT> struct Tiles;  // (lanes per row, 16-byte chunks per lane) per phase
+template <int WT> struct Tiles;  // (lanes per row, 16-byte chunks per lane) per phase, <= NC threads
 template <> struct Tiles<FTTS_BF16> {
-    static constexpr int QL = 32, QC = 5, OL = 32, OC = 5, AL = 16, AC = 10, BL = 64, BC = 10;
+    static constexpr int QL = 16, QC = 10, OL = 32, OC = 5, AL = 16, AC = 10, BL = 64, BC = 10;
 };
 template <> struct Tiles<FTTS_W8A16> {
     static constexpr int QL = 16, QC = 5, OL = 16, OC = 5, AL = 16, AC = 5, BL = 64, BC = 5;
@@ -50,7 +62,40 @@ template <> struct Tiles<FTTS_W8A16> {
 template <> struct Tiles<FTTS_W4A16> {
     static constexpr int QL = 8, QC = 5, OL = 8, OC = 5, AL = 8, AC = 5, BL = 32, BC = 5;
 };
-constexpr int HL = 8, HC = 20;        // LM head (bf16): 64 rows per group
+constexpr int HL = 8, HC = 20;  // LM head (bf16)
+
+template <int WT, int K>
+constexpr int row_bytes() { return WT == FTTS_W4A16 ? K / 2 : WT == FTTS_W8A16 ? K : 2 * K; }
+// Direct-to-LDS instructions the copy wave issues for `bytes` (1 KB each).
+constexpr int dma_ops(int bytes) { return (bytes + 1023) / 1024; }
+template <int WT> struct Ops {  // per share, fixed by the shape: rows per group = 15, 5, 20, 5
+    static constexpr int PQ = dma_ops(3 * D / G * row_bytes<WT, D>());
+    static constexpr int PO = dma_ops(D / G * row_bytes<WT, D>());
+    static constexpr int P1 = dma_ops(FF / G * row_bytes<WT, D>());
+    static constexpr int P2 = dma_ops(D / G * row_bytes<WT, FF>());
+    static_assert(PQ <= 63 && PO <= 63 && P1 <= 63 && P2 <= 63, "vmcnt holds 63");
+    static_assert(3 * D / G * row_bytes<WT, D>() <= kBuf && FF / G * row_bytes<WT, D>() <= kBuf &&
+                      D / G * row_bytes<WT, FF>() <= kBuf, "share exceeds an LDS buffer");
+};
+static_assert(3 * D % G == 0 && D % G == 0 && FF % G == 0, "rows split evenly over the groups");
+static_assert(D + NH * kMaxSplit * kPartWords <= FF, "merged o and the attention partials share s_in");
+static_assert(BM * NH * kMaxSplit <= G, "attention groups fit the grid");
+static_assert(BM * NH * kMaxSplit <= kDoneStride && kDoneReplicas + 2 <= 64, "done-word layout");
+
+// Optional phase timeline (built only with FTTS_MEGA_TRACE): thread 0 of each
+// group stamps the 100 MHz wall clock at fixed points of every layer.
+constexpr int kMarksPerLayer = 20, kMarkSlots = 1 + 50 * kMarksPerLayer + 8;
+#ifdef FTTS_MEGA_TRACE
+__device__ unsigned long long g_mega_marks[G][2][kMarkSlots];  // [group][compute wave 0 | copy wave]
+#define MEGA_MARK(slot)                                                                                   \
+    do {                                                                                                  \
+        if ((threadIdx.x & 63) == 0 && threadIdx.x / 64 % 7 == 0)                                          \
+            g_mega_marks[blockIdx.x][threadIdx.x / (64 * 7)][(slot)] = wall_clock64();                     \
+    } while (0)
+#else
+#define MEGA_MARK(slot) ((void)0)
+#endif
+#define MEGA_LMARK(l, e) MEGA_MARK(1 + (l) * kMarksPerLayer + (e))
 
 __device__ __forceinline__ uint32_t ld_agent(const uint32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -63,35 +108,169 @@ __device__ __forceinline__ void put(uint64_t* p, uint32_t epoch, float v) {
                        __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// threadIdx.x as a value the compiler cannot prove loop-invariant: addresses
+// derived from it are formed where they are used instead of being hoisted out
+// of the layer loop and held in registers for the whole step.
+__device__ __forceinline__ int fresh_tid() {
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return t;
+}
+
+// Workgroup barrier that waits only for the wave's own LDS traffic.
+__device__ __forceinline__ void bar() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// Wait until at most N of the wave's vector memory operations are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 typedef __attribute__((address_space(3))) char lds_char;
 
-// Copy `bytes` (a multiple of 16) from global memory to LDS with direct
-// global->LDS loads: each wave moves 1 KB per instruction, no registers held.
-// The LDS buffer must be a multiple of 1 KB long (the last wave instruction may
-// write up to 1 KB - 16 bytes past `bytes`, with a repeat of the last chunk).
-__device__ __forceinline__ void dma_to_lds(const void* src, int bytes, char* dst) {
-    const int n = bytes >> 4;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const char* s = reinterpret_cast<const char*>(src);
+// Copy wave: rows [r0, r0 + nrows) of a row-major matrix (row_b bytes a row,
+// 16-byte aligned) into LDS, 1 KB per instruction.  Lanes past the end repeat
+// the last 16 bytes, so up to 1 KB - 16 bytes past the share are written.
+__device__ __forceinline__ void dma_rows(const void* W, int row_b, int r0, int nrows, char* dst) {
+    const int lane = threadIdx.x & 63;
+    const int n = nrows * row_b >> 4;
+    const char* s = reinterpret_cast<const char*>(W) + (size_t)r0 * row_b;
     lds_char* d = (lds_char*)(dst);
-    for (int c0 = wave * 64; c0 < n; c0 += NT) {
+    for (int c0 = 0; c0 < n; c0 += 64) {
         const int c = min(c0 + lane, n - 1);
         __builtin_amdgcn_global_load_lds(s + (size_t)c * 16, d + c0 * 16, 16, 0, 0);
     }
 }
 
-// One phase's share of a weight matrix: rows [r0, r0 + R), contiguous in memory,
-// copied into an LDS buffer ahead of use; per-row bias and quantisation
-// parameters of this thread's row are kept in registers.
+// Workgroup agreement on a failed wait: a flag in LDS, set by any wave that
+// gave up, read by every wave after the barrier that ends each gather.
+struct Sync {
+    int* fail;
+};
+
+// Compute waves: wait until the n exchange words all carry `epoch` and leave their
+// values in dst (LDS); idx(j) maps value j to its word.  Each wave polls its own
+// words (device-scope relaxed atomic loads) with two rounds in flight -- the next
+// round goes out before the previous one is checked, re-reading only words not
+// yet seen -- so a word is picked up about half a round trip after it lands
+// rather than up to a full one.  The workgroup then meets at one barrier.
+// Returns false when a wave's wait ran out or another group gave up.
+//
+// With sentinels (sent.n > 0, at most 64), wave 0 first polls only those
+// consecutive words (one per producer, stored after its data; each group reads
+// the replica of its own index mod kDoneReplicas, so that the many waiting groups
+// do not all hammer the same few lines), the workgroup meets at a barrier, and
+// then every wave reads its share of the full set.  A group that waits through a
+// long phase thus sends one small request per round instead of many.
+struct NoSentinels {
+    static constexpr int n = 0;
+    const uint64_t* w = nullptr;
+};
+struct Sentinels {
+    const uint64_t* w;  // n consecutive words
+    int n;
+};
+template <int U, typename Idx, typename Sent = NoSentinels>
+__device__ __forceinline__ bool gather(const uint64_t* src, int n, Idx idx, uint32_t epoch, float* dst, uint32_t* ctl,
+                                       Sync& sy, Sent sent = Sent{}, int mark = -1) {
+    const int tid = fresh_tid();
+    bool failed = false;
+    if (sent.n > 0) {
+        if (tid < 64) {
+            const uint64_t* w = sent.w + min(tid, sent.n - 1);
+            unsigned spins = 0;
+            uint64_t a0 = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            while (true) {
+                const uint32_t ab = ld_agent(ctl + 1);
+                const uint64_t a1 = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (__all((uint32_t)(a0 >> 32) == epoch)) break;
+                if (++spins > kSpinLimit || ab != 0) {
+                    failed = true;
+                    break;
+                }
+                a0 = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (__all((uint32_t)(a1 >> 32) == epoch)) break;
+            }
+            if (failed && tid == 0) {
+                *sy.fail = 1;
+                st_agent(ctl + 1, 1u);
+            }
+        }
+        bar();
+        failed = *sy.fail != 0;
+    }
+    for (int base = 0; base < n && !failed; base += NC * U) {
+        uint64_t va[U], vb[U];
+        bool seen[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) seen[u] = false;
+        // Every round reads all U words, so the compiler can wait for one round
+        // while the next is in flight (loads retire in order).
+        auto issue = [&](uint64_t (&v)[U]) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int j = min(base + tid + NC * u, n - 1);
+                v[u] = __hip_atomic_load(src + idx(j), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        };
+        auto take = [&](const uint64_t (&v)[U]) {  // record newly arrived words; true when all have
+            bool all = true;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (!seen[u] && (uint32_t)(v[u] >> 32) == epoch) {
+                    seen[u] = true;
+                    const int j = base + tid + NC * u;
+                    if (j < n) dst[j] = __uint_as_float((uint32_t)v[u]);
+                }
+                all = all && seen[u];
+            }
+            return __all(all);
+        };
+        unsigned spins = 0;
+        issue(va);
+        while (true) {
+            const uint32_t ab = ld_agent(ctl + 1);  // abort word, older than the round issued next
+            issue(vb);
+            if (take(va)) break;
+            if (++spins > kSpinLimit || ab != 0) {
+                failed = true;
+                break;
+            }
+            issue(va);
+            if (take(vb)) break;
+        }
+    }
+    if (mark >= 0) MEGA_MARK(mark + 1);
+    if (failed && (tid & 63) == 0) {
+        *sy.fail = 1;
+        st_agent(ctl + 1, 1u);
+    }
+    bar();
+    return *sy.fail == 0;
+}
+struct Flat {
+    __device__ int operator()(int j) const { return j; }
+};
+
+// Copy wave: the barrier that ends a gather.
+__device__ __forceinline__ bool follow(Sync& sy) {
+    bar();
+    return *sy.fail == 0;
+}
+
+// One phase's share of a weight matrix: rows [r0, r0 + R) in an LDS buffer
+// (copied there by the copy wave); per-row bias and quantisation parameters of
+// this thread's row in registers.
 template <int WT, int LPR, int NCH, int K>
 struct Share {
-    static constexpr int ROW_BYTES = WT == FTTS_W4A16 ? K / 2 : WT == FTTS_W8A16 ? K : 2 * K;
+    static constexpr int ROW_BYTES = row_bytes<WT, K>();
+    static_assert(LPR * NCH * 16 == ROW_BYTES, "tiling must cover a row");
     float s4[NCH], z4[NCH];
     float rs, bias;
     int R;
-    char* buf;
-    __device__ __forceinline__ void issue(const void* W, const void* S, const void* Z, const void* bias_p, int r0,
-                                          int nrows, char* lds) {
+    const char* buf;
+    __device__ __forceinline__ void params(const void* S, const void* Z, const void* bias_p, int r0, int nrows,
+                                           const char* lds) {
         const int li = threadIdx.x & (LPR - 1);
         const int row = r0 + min((int)threadIdx.x / LPR, nrows - 1);
         R = nrows;
@@ -109,14 +288,14 @@ struct Share {
                 z4[i] = bf16_to_f32(reinterpret_cast<const uint16_t*>(Z)[(size_t)row * (K / 128) + g]);
             }
         }
-        dma_to_lds(reinterpret_cast<const char*>(W) + (size_t)r0 * ROW_BYTES, nrows * ROW_BYTES, lds);
     }
     // acc[b] = dot product of this thread's row with s_in[b] (+ bias); every lane of the row gets it.
     template <int B_>
     __device__ __forceinline__ void dot(const float* s_in, const float* s_xs, int B, float (&acc)[B_]) const {
         constexpr int EPC = WInfo<WT>::EPC;
-        const int li = threadIdx.x & (LPR - 1);
-        const int slot = min((int)threadIdx.x / LPR, R - 1);
+        const int t = fresh_tid();
+        const int li = t & (LPR - 1);
+        const int slot = min(t / LPR, R - 1);
         const uint4* wrow = reinterpret_cast<const uint4*>(buf + slot * ROW_BYTES);
 #pragma unroll
         for (int b = 0; b < B_; ++b) acc[b] = 0.f;
@@ -126,224 +305,311 @@ struct Share {
             dot_chunk<WT, B_>(wrow[c], s_in + c * EPC, K, B, acc, s4[i], z4[i], s_xs + c, K / 32);
         }
 #pragma unroll
-        for (int b = 0; b < B_; ++b) {
-            float v = acc[b];
-#pragma unroll
-            for (int o = LPR >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-            acc[b] = fmaf(v, rs, bias);
-        }
+        for (int b = 0; b < B_; ++b) acc[b] = fmaf(group_sum<LPR>(acc[b]), rs, bias);
     }
 };
 
-// The LM head (bf16), streamed straight into registers: 64 rows per group at most.
-template <int LPR, int NCH, int K>
-struct RegShare {
-    uint4 w[NCH];
-    float bias;
-    __device__ __forceinline__ void issue(const void* W, const void* bias_p, int row) {
-        const int li = threadIdx.x & (LPR - 1);
-        bias = bf16_to_f32(reinterpret_cast<const uint16_t*>(bias_p)[row]);
-        const uint4* wr = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(W) + (size_t)2 * K * row);
-#pragma unroll
-        for (int i = 0; i < NCH; ++i) w[i] = ld_stream(wr + li + i * LPR);
-    }
-    template <int B_>
-    __device__ __forceinline__ void dot(const float* s_in, int B, float (&acc)[B_]) const {
-        const int li = threadIdx.x & (LPR - 1);
-#pragma unroll
-        for (int b = 0; b < B_; ++b) acc[b] = 0.f;
-#pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-            const int c = li + i * LPR;
-            dot_chunk<FTTS_BF16, B_>(w[i], s_in + c * 8, K, B, acc, 0.f, 0.f, nullptr, 0);
-        }
-#pragma unroll
-        for (int b = 0; b < B_; ++b) {
-            float v = acc[b];
-#pragma unroll
-            for (int o = LPR >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-            acc[b] = v + bias;
-        }
+// LayerNorm gains of columns 4t .. 4t+3 (thread t < 320), packed bf16.
+struct LnCols {
+    uint2 g, b;
+    __device__ __forceinline__ void load(const void* gp, const void* bp) {
+        const int c = min((int)threadIdx.x, D / 4 - 1);
+        g = reinterpret_cast<const uint2*>(gp)[c];
+        b = reinterpret_cast<const uint2*>(bp)[c];
     }
 };
 
-// Wait until the n words at src all carry `epoch`, then store their values to dst
-// (LDS).  All threads of the workgroup take part and agree on the outcome.  The
-// words are read with device-scope relaxed atomic loads (sc1), which the
-// compiler waits for before their use.  Returns false when the wait ran out or
-// another workgroup gave up.
-__device__ __forceinline__ bool gather(const uint64_t* src, int n, uint32_t epoch, float* dst, uint32_t* ctl) {
-    constexpr int U = 10;
-    const int tid = threadIdx.x;
-    for (int base = 0; base < n; base += NT * U) {
-        uint64_t v[U];
-        unsigned spins = 0;
-        while (true) {
+// LayerNorm of the B rows of s_x into s_in (and, for W4A16, the 32-column sums
+// of the result into s_xs).  Thread t < 320 (waves 0-4) normalises columns
+// 4t .. 4t+3 of every row, so consecutive lanes touch consecutive LDS words;
+// each of those waves forms every row's mean and variance itself, so no
+// barrier is needed until the result is complete.
+template <int BMAX, bool SUMS>
+__device__ __forceinline__ void layer_norm(const float* s_x, float* s_in, float* s_xs, const LnCols& ln, float eps,
+                                           int B) {
+    const int tid = fresh_tid(), lane = tid & 63;
+    if (tid >= D / 4) return;  // whole waves
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int j = min(base + tid + NT * u, n - 1);
-                v[u] = __hip_atomic_load(src + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int b = 0; b < BMAX; ++b) {
+        if (b < B) {
+            const float* x = s_x + b * D;
+            float4 xv[D / 256];
+            float s = 0.f;
+#pragma unroll
+            for (int i = 0; i < D / 256; ++i) {
+                xv[i] = *reinterpret_cast<const float4*>(x + i * 256 + lane * 4);
+                s += (xv[i].x + xv[i].y) + (xv[i].z + xv[i].w);
             }
-            bool ok = true;
+            const float m = wave_sum(s) * (1.0f / (float)D);
+            float q = 0.f;
 #pragma unroll
-            for (int u = 0; u < U; ++u) ok = ok && (uint32_t)(v[u] >> 32) == epoch;
-            if (__syncthreads_and(ok)) break;
-            const bool give_up = ++spins > kSpinLimit || ld_agent(ctl + 1) != 0;
-            if (__syncthreads_or(give_up)) {
-                if (tid == 0) st_agent(ctl + 1, 1u);
-                return false;
+            for (int i = 0; i < D / 256; ++i) {
+                const float d0 = xv[i].x - m, d1 = xv[i].y - m, d2 = xv[i].z - m, d3 = xv[i].w - m;
+                q = fmaf(d0, d0, q);
+                q = fmaf(d1, d1, q);
+                q = fmaf(d2, d2, q);
+                q = fmaf(d3, d3, q);
+            }
+            const float r = 1.0f / sqrtf(wave_sum(q) * (1.0f / (float)D) + eps);
+            const float4 v = *reinterpret_cast<const float4*>(x + tid * 4);
+            float4 y;
+            y.x = fmaf((v.x - m) * r, bf16lo(ln.g.x), bf16lo(ln.b.x));
+            y.y = fmaf((v.y - m) * r, bf16hi(ln.g.x), bf16hi(ln.b.x));
+            y.z = fmaf((v.z - m) * r, bf16lo(ln.g.y), bf16lo(ln.b.y));
+            y.w = fmaf((v.w - m) * r, bf16hi(ln.g.y), bf16hi(ln.b.y));
+            *reinterpret_cast<float4*>(s_in + b * D + tid * 4) = y;
+            if constexpr (SUMS) {
+                const float cs = group_sum<8>((y.x + y.y) + (y.z + y.w));
+                if ((lane & 7) == 0) s_xs[b * (D / 32) + (tid >> 3)] = cs;
             }
         }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int j = base + tid + NT * u;
-            if (j < n) dst[j] = __uint_as_float((uint32_t)v[u]);
-        }
-    }
-    __syncthreads();
-    return true;
-}
-
-// Sum over the workgroup (every thread gets it).
-__device__ __forceinline__ float block_sum(float v, float* red) {
-    v = wave_sum(v);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-    __syncthreads();
-    float t = 0.f;
-#pragma unroll
-    for (int i = 0; i < NT / 64; ++i) t += red[i];
-    __syncthreads();
-    return t;
-}
-
-// LayerNorm of the B rows of src (LDS, width D) into dst; g/b hold this thread's
-// columns tid, tid + 512, ... (preloaded).
-template <int NPER>
-__device__ __forceinline__ void layer_norm_rows(const float* src, float* dst, const float (&g)[NPER],
-                                                const float (&bb)[NPER], float eps, int B, float* red) {
-    const int tid = threadIdx.x;
-    for (int b = 0; b < B; ++b) {
-        const float* x = src + b * D;
-        float xv[NPER];
-        float s = 0.f;
-#pragma unroll
-        for (int i = 0; i < NPER; ++i) {
-            const int k = tid + NT * i;
-            xv[i] = k < D ? x[k] : 0.f;
-            s += xv[i];
-        }
-        const float mean = block_sum(s, red) / (float)D;
-        float var = 0.f;
-#pragma unroll
-        for (int i = 0; i < NPER; ++i) {
-            const int k = tid + NT * i;
-            const float d = k < D ? xv[i] - mean : 0.f;
-            var = fmaf(d, d, var);
-        }
-        var = block_sum(var, red) / (float)D;
-        const float rstd = 1.0f / sqrtf(var + eps);
-#pragma unroll
-        for (int i = 0; i < NPER; ++i) {
-            const int k = tid + NT * i;
-            if (k < D) dst[b * D + k] = (xv[i] - mean) * rstd * g[i] + bb[i];
-        }
-    }
-    __syncthreads();
-}
-
-template <int NPER>
-__device__ __forceinline__ void load_ln(const void* g, const void* bb, float (&gv)[NPER], float (&bv)[NPER]) {
-#pragma unroll
-    for (int i = 0; i < NPER; ++i) {
-        const int k = min((int)threadIdx.x + NT * i, D - 1);
-        gv[i] = bf16_to_f32(reinterpret_cast<const uint16_t*>(g)[k]);
-        bv[i] = bf16_to_f32(reinterpret_cast<const uint16_t*>(bb)[k]);
     }
 }
 
-// Per-32-column sums of the staged activations (W4A16 only).
+// Per-32-column sums of the gathered activations (W4A16 only): eight
+// consecutive lanes hold one chunk's eight float4s.
 __device__ __forceinline__ void chunk_sums(const float* src, float* xs, int K, int B) {
-    const int nc = K / 32;
-    for (int i = threadIdx.x; i < B * nc; i += NT) {
-        const int b = i / nc, c = i - b * nc;
-        const float* p = src + b * K + c * 32;
-        float s = 0.f;
-#pragma unroll
-        for (int j = 0; j < 32; ++j) s += p[j];
-        xs[b * nc + c] = s;
+    const int total = B * K / 4;  // a multiple of 64
+    for (int i = fresh_tid(); i < total; i += NC) {
+        const float4 t = reinterpret_cast<const float4*>(src)[i];
+        const float cs = group_sum<8>((t.x + t.y) + (t.z + t.w));
+        if ((i & 7) == 0) xs[i >> 3] = cs;
     }
-    __syncthreads();
+}
+
+// Online-softmax update of one wave's (m, lsum, o) with one 64-token page of
+// keys and values (page p of the sequence).  Slots at or past ncache, or of an
+// invalid page, may hold anything (NaN included): their scores are replaced by
+// -inf (a select, so a NaN key never reaches the max) and, on a page that has
+// such slots, their values are zeroed first, so 0 * value stays 0.
+__device__ __forceinline__ void attend_page(PageRegs<false>& pg, bool ok, int p, int ncache, const float (&q)[8],
+                                            int grp, float& m, float& lsum, float (&o)[8]) {
+    if (!(ok && (p + 1) * kPage <= ncache)) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            if (!(ok && p * kPage + i * 8 + grp < ncache)) pg.v[i] = make_uint4(0u, 0u, 0u, 0u);
+    }
+    float sc[8];
+    float pm = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float kv[8];
+        unpack8<false>(pg, false, i, kv);
+        float t = 0.f;
+#pragma unroll
+        for (int d = 0; d < 8; ++d) t = fmaf(q[d], kv[d], t);
+        t = group_sum<8>(t);
+        sc[i] = (ok && p * kPage + i * 8 + grp < ncache) ? t : -INFINITY;
+        pm = fmaxf(pm, sc[i]);
+    }
+    pm = stride8_max(pm);
+    if (pm > -INFINITY) {
+        const float mn = fmaxf(m, pm);
+        const float alpha = __expf(m - mn);
+        m = mn;
+        lsum *= alpha;
+#pragma unroll
+        for (int d = 0; d < 8; ++d) o[d] *= alpha;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            float vv[8];
+            unpack8<false>(pg, true, i, vv);
+            const float pr = __expf(sc[i] - m);  // 0 for a left-out slot
+            lsum += pr;
+#pragma unroll
+            for (int d = 0; d < 8; ++d) o[d] = fmaf(pr, vv[d], o[d]);
+        }
+    }
+}
+
+template <int BMAX> constexpr int ux() { return (BMAX * D + NC - 1) / NC; }           // words per thread: x, o
+template <int BMAX> constexpr int uh() { return (BMAX * FF + NC - 1) / NC < 12 ? (BMAX * FF + NC - 1) / NC : 12; }  // h
+template <int BMAX> constexpr int uo() {  // attention partials, S <= kMaxSplit
+    return (BMAX * NH * kMaxSplit * kPartWords + NC - 1) / NC;
+}
+template <int BMAX> constexpr int ua() { return (G * BMAX * 2 + NC - 1) / NC; }        // argmax candidates
+
+// The copy wave's program: every share copy, and the barriers of the compute
+// waves' program in the same order.
+template <int WT, int BMAX>
+__device__ __forceinline__ void copy_wave(const Args& a, char* s_w, Sync& sy) {
+    using O = Ops<WT>;
+    const int wg = blockIdx.x, B = a.B;
+    const int q0 = 3 * D / G * wg, d0 = D / G * wg, f0 = FF / G * wg;
+    const int v0 = a.V * wg / G, nv = a.V * (wg + 1) / G - v0;
+    const int nA = min(nv, kBuf / (2 * D));
+    const bool is_att = wg < B * NH * a.att_split;
+    constexpr bool W4 = WT == FTTS_W4A16;
+    constexpr int RD = row_bytes<WT, D>(), RF = row_bytes<WT, FF>();
+
+    dma_rows(a.qkv_w.at(0), RD, q0, 3 * D / G, s_w);
+    for (int l = 0; l < a.n_layer; ++l) {
+        // P0
+        bar();
+        MEGA_LMARK(l, 0);
+        dma_rows(a.out_w.at(l), RD, d0, D / G, s_w + kBuf);
+        if (l == 0) bar();
+        else if (!follow(sy)) goto out;
+        wait_vm<O::PO>();  // q/k/v share in LDS
+        MEGA_LMARK(l, 1);
+        bar();             // LN1 done
+        // P1: no weight traffic while the attention phase runs (its q/k/v and
+        // output exchanges and KV page reads are the critical path; measured
+        // faster than spreading the FC1 share over the phase)
+        bar();
+        MEGA_LMARK(l, 2);
+        if (is_att) {
+            if (!follow(sy)) goto out;
+            bar();  // wave partials in LDS
+        }
+        // P2
+        bar();  // every partial's done-word seen: attention is over
+        dma_rows(a.fc1_w.at(l), RD, f0, FF / G, s_w);
+        wait_vm<O::P1>();  // out-proj share in LDS
+        MEGA_LMARK(l, 3);
+        if (!follow(sy)) goto out;
+        bar();  // attention partials merged
+        if constexpr (W4) bar();
+        // P3
+        bar();
+        MEGA_LMARK(l, 4);
+        dma_rows(a.fc2_w.at(l), RF, d0, D / G, s_w + kBuf);
+        if (!follow(sy)) goto out;
+        wait_vm<O::P2>();  // FC1 share in LDS
+        MEGA_LMARK(l, 5);
+        bar();             // LN2 done
+        // P4
+        bar();
+        MEGA_LMARK(l, 6);
+        if (l + 1 < a.n_layer) {
+            dma_rows(a.qkv_w.at(l + 1), RD, q0, 3 * D / G, s_w);
+            wait_vm<O::PQ>();  // FC2 share in LDS
+            MEGA_LMARK(l, 7);
+        } else {
+            wait_vm<0>();
+            dma_rows(a.head_w, 2 * D, v0, nA, s_w);
+        }
+        if (!follow(sy)) goto out;
+        if constexpr (W4) bar();
+    }
+    // head
+    bar();
+    if (nv > nA) dma_rows(a.head_w, 2 * D, v0 + nA, nv - nA, s_w + kBuf);
+    if (!follow(sy)) goto out;
+    wait_vm<0>();
+    bar();  // LN_f done
+    if (a.greedy) {
+        bar();  // candidates in LDS
+        if (wg == 0) follow(sy);
+    }
+out:
+    wait_vm<0>();
 }
 
 template <int WT, int BMAX>
 __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
     using T = Tiles<WT>;
-    constexpr int NPER = (D + NT - 1) / NT;
-    constexpr int kBuf = 51200;                                       // largest share: 20 x 1280 or 5 x 5120 bf16
-    __shared__ __attribute__((aligned(1024))) char s_w[2][kBuf];     // weight shares, alternating by phase
+    constexpr bool W4 = WT == FTTS_W4A16;
+    __shared__ __attribute__((aligned(1024))) char s_w[2 * kBuf];     // weight shares, two buffers
     __shared__ __attribute__((aligned(16))) float s_in[BMAX * FF];    // phase input (normalised for LN phases)
     __shared__ __attribute__((aligned(16))) float s_x[BMAX * D];      // residual stream as last gathered
-    __shared__ float s_xs[BMAX * FF / 32];                            // W4A16 chunk sums
-    __shared__ float s_q[3 * 64];                                     // attention: q, k, v of the new token
-    __shared__ float s_pm[8], s_pl[8], s_po[8][64];                   // attention wave partials
-    __shared__ float s_cv[BMAX][64];                                  // head: per-slot best value
-    __shared__ int s_ci[BMAX][64];                                    //       and its row
-    __shared__ int s_active[BMAX];
-    __shared__ float s_red[NT / 64];
+    __shared__ __attribute__((aligned(16))) float s_xs[BMAX * FF / 32];  // W4A16 chunk sums
+    __shared__ __attribute__((aligned(16))) float s_q[3 * 64];        // attention: q, k, v of the new token
+    __shared__ float s_pm[NWC], s_pl[NWC], s_po[NWC][64];             // attention wave partials
+    __shared__ float s_cv[BMAX][NC / HL];                             // head: per-slot best value
+    __shared__ int s_ci[BMAX][NC / HL];                               //       and its row
+    __shared__ int s_active[BMAX], s_tok[BMAX], s_pos[BMAX], s_slot[BMAX], s_phys[BMAX];  // per sequence
+    __shared__ int s_fail;
     __shared__ int s_abort;
 
-    const int wg = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int wg = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int B = a.B;
     const uint32_t step = ld_agent(a.ctl);
     auto E = [&](int ev) { return (step << 8) | (uint32_t)ev; };
     if (tid == 0) s_abort = ld_agent(a.ctl + 1) != 0;
+    if (tid == 0) s_fail = 0;
+    if (tid < B) {  // the sequence's token, position and KV slot; inactive rows produce nothing
+        const int b = tid;
+        const int t = a.tokens[b], p = a.positions[b], s = a.seq_lens[b];
+        bool act = t >= 0 && t < a.V && p >= 0 && p < a.n_pos && s >= 0 && s < a.max_pages * kPage;
+        int phys = -1;
+        if (act) {
+            phys = a.block_table[(size_t)b * a.max_pages + s / kPage];
+            act = phys >= 0 && phys < a.n_pages;
+        }
+        s_active[b] = act;
+        s_tok[b] = t;
+        s_pos[b] = p;
+        s_slot[b] = s;
+        s_phys[b] = phys;
+        if (wg == 0) a.active_out[b] = act;
+    }
     __syncthreads();
     if (s_abort) return;
+    Sync sy{&s_fail};
+    MEGA_MARK(0);
+    if (wave == DW) {
+        copy_wave<WT, BMAX>(a, s_w, sy);
+        return;
+    }
 
-    const int q0 = 3 * D * wg / G, q1 = 3 * D * (wg + 1) / G;
-    const int d0 = D * wg / G, d1 = D * (wg + 1) / G;
-    const int f0 = FF * wg / G, f1 = FF * (wg + 1) / G;
+    const int q0 = 3 * D / G * wg, q1 = q0 + 3 * D / G;
+    const int d0 = D / G * wg, d1 = d0 + D / G;
+    const int f0 = FF / G * wg, f1 = f0 + FF / G;
     const int v0 = a.V * wg / G, v1 = a.V * (wg + 1) / G;
-    const bool is_att = wg < B * NH;
-    const int att_b = wg / NH, att_h = wg % NH;
+    // Attention: S groups per (sequence, head); split s takes the sequence's pages
+    // s, s + S, s + 2S, ..., and its wave w every seventh of those from the w-th.
+    const int S = a.att_split;
+    const bool is_att = wg < B * NH * S;
+    const int att_b = wg / (NH * S), att_h = wg / S % NH, att_s = wg % S;
 
     Share<WT, T::QL, T::QC, D> pq;
     Share<WT, T::OL, T::OC, D> po;
     Share<WT, T::AL, T::AC, D> p1;
     Share<WT, T::BL, T::BC, FF> p2;
     const int sq = tid / T::QL, so = tid / T::OL, s1 = tid / T::AL, s2 = tid / T::BL, sh = tid / HL;
-    float lg[NPER], lb[NPER];
-    // Buffer use: q/k/v and FC1 in s_w[0], out-proj and FC2 in s_w[1]; each DMA
-    // into a buffer is issued after a barrier that follows the buffer's last read.
-    pq.issue(a.qkv_w.at(0), a.qkv_s.at(0), a.qkv_z.at(0), a.qkv_b.at(0), q0, q1 - q0, s_w[0]);
+    LnCols ln;
+    pq.params(a.qkv_s.at(0), a.qkv_z.at(0), a.qkv_b.at(0), q0, q1 - q0, s_w);
+    // Attention groups: the sequence's cached slots (the new token excluded) are
+    // the same in every layer; this wave's pages are wave, wave + 7, ... and lane
+    // j holds the physical id of its j-th (and j+64-th) one.
+    int ncache = 0, my_pages = 0, my_phys0 = -1, my_phys1 = -1;
+    if (is_att && s_active[att_b]) {
+        ncache = s_slot[att_b];
+        const int npg = (ncache + kPage - 1) / kPage;
+        const int nsplit = npg > att_s ? (npg - att_s + S - 1) / S : 0;  // pages of this split
+        const int32_t* bt = a.block_table + (size_t)att_b * a.max_pages;
+        const int lp0 = att_s + S * (wave + NWC * lane), lp1 = att_s + S * (wave + NWC * (lane + 64));
+        my_phys0 = lp0 < npg ? bt[lp0] : -1;
+        my_phys1 = lp1 < npg ? bt[lp1] : -1;
+        my_pages = nsplit > wave ? (nsplit - wave + NWC - 1) / NWC : 0;
+    }
 
     for (int l = 0; l < a.n_layer; ++l) {
         // ---------------- P0: LN1 + q/k/v -------------------------------------------------
-        load_ln<NPER>(a.ln1_g.at(l), a.ln1_b.at(l), lg, lb);
-        po.issue(a.out_w.at(l), a.out_s.at(l), a.out_z.at(l), a.out_b.at(l), d0, d1 - d0, s_w[1]);
+        bar();  // P4's reads of s_w[1], s_in and s_x are done
+        MEGA_LMARK(l, 0);
+        ln.load(a.ln1_g.at(l), a.ln1_b.at(l));
+        po.params(a.out_s.at(l), a.out_z.at(l), a.out_b.at(l), d0, d1 - d0, s_w + kBuf);
         if (l == 0) {  // the embedding, computed locally by every group
             for (int b = 0; b < B; ++b) {
-                const int t = a.tokens[b], p = a.positions[b], s = a.seq_lens[b];
-                bool act = t >= 0 && t < a.V && p >= 0 && p < a.n_pos && s >= 0 && s < a.max_pages * kPage;
-                if (act) {
-                    const int phys = a.block_table[(size_t)b * a.max_pages + s / kPage];
-                    act = phys >= 0 && phys < a.n_pages;
-                }
-                for (int k = tid; k < D; k += NT)
+                const bool act = s_active[b];
+                const int t = s_tok[b], p = s_pos[b];
+                for (int k = tid; k < D; k += NC)
                     s_x[b * D + k] = act ? ld_act<false>(a.tok_emb, (size_t)t * D + k) +
                                                ld_act<false>(a.pos_emb, (size_t)p * D + k)
                                          : 0.f;
-                if (tid == 0) {
-                    s_active[b] = act;
-                    if (wg == 0) a.active_out[b] = act;
-                }
             }
-            __syncthreads();
-        } else if (!gather(a.ex_x, B * D, E(5 * l), s_x, a.ctl)) {
+            bar();
+        } else if (!gather<ux<BMAX>()>(a.ex_x, B * D, Flat{}, E(5 * l), s_x, a.ctl, sy)) {
             return;
         }
-        layer_norm_rows<NPER>(s_x, s_in, lg, lb, a.eps, B, s_red);
-        if constexpr (WT == FTTS_W4A16) chunk_sums(s_in, s_xs, D, B);
+        MEGA_LMARK(l, 1);
+        layer_norm<BMAX, W4>(s_x, s_in, s_xs, ln, a.eps, B);
+        MEGA_LMARK(l, 13);
+        bar();  // s_in complete; the copy wave has waited for the q/k/v share
+        MEGA_LMARK(l, 2);
         {
             float acc[BMAX];
             pq.template dot<BMAX>(s_in, s_xs, B, acc);
@@ -357,10 +623,9 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
                         if (row >= D && s_active[b]) {
                             const int kvsel = row >= 2 * D;
                             const int r = row - D - kvsel * D;
-                            const int slot = a.seq_lens[b];
-                            const int phys = a.block_table[(size_t)b * a.max_pages + slot / kPage];
                             st_act<false>(a.kv,
-                                          kv_offset(l, a.n_pages, phys, kvsel, NH, r / 64, slot % kPage) + r % 64,
+                                          kv_offset(l, a.n_pages, s_phys[b], kvsel, NH, r / 64, s_slot[b] % kPage) +
+                                              r % 64,
                                           acc[b]);
                         }
                     }
@@ -368,36 +633,33 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
             }
         }
         // ---------------- P1: attention, one group per (sequence, head) ---------------------
-        __syncthreads();  // P0's reads of s_w[0] are done
-        p1.issue(a.fc1_w.at(l), a.fc1_s.at(l), a.fc1_z.at(l), a.fc1_b.at(l), f0, f1 - f0, s_w[0]);
+        bar();  // P0's reads of s_w[0] are done
+        MEGA_LMARK(l, 3);
+        p1.params(a.fc1_s.at(l), a.fc1_z.at(l), a.fc1_b.at(l), f0, f1 - f0, s_w);
         if (is_att) {
             const int b = att_b, h = att_h;
-            const int ncache = a.seq_lens[b];                 // cached slots (new token excluded)
-            const int npg = (ncache + kPage - 1) / kPage;
             const int grp = lane >> 3, sub = lane & 7;
-            // this wave's first page goes out before the new token's q/k/v arrive
-            const int lp = wave + 8 * lane;
-            const int my_phys = (s_active[b] && lp < npg) ? a.block_table[(size_t)b * a.max_pages + lp] : -1;
-            const int my_pages = (s_active[b] && npg > wave) ? (npg - wave + 7) / 8 : 0;
-            PageRegs<false> cur;
-            bool ok_cur = false;
             auto bases = [&](int j, size_t& kb, size_t& vb) {
-                int phys = __shfl(my_phys, j, kWave);
+                int phys = j < 64 ? __builtin_amdgcn_readlane(my_phys0, j & 63)
+                                  : __builtin_amdgcn_readlane(my_phys1, j & 63);
                 const bool ok = phys >= 0 && phys < a.n_pages;
                 phys = ok ? phys : 0;
                 kb = kv_offset(l, a.n_pages, phys, 0, NH, h, 0);
                 vb = kv_offset(l, a.n_pages, phys, 1, NH, h, 0);
                 return ok;
             };
+            PageRegs<false> cur;
+            bool ok_cur = false;
             size_t kb, vb;
+            // the first page goes out before the new token's q/k/v arrive
             if (my_pages > 0) {
                 ok_cur = bases(0, kb, vb);
                 load_page<false>(a.kv, kb, vb, lane, cur);
             }
             const uint64_t* src = a.ex_qkv + (size_t)b * 3 * D + h * 64;
-            if (!gather(src, 64, E(5 * l + 1), s_q, a.ctl) || !gather(src + D, 64, E(5 * l + 1), s_q + 64, a.ctl) ||
-                !gather(src + 2 * D, 64, E(5 * l + 1), s_q + 128, a.ctl))
-                return;
+            auto seg = [](int j) { return (j >> 6) * D + (j & 63); };  // q, k, v of head h
+            if (!gather<1>(src, 3 * 64, seg, E(5 * l + 1), s_q, a.ctl, sy)) return;
+            MEGA_LMARK(l, 4);
             float q[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) q[j] = s_q[sub * 8 + j] * 0.125f;  // 1/sqrt(64), exact
@@ -406,76 +668,30 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
             float m = -INFINITY, lsum = 0.f, o[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) o[j] = 0.f;
-            if (wave == 0) {  // the new token itself, straight from the exchange
+            if (att_s == 0 && wave == 0 && s_active[b]) {  // the new token itself, straight from the exchange
                 float t = 0.f;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) t = fmaf(q[j], cached(s_q[64 + sub * 8 + j]), t);
-                t += __shfl_xor(t, 1, kWave);
-                t += __shfl_xor(t, 2, kWave);
-                t += __shfl_xor(t, 4, kWave);
-                m = t;
+                m = group_sum<8>(t);
                 if (grp == 0) {
                     lsum = 1.f;
 #pragma unroll
                     for (int j = 0; j < 8; ++j) o[j] = cached(s_q[128 + sub * 8 + j]);
                 }
             }
+            MEGA_LMARK(l, 14);
             for (int j = 0; j < my_pages; ++j) {
-                const int p = wave + 8 * j;
+                const int p = att_s + S * (wave + NWC * j);
                 if (j > 0) {
                     ok_cur = bases(j, kb, vb);
                     load_page<false>(a.kv, kb, vb, lane, cur);
                 }
-                float sc[8];
-                float pm = -INFINITY;
-#pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    float kv[8];
-                    unpack8<false>(cur, false, i, kv);
-                    float t = 0.f;
-#pragma unroll
-                    for (int d = 0; d < 8; ++d) t = fmaf(q[d], kv[d], t);
-                    t += __shfl_xor(t, 1, kWave);
-                    t += __shfl_xor(t, 2, kWave);
-                    t += __shfl_xor(t, 4, kWave);
-                    const int tok = p * kPage + i * 8 + grp;
-                    sc[i] = (ok_cur && tok < ncache) ? t : -INFINITY;
-                    pm = fmaxf(pm, sc[i]);
-                }
-                pm = fmaxf(pm, __shfl_xor(pm, 8, kWave));
-                pm = fmaxf(pm, __shfl_xor(pm, 16, kWave));
-                pm = fmaxf(pm, __shfl_xor(pm, 32, kWave));
-                if (pm > -INFINITY) {
-                    const float mn = fmaxf(m, pm);
-                    const float alpha = expf(m - mn);
-                    m = mn;
-                    lsum *= alpha;
-#pragma unroll
-                    for (int d = 0; d < 8; ++d) o[d] *= alpha;
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) {
-                        if (sc[i] > -INFINITY) {  // slots past the context never enter the sum
-                            const float pr = expf(sc[i] - m);
-                            float vv[8];
-                            unpack8<false>(cur, true, i, vv);
-                            lsum += pr;
-#pragma unroll
-                            for (int d = 0; d < 8; ++d) o[d] = fmaf(pr, vv[d], o[d]);
-                        }
-                    }
-                }
+                attend_page(cur, ok_cur, p, ncache, q, grp, m, lsum, o);
             }
+            MEGA_LMARK(l, 15);
 #pragma unroll
-            for (int d = 0; d < 8; ++d) {
-                float t = o[d];
-                t += __shfl_xor(t, 8, kWave);
-                t += __shfl_xor(t, 16, kWave);
-                t += __shfl_xor(t, 32, kWave);
-                o[d] = t;
-            }
-            lsum += __shfl_xor(lsum, 8, kWave);
-            lsum += __shfl_xor(lsum, 16, kWave);
-            lsum += __shfl_xor(lsum, 32, kWave);
+            for (int d = 0; d < 8; ++d) o[d] = stride8_sum(o[d]);
+            lsum = stride8_sum(lsum);
             if (lane < 8) {
 #pragma unroll
                 for (int d = 0; d < 8; ++d) s_po[wave][lane * 8 + d] = o[d];
@@ -484,27 +700,65 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
                 s_pm[wave] = m;
                 s_pl[wave] = lsum;
             }
-            __syncthreads();
-            if (tid < 64) {  // log-sum-exp merge of the 8 wave partials
+            MEGA_LMARK(l, 16);
+            bar();
+            MEGA_LMARK(l, 5);
+            if (wave == 0) {  // log-sum-exp merge of the wave partials, published unnormalised
                 float M = -INFINITY;
 #pragma unroll
-                for (int i = 0; i < 8; ++i) M = fmaxf(M, s_pm[i]);
+                for (int i = 0; i < NWC; ++i) M = fmaxf(M, s_pm[i]);
                 float L = 0.f, acc = 0.f;
 #pragma unroll
-                for (int i = 0; i < 8; ++i) {
+                for (int i = 0; i < NWC; ++i) {
                     if (s_pm[i] > -INFINITY) {
                         const float wgt = expf(s_pm[i] - M);
                         L = fmaf(s_pl[i], wgt, L);
-                        acc = fmaf(s_po[i][tid], wgt, acc);
+                        acc = fmaf(s_po[i][lane], wgt, acc);
                     }
                 }
-                put(a.ex_o + (size_t)b * D + h * 64 + tid, E(5 * l + 2), (s_active[b] && L > 0.f) ? acc / L : 0.f);
+                const size_t pi = ((size_t)b * NH + h) * S + att_s;
+                uint64_t* part = a.ex_o + pi * kPartWords;
+                put(part + lane, E(5 * l + 2), acc);
+                if (lane == 0) put(part + 64, E(5 * l + 2), M);
+                if (lane == 1) put(part + 65, E(5 * l + 2), L);
+                if (lane >= 2 && lane < 2 + kDoneReplicas)  // a hint only: the words carry their own epoch
+                    put(a.ex_odone + (lane - 2) * kDoneStride + pi, E(5 * l + 2), 0.f);
             }
         }
         // ---------------- P2: out-proj + residual --------------------------------------------
-        __syncthreads();  // every wave is done reading s_in (P0) before it is overwritten
-        if (!gather(a.ex_o, B * D, E(5 * l + 2), s_in, a.ctl)) return;
-        if constexpr (WT == FTTS_W4A16) chunk_sums(s_in, s_xs, D, B);
+        // (s_in was last read by P0's dot, before P1's barrier)
+        float* s_part = s_in + BMAX * D;  // the S partials of every (sequence, head)
+        // (groups outside attention wait here through the whole attention phase:
+        // they watch the contiguous done-words of up to 64 partials, a few cache
+        // lines, before reading all the partials)
+        if (!gather<uo<BMAX>()>(a.ex_o, B * NH * S * kPartWords, Flat{}, E(5 * l + 2), s_part, a.ctl, sy,
+                                Sentinels{a.ex_odone + (wg % kDoneReplicas) * kDoneStride, min(B * NH * S, 64)},
+                                1 + l * kMarksPerLayer + 17))
+            return;
+        for (int i = tid; i < B * D; i += NC) {  // o = sum_s w_s acc_s / sum_s w_s L_s, w_s = exp(M_s - max M)
+            const int b = i / D, c = i - b * D;
+            const float* pp = s_part + (b * NH + c / 64) * S * kPartWords;
+            float M = -INFINITY;
+            for (int sp = 0; sp < S; ++sp) M = fmaxf(M, pp[sp * kPartWords + 64]);
+            float L = 0.f, acc = 0.f;
+            if (M > -INFINITY) {
+                for (int sp = 0; sp < S; ++sp) {
+                    const float Ms = pp[sp * kPartWords + 64];
+                    if (Ms > -INFINITY) {
+                        const float wgt = expf(Ms - M);
+                        L = fmaf(pp[sp * kPartWords + 65], wgt, L);
+                        acc = fmaf(pp[sp * kPartWords + (c & 63)], wgt, acc);
+                    }
+                }
+            }
+            s_in[i] = (s_active[b] && L > 0.f) ? acc / L : 0.f;
+        }
+        bar();
+        MEGA_LMARK(l, 6);
+        if constexpr (W4) {
+            chunk_sums(s_in, s_xs, D, B);
+            bar();
+        }
         {
             float acc[BMAX];
             po.template dot<BMAX>(s_in, s_xs, B, acc);
@@ -517,12 +771,15 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
             }
         }
         // ---------------- P3: LN2 + FC1 + GELU -----------------------------------------------
-        __syncthreads();  // every wave is done reading s_in / s_x / s_w[1] of P2
-        load_ln<NPER>(a.ln2_g.at(l), a.ln2_b.at(l), lg, lb);
-        p2.issue(a.fc2_w.at(l), a.fc2_s.at(l), a.fc2_z.at(l), a.fc2_b.at(l), d0, d1 - d0, s_w[1]);
-        if (!gather(a.ex_x, B * D, E(5 * l + 3), s_x, a.ctl)) return;
-        layer_norm_rows<NPER>(s_x, s_in, lg, lb, a.eps, B, s_red);
-        if constexpr (WT == FTTS_W4A16) chunk_sums(s_in, s_xs, D, B);
+        bar();  // P2's reads of s_in / s_x / s_w[1] are done
+        MEGA_LMARK(l, 7);
+        ln.load(a.ln2_g.at(l), a.ln2_b.at(l));
+        p2.params(a.fc2_s.at(l), a.fc2_z.at(l), a.fc2_b.at(l), d0, d1 - d0, s_w + kBuf);
+        if (!gather<ux<BMAX>()>(a.ex_x, B * D, Flat{}, E(5 * l + 3), s_x, a.ctl, sy)) return;
+        MEGA_LMARK(l, 8);
+        layer_norm<BMAX, W4>(s_x, s_in, s_xs, ln, a.eps, B);
+        bar();  // s_in complete; the copy wave has waited for the FC1 share
+        MEGA_LMARK(l, 9);
         {
             float acc[BMAX];
             p1.template dot<BMAX>(s_in, s_xs, B, acc);
@@ -535,11 +792,16 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
             }
         }
         // ---------------- P4: FC2 + residual -------------------------------------------------
-        __syncthreads();  // every wave is done reading s_in / s_w[0] of P3
+        bar();  // P3's reads of s_in / s_w[0] are done
+        MEGA_LMARK(l, 10);
         if (l + 1 < a.n_layer)
-            pq.issue(a.qkv_w.at(l + 1), a.qkv_s.at(l + 1), a.qkv_z.at(l + 1), a.qkv_b.at(l + 1), q0, q1 - q0, s_w[0]);
-        if (!gather(a.ex_h, B * FF, E(5 * l + 4), s_in, a.ctl)) return;
-        if constexpr (WT == FTTS_W4A16) chunk_sums(s_in, s_xs, FF, B);
+            pq.params(a.qkv_s.at(l + 1), a.qkv_z.at(l + 1), a.qkv_b.at(l + 1), q0, q1 - q0, s_w);
+        if (!gather<uh<BMAX>()>(a.ex_h, B * FF, Flat{}, E(5 * l + 4), s_in, a.ctl, sy)) return;
+        MEGA_LMARK(l, 11);
+        if constexpr (W4) {
+            chunk_sums(s_in, s_xs, FF, B);
+            bar();
+        }
         {
             float acc[BMAX];
             p2.template dot<BMAX>(s_in, s_xs, B, acc);
@@ -551,19 +813,22 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
                     if (b < B && li == b) put(a.ex_x + (size_t)b * D + row, E(5 * l + 5), s_x[b * D + row] + acc[b]);
             }
         }
-        __syncthreads();  // s_in / s_x free for the next layer
+        MEGA_LMARK(l, 12);
     }
 
     // ---------------- LN_f + LM head (+ greedy argmax) -------------------------------------
-    // (the head's weights stream while the last FC2 outputs are gathered)
-    RegShare<HL, HC, D> ph;
-    ph.issue(a.head_w, a.head_b, v0 + min(sh, v1 - v0 - 1));
-    load_ln<NPER>(a.lnf_g, a.lnf_b, lg, lb);
-    if (!gather(a.ex_x, B * D, E(5 * a.n_layer), s_x, a.ctl)) return;
-    layer_norm_rows<NPER>(s_x, s_in, lg, lb, a.eps, B, s_red);
+    bar();  // the last FC2's reads of s_w[1] / s_in / s_x are done
+    Share<FTTS_BF16, HL, HC, D> ph;
+    ph.params(nullptr, nullptr, a.head_b, v0, v1 - v0, s_w);
+    ln.load(a.lnf_g, a.lnf_b);
+    if (!gather<ux<BMAX>()>(a.ex_x, B * D, Flat{}, E(5 * a.n_layer), s_x, a.ctl, sy)) return;
+    MEGA_MARK(1 + a.n_layer * kMarksPerLayer);
+    layer_norm<BMAX, false>(s_x, s_in, s_xs, ln, a.eps, B);
+    bar();  // s_in complete; the copy wave has waited for the head share
+    MEGA_MARK(2 + a.n_layer * kMarksPerLayer);
     {
         float acc[BMAX];
-        ph.template dot<BMAX>(s_in, B, acc);
+        ph.template dot<BMAX>(s_in, s_xs, B, acc);
         const int row = v0 + sh;
         const int li = tid & (HL - 1);
         const bool mine = sh < v1 - v0;
@@ -580,11 +845,11 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         if (wg == 0 && tid == 0) st_agent(a.ctl, step + 1);
         return;
     }
-    __syncthreads();
+    bar();
     if (tid < B) {  // this group's best row for each sequence
         float bv = -INFINITY;
         int bi = 0x7FFFFFFF;
-        for (int s = 0; s < NT / HL; ++s) {
+        for (int s = 0; s < NC / HL; ++s) {
             const float v = s_cv[tid][s];
             const int i = s_ci[tid][s];
             if (v > bv || (v == bv && i < bi)) {
@@ -596,7 +861,7 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         put(a.ex_arg + ((size_t)wg * B + tid) * 2 + 1, E(5 * a.n_layer + 1), __int_as_float(bi));
     }
     if (wg != 0) return;
-    if (!gather(a.ex_arg, G * B * 2, E(5 * a.n_layer + 1), s_in, a.ctl)) return;
+    if (!gather<ua<BMAX>()>(a.ex_arg, G * B * 2, Flat{}, E(5 * a.n_layer + 1), s_in, a.ctl, sy)) return;
     if (wave < B) {
         const int b = wave;
         float bv = -INFINITY;
@@ -620,10 +885,18 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         }
         if (lane == 0) a.sampled[b] = s_active[b] ? (bi < a.V ? bi : 0) : -1;
     }
+    MEGA_MARK(3 + a.n_layer * kMarksPerLayer);
     if (tid == 0) st_agent(a.ctl, step + 1);
 }
 
 }  // namespace mega
+
+#ifdef FTTS_MEGA_TRACE
+extern "C" int ftts_mega_trace_read(void* host, size_t bytes) {
+    if (bytes < sizeof(mega::g_mega_marks)) return -1;
+    return hipMemcpyFromSymbol(host, HIP_SYMBOL(mega::g_mega_marks), sizeof(mega::g_mega_marks)) == hipSuccess ? 0 : -1;
+}
+#endif
 
 hipError_t launch_decode_mega(int wdtype, const mega::Args& a, hipStream_t st) {
     using namespace mega;

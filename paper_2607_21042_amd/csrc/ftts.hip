@@ -1,6 +1,7 @@
 // C ABI entry points of libftts: argument validation, workspace carving and the
 // order of kernel launches for prefill and for one decode step.  Every check
 // happens before the first enqueue, so a rejected call has no side effects.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -151,7 +152,7 @@ struct PrefillWs {
 // with different batch sizes agree on where they are.
 struct MegaWs {
     uint32_t* ctl;
-    uint64_t *x, *qkv, *o, *h, *arg;
+    uint64_t *x, *qkv, *o, *h, *arg, *odone;
 };
 
 size_t mega_bytes(MegaWs* out, char* base) {
@@ -161,10 +162,13 @@ size_t mega_bytes(MegaWs* out, char* base) {
     char* ctl = take(256);
     char* x = take((size_t)BM * D * 8);
     char* qkv = take((size_t)BM * 3 * D * 8);
-    char* o = take((size_t)BM * D * 8);
+    char* o = take((size_t)BM * NH * kMaxSplit * kPartWords * 8);
     char* h = take((size_t)BM * FF * 8);
     char* arg = take((size_t)G * BM * 2 * 8);
-    if (out) *out = MegaWs{(uint32_t*)ctl, (uint64_t*)x, (uint64_t*)qkv, (uint64_t*)o, (uint64_t*)h, (uint64_t*)arg};
+    char* odone = take((size_t)kDoneReplicas * kDoneStride * 8);
+    if (out)
+        *out = MegaWs{(uint32_t*)ctl, (uint64_t*)x, (uint64_t*)qkv, (uint64_t*)o, (uint64_t*)h, (uint64_t*)arg,
+                      (uint64_t*)odone};
     return off;
 }
 
@@ -224,7 +228,8 @@ bool mega_args(const ftts_weights* w, int B, mega::Args* a) {
     const ftts_config& c = w->cfg;
     using namespace ftts::mega;
     if (c.wdtype == FTTS_F32 || c.d_model != D || c.d_ff != FF || c.n_head != NH) return false;
-    if (B < 1 || B > BM || c.n_layer > 50 || c.vocab < G || c.vocab > G * 64) return false;
+    // LM-head rows per group must fit the two 50 KB LDS weight buffers (40 rows of 1280 bf16).
+    if (B < 1 || B > BM || c.n_layer > 50 || c.vocab < G || c.vocab > G * 40) return false;
     if (device_cus() != G) return false;
     bool ok = true;
     ok &= stride_of(w, [](const ftts_layer& L) { return L.ln1_g; }, &a->ln1_g);
@@ -238,6 +243,12 @@ bool mega_args(const ftts_weights* w, int B, mega::Args* a) {
     ok &= stride_of(w, [](const ftts_layer& L) { return L.NAME.bias; }, &a->NAME##_b);
     FTTS_LIN(qkv) FTTS_LIN(out) FTTS_LIN(fc1) FTTS_LIN(fc2)
 #undef FTTS_LIN
+    if (!ok) return false;
+    // Weight shares are copied to LDS 16 bytes at a time; LayerNorm gains are read 16 bytes at a time.
+    auto al16 = [](const Strided& t) { return ((uintptr_t)t.p % 16) == 0 && (t.s % 16) == 0; };
+    ok &= al16(a->qkv_w) && al16(a->out_w) && al16(a->fc1_w) && al16(a->fc2_w);
+    ok &= al16(a->ln1_g) && al16(a->ln1_b) && al16(a->ln2_g) && al16(a->ln2_b);
+    ok &= (uintptr_t)w->head.w % 16 == 0 && (uintptr_t)w->lnf_g % 16 == 0 && (uintptr_t)w->lnf_b % 16 == 0;
     if (!ok) return false;
     a->n_layer = c.n_layer;
     a->V = c.vocab;
@@ -382,6 +393,9 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
         MegaWs M;
         mega_bytes(&M, reinterpret_cast<char*>(ws));
         ma.max_pages = pt->max_pages;
+        // Enough workgroups per (sequence, head) that each of a group's seven
+        // attention waves holds at most one page, as far as kMaxSplit allows.
+        ma.att_split = std::min(mega::kMaxSplit, std::max(1, (pt->max_pages + 6) / 7));
         ma.n_pages = kv->n_pages;
         ma.greedy = samp->top_k == 1;
         ma.tokens = tokens;
@@ -397,6 +411,7 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
         ma.ex_o = M.o;
         ma.ex_h = M.h;
         ma.ex_arg = M.arg;
+        ma.ex_odone = M.odone;
         ma.ctl = M.ctl;
         (void)hipGetLastError();
         hipError_t e = launch_decode_mega(c.wdtype, ma, st);

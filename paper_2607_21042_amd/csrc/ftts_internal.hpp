@@ -20,12 +20,13 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_floa
 __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// Round to nearest bf16, ties to even (finite inputs; NaN stays NaN).
+// Round to nearest bf16, ties to even (NaN stays NaN, quietened).  Branch-free,
+// so a run of conversions stays one straight line of VALU selects.
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x7FFFFFu)) return (uint16_t)((u >> 16) | 0x40);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+    const uint32_t u = __float_as_uint(f);
+    const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+    const bool nan = (u & 0x7FFFFFFFu) > 0x7F800000u;
+    return (uint16_t)(nan ? ((u >> 16) | 0x40u) : r);
 }
 
 // 16-byte streaming load (weights are read once per call; the hint keeps them from
@@ -53,19 +54,67 @@ __device__ __forceinline__ void st_act(void* p, size_t i, float v) {
     else reinterpret_cast<uint16_t*>(p)[i] = f32_to_bf16(v);
 }
 
-// ---- reductions -------------------------------------------------------------------
+// ---- cross-lane reductions ----------------------------------------------------------
+// Built from DPP lane moves within 16-lane rows and the gfx950 row swaps
+// (v_permlane16_swap / v_permlane32_swap), which stay in the VALU instead of
+// going through the LDS crossbar as ds_bpermute does.  Every lane of a group
+// ends with the same bits (each step adds a pair in both orders, and fp32
+// addition is commutative).  The whole wave must be active.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppQuadSwap1 = 0xB1;      // quad_perm [1,0,3,2]
+constexpr int kDppQuadSwap2 = 0x4E;      // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;    // lane i <-> 7 - i within each 8
+constexpr int kDppMirror = 0x140;        // lane i <-> 15 - i within each 16
+constexpr int kDppRor8 = 0x128;          // lane i <- (i + 8) mod 16 within each 16
+struct RowPair { float a, b; };
+__device__ __forceinline__ RowPair swap16(float v) {  // a: own row pair's even row, b: its odd row
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+__device__ __forceinline__ RowPair swap32(float v) {  // a: lanes 0-31 value, b: lanes 32-63 value
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+
+// Sum / max over aligned groups of W consecutive lanes (W a power of two <= 64).
 template <int W>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-    for (int o = W / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    if constexpr (W >= 2) v += dpp_mov<kDppQuadSwap1>(v);
+    if constexpr (W >= 4) v += dpp_mov<kDppQuadSwap2>(v);
+    if constexpr (W >= 8) v += dpp_mov<kDppHalfMirror>(v);
+    if constexpr (W >= 16) v += dpp_mov<kDppMirror>(v);
+    if constexpr (W >= 32) { const RowPair p = swap16(v); v = p.a + p.b; }
+    if constexpr (W >= 64) { const RowPair p = swap32(v); v = p.a + p.b; }
+    return v;
+}
+template <int W>
+__device__ __forceinline__ float group_max(float v) {
+    if constexpr (W >= 2) v = fmaxf(v, dpp_mov<kDppQuadSwap1>(v));
+    if constexpr (W >= 4) v = fmaxf(v, dpp_mov<kDppQuadSwap2>(v));
+    if constexpr (W >= 8) v = fmaxf(v, dpp_mov<kDppHalfMirror>(v));
+    if constexpr (W >= 16) v = fmaxf(v, dpp_mov<kDppMirror>(v));
+    if constexpr (W >= 32) { const RowPair p = swap16(v); v = fmaxf(p.a, p.b); }
+    if constexpr (W >= 64) { const RowPair p = swap32(v); v = fmaxf(p.a, p.b); }
+    return v;
+}
+// Sum / max over the 8 lanes sharing lane % 8 (lanes i, i + 8, ..., i + 56).
+__device__ __forceinline__ float stride8_sum(float v) {
+    v += dpp_mov<kDppRor8>(v);
+    { const RowPair p = swap16(v); v = p.a + p.b; }
+    { const RowPair p = swap32(v); v = p.a + p.b; }
+    return v;
+}
+__device__ __forceinline__ float stride8_max(float v) {
+    v = fmaxf(v, dpp_mov<kDppRor8>(v));
+    { const RowPair p = swap16(v); v = fmaxf(p.a, p.b); }
+    { const RowPair p = swap32(v); v = fmaxf(p.a, p.b); }
     return v;
 }
 __device__ __forceinline__ float wave_sum(float v) { return group_sum<kWave>(v); }
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-    return v;
-}
+__device__ __forceinline__ float wave_max(float v) { return group_max<kWave>(v); }
 
 // GPT-2 tanh GELU.
 __device__ __forceinline__ float gelu_tanh(float u) {
@@ -178,8 +227,13 @@ namespace mega {
 constexpr int D = 1280, FF = 5120, NH = 20;
 constexpr int G = 256;   // workgroups of the persistent decode step, one per CU
 constexpr int BM = 2;    // largest batch it takes
+constexpr int kMaxSplit = 2;   // workgroups per (sequence, head) in attention
+constexpr int kPartWords = 66;  // one attention partial: 64 unnormalised sums, max score, weight sum
+constexpr int kDoneReplicas = 8;   // copies of the attention done-words (one read per group index mod 8)
+constexpr int kDoneStride = 512;   // words between copies (4 KB)
 struct Args {
     int n_layer, V, n_pos, B, max_pages, n_pages, greedy;
+    int att_split;  // S: workgroups per (sequence, head), 1..kMaxSplit
     float eps;
     Strided ln1_g, ln1_b, ln2_g, ln2_b;
     Strided qkv_w, qkv_s, qkv_z, qkv_b, out_w, out_s, out_z, out_b;
@@ -191,6 +245,7 @@ struct Args {
     int32_t* sampled;
     int32_t* active_out;
     uint64_t *ex_x, *ex_qkv, *ex_o, *ex_h, *ex_arg;
+    uint64_t* ex_odone;  // one word per attention partial, written after it
     uint32_t* ctl;  // [0] step counter, [1] abort
 };
 

@@ -254,10 +254,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvArgs a) {
 #pragma unroll
     for (int b = 0; b < BMAX; ++b) {
         if (b < B) {
-            float v = acc[b];
-#pragma unroll
-            for (int o = LPR >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-            acc[b] = v;
+            acc[b] = group_sum<LPR>(acc[b]);
         }
     }
     if (!row_ok) return;

@@ -426,6 +426,29 @@ def test_persistent_step_matches_oracle(torch_cuda, decode_path, mid_master, mod
         assert np.all(res["sampled"][7:, 0] == -1)
 
 
+@pytest.mark.parametrize("mode,lens", [("bf16", [900]), ("bf16", [600, 900]), ("w4a16", [600, 900])])
+def test_persistent_step_split_attention(torch_cuda, decode_path, mid_master, mode, lens):
+    """Contexts long enough that each (sequence, head) is attended by two
+    workgroups, some of whose waves take two pages: the out-projection groups
+    merge the two partial softmax states."""
+    from paper_2607_21042_amd import ftts
+    decode_path(ftts.PATH_PERSISTENT)
+    inputs = model_inputs(MID, mode, mid_master)
+    B = len(lens)
+    flat = workload.prefix_embeddings(lens, MID.d_model, seed=1)
+    prefixes = np.split(flat, np.cumsum(lens)[:-1])
+    T = 6
+    fed = workload.random_tokens(T, B, MID.vocab, seed=4)
+    fed[0, :] = MID.start_token
+    say(f"persistent split attention {mode} lens={lens}")
+    dm = ftts.DeviceModel(inputs, MID, wd(mode))
+    res = helpers.run_gpu(dm, MID, prefixes, fed)
+    ftts.check_workspace(res["ws"])
+    om = ogpt.GPT(helpers.oracle_weights(inputs, mode), MID.n_head, MID.d_head, dtype=np.float32)
+    worst, near = compare_run(res, om, prefixes, fed, mode)
+    say(f"  worst abs err {worst:.3g}, near ties {near}")
+
+
 def test_persistent_step_agrees_with_kernel_path(torch_cuda, decode_path, mid_master):
     """Same inputs through both decode implementations: logits agree to fp32
     reduction-order noise, and the persistent step is independent of where the
