@@ -6,12 +6,22 @@ prefix, then `--decode` greedy decode steps for every sequence of the batch,
 each step's sampled ids fed straight back as the next step's tokens (device to
 device, no host round trip).  Inputs are seeded synthetic tensors resident in
 HBM before timing starts.  The JSON line reports generated tokens per second
-over the whole job, the HBM roofline of the decode step, and the CPU oracle's
-rate on a bounded sample of the same workload.
+over the whole job, the HBM roofline of the decode step's dominant kernel, and
+the CPU oracle's rate on a bounded sample of the same workload.
+
+Roofline: when the persistent single-launch step serves the batch, that kernel
+is the whole decode step and is timed per launch with HIP events on the stream
+it runs on; otherwise the step (several kernels, replayed from a HIP graph) is
+timed per replay.  `achieved` is the algorithmic bytes of a step divided by
+that time.  `traffic` is the HBM bytes per launch measured by rocprofv3
+counters (stored next to the kernel-trace summaries under profiles/), reported
+only for the workload they were taken on and only while the kernel sources
+are unchanged since.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -25,6 +35,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "GPT decode tokens/s on 1 MI355X at batch 1 & 32; achieved HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0
+COUNTERS = os.path.join(ROOT, "profiles", "decode_mega_counters.json")
 
 
 def parse():
@@ -37,9 +48,48 @@ def parse():
     p.add_argument("--prefix", type=int, default=256)
     p.add_argument("--decode", type=int, default=512)
     p.add_argument("--cpu-steps", type=int, default=16, help="decode steps timed for the CPU oracle baseline")
-    p.add_argument("--graph-steps", type=int, default=32, help="decode steps captured per HIP graph")
+    p.add_argument("--graph-steps", type=int, default=32, help="decode steps per HIP graph (kernel-per-phase path)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only run a plain device copy of known size (scales the rocprofv3 byte counters)")
     return p.parse_args()
+
+
+def copy_calibration():
+    """Four plain device-to-device copies of 256 MiB each, one kernel apiece:
+    a counter run over this gives FETCH_SIZE / WRITE_SIZE for known traffic."""
+    import torch
+    n = 256 << 20
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(4):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": {"bytes_read_per_copy": n, "bytes_written_per_copy": n, "copies": 4}}))
+
+
+def kernel_sources_sha() -> str:
+    """Hash of the sources the persistent decode kernel is built from."""
+    csrc = os.path.join(ROOT, "paper_2607_21042_amd", "csrc")
+    h = hashlib.sha256()
+    for f in ("decode_mega.hip", "ftts_internal.hpp", "gemv_impl.hpp", "kv_page.hpp"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(ROOT, "include", "ftts.h"), "rb") as fh:
+        h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed counter runs, if they apply."""
+    try:
+        with open(COUNTERS) as fh:
+            c = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if c.get("workload") != workload or c.get("source_sha256") != kernel_sources_sha():
+        return None
+    return c.get("hbm_bytes_per_launch")
 
 
 def algorithmic_step_bytes(shape, dm, B, ctx_lens, kv_elem):
@@ -80,6 +130,9 @@ def cpu_baseline(inputs, shape, mode, prefix, n_steps):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1",
                           "n_gpus": args.gpus}))
@@ -124,6 +177,7 @@ def main():
     pt = ftts.PageTableView(bt, seq_lens)
     pt.seq_lens = seq_lens  # keep the same storage: the graph reads these pointers
     pt.c = ftts.PageTable(bt.data_ptr(), seq_lens.data_ptr(), max_pages)
+    persistent = ftts.decode_path(dm, B) == 2
 
     def reset():
         tokens.fill_(shape.start_token)
@@ -131,38 +185,56 @@ def main():
         seq_lens.fill_(P)
         counter.zero_()
 
-    def one_step():
+    def step_kernel():
         ftts.decode_step(dm, tokens, positions, pt, kv, logits, sampled, None, greedy, ws)
+
+    def step_advance():
         ftts.advance(tokens, positions, seq_lens, sampled, None, shape.stop_token, history, counter)
 
-    S = args.graph_steps if T % args.graph_steps == 0 else 1
     stream = torch.cuda.current_stream()
-    # eager warm-up (sets kernel attributes), then capture S steps into one graph
+    S = 1
+    graph = None
     reset()
     ftts.prefill(dm, prefix, [P] * B, pt, kv, last, ws)
     for _ in range(2):
-        one_step()
+        step_kernel()
+        step_advance()
     torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        for _ in range(S):
-            one_step()
-    torch.cuda.synchronize()
+    if not persistent:
+        # several kernels per step: capture S steps into one graph
+        S = args.graph_steps if T % args.graph_steps == 0 else 1
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(S):
+                step_kernel()
+                step_advance()
+        torch.cuda.synchronize()
 
-    def job(ev=None):
+    def job(evs=None):
         reset()
         ftts.prefill(dm, prefix, [P] * B, pt, kv, last, ws)
-        if ev is not None:
-            ev[0].record(stream)
-        for _ in range(T // S):
-            graph.replay()
-        if ev is not None:
-            ev[1].record(stream)
+        if persistent:
+            for t in range(T):
+                if evs is not None:
+                    evs[t][0].record(stream)
+                step_kernel()
+                if evs is not None:
+                    evs[t][1].record(stream)
+                step_advance()
+        else:
+            for r in range(T // S):
+                if evs is not None:
+                    evs[r][0].record(stream)
+                graph.replay()
+                if evs is not None:
+                    evs[r][1].record(stream)
 
     for _ in range(args.warmup):
         job()
     torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    n_units = T if persistent else T // S
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_units)]
+           for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -173,30 +245,40 @@ def main():
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
+    if persistent:
+        ftts.check_workspace(ws)
     total_ms = t_start.elapsed_time(t_end)
-    decode_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
     job_ms = total_ms / args.steps
-    tokens_per_job = B * T
-    value = tokens_per_job / (job_ms / 1e3)
+    value = B * T / (job_ms / 1e3)
 
     kv_elem = 4 if mode == "f32" else 2
-    step_bytes = [algorithmic_step_bytes(shape, dm, B, [P + t] * B, kv_elem) for t in range(T)]
-    per_step_s = decode_ms / 1e3 / T
-    achieved = (sum(step_bytes) / T) / per_step_s / 1e9
+    step_bytes = np.array([algorithmic_step_bytes(shape, dm, B, [P + t] * B, kv_elem) for t in range(T)], np.float64)
+    unit_ms = np.array([[a.elapsed_time(b) for a, b in row] for row in evs], np.float64)  # [steps][units]
+    if persistent:
+        unit_bytes = step_bytes
+        kernel = "decode_mega_kernel (persistent single-launch decode step)"
+    else:
+        unit_bytes = step_bytes.reshape(T // S, S).sum(axis=1)
+        kernel = f"decode step, kernel per phase ({S} steps per graph replay)"
+    launch_us = float(unit_ms.mean() * 1e3)
+    achieved = float(unit_bytes.sum() * args.steps / (unit_ms.sum() / 1e3) / 1e9)
+    decode_ms = float(unit_ms.sum(axis=1).mean())
+    workload_name = f"indextts2-gpt {mode} batch={B} prefix={P} greedy decode={T}"
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(job_ms, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": {"f32": "f32", "bf16": "bf16", "w8a16": "int8-w/bf16", "w4a16": "int4-w/bf16"}[mode],
         "data": "synthetic: seeded random-init IndexTTS-2-shaped GPT (24x1280, 20 heads, FFN 5120, vocab 8194)",
-        "config": {"workload": f"indextts2-gpt {mode} batch={B} prefix={P} greedy decode={T}", "batch": B,
-                   "prefix": P, "decode_tokens": T, "weights": mode, "graph_steps": S},
+        "config": {"workload": workload_name, "batch": B, "prefix": P, "decode_tokens": T, "weights": mode,
+                   "decode_path": "persistent" if persistent else "kernel-per-phase"},
         "decode_ms_per_token_step": round(decode_ms / T, 4),
         "prefill_ms": round(job_ms - decode_ms, 3),
         "wall_s": round(wall, 3),
-        "roofline": {"bound": "hbm", "kernel": "decode step (all kernels of one ftts_decode_step)",
-                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "algorithmic_bytes_per_step": int(sum(step_bytes) / T), "traffic": None},
+        "roofline": {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "launch_us": round(launch_us, 2),
+                     "algorithmic_bytes_per_launch": int(unit_bytes.mean()),
+                     "traffic": measured_traffic(workload_name) if persistent else None},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(inputs, shape, mode, prefix_np[:P], args.cpu_steps)

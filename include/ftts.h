@@ -168,11 +168,19 @@ const char* ftts_version(void);
 
 /* Decode implementation for later ftts_decode_step calls of this process:
  * 0 automatic (the persistent single-launch step when the model and batch
- * qualify -- d_model 1280, 20 heads, d_ff 5120, 256 <= vocab <= 16384, at most
+ * qualify -- d_model 1280, 20 heads, d_ff 5120, 256 <= vocab <= 10240, at most
  * 50 layers, 16-bit or quantised weights, batch <= 2, per-layer tensors of each
- * kind at a fixed stride, a 256-CU device -- otherwise one kernel per phase), 1 always one kernel per phase, 2 always
- * the persistent step (calls that do not qualify return FTTS_E_UNSUPPORTED). */
+ * kind at a fixed stride, weight matrices and LayerNorm vectors 16-byte aligned,
+ * a 256-CU device -- otherwise one kernel per phase), 1 always one kernel per
+ * phase, 2 always the persistent step (calls that do not qualify return
+ * FTTS_E_UNSUPPORTED). */
 int ftts_set_decode_path(int32_t path);
+
+/* Which implementation an ftts_decode_step call on these weights with `batch`
+ * sequences would use under the current setting: 1 one kernel per phase, 2 the
+ * persistent single-launch step, or a negative FTTS_E_* code if the call would
+ * be refused for its weights or batch.  Reads only host memory. */
+int ftts_decode_path(const ftts_weights* w, int32_t batch);
 
 /* Synchronises `stream`, then reports FTTS_E_HIP if a persistent decode step on
  * this workspace gave up waiting for one of its inputs (its bounded wait ran

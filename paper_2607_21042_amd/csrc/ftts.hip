@@ -291,6 +291,19 @@ int ftts_set_decode_path(int32_t path) {
     return FTTS_OK;
 }
 
+int ftts_decode_path(const ftts_weights* w, int32_t batch) {
+    if (!w) return fail(FTTS_E_INVALID_ARG, "weights is NULL");
+    int e = check_config(&w->cfg);
+    if (e != FTTS_OK) return e;
+    if (batch < 1 || batch > FTTS_MAX_BATCH) return fail(FTTS_E_RANGE, "batch must be in [1, %d]", FTTS_MAX_BATCH);
+    if (g_decode_path == 1) return 1;
+    mega::Args ma{};
+    const bool ok = mega_args(w, batch, &ma);
+    if (g_decode_path == 2 && !ok)
+        return fail(FTTS_E_UNSUPPORTED, "the persistent decode step does not take this model/batch/device");
+    return ok ? 2 : 1;
+}
+
 int ftts_check_workspace(const void* ws, size_t ws_bytes, void* stream) {
     if (!ws) return fail(FTTS_E_INVALID_ARG, "workspace is NULL");
     if (ws_bytes < mega_bytes(nullptr, nullptr)) return fail(FTTS_E_WORKSPACE, "workspace too small");

@@ -93,6 +93,8 @@ def lib():
         L.ftts_set_decode_path.argtypes = [i32]
         L.ftts_check_workspace.restype = _c.c_int
         L.ftts_check_workspace.argtypes = [vp, _c.c_size_t, vp]
+        L.ftts_decode_path.restype = _c.c_int
+        L.ftts_decode_path.argtypes = [P(Weights), i32]
         L.ftts_advance.restype = _c.c_int
         L.ftts_advance.argtypes = [vp, vp, vp, vp, vp, i32, vp, vp, i32, i32, vp]
         L.ftts_sample.restype = _c.c_int
@@ -185,6 +187,13 @@ PATH_AUTO, PATH_KERNELS, PATH_PERSISTENT = 0, 1, 2
 def set_decode_path(path: int):
     """ftts_set_decode_path: 0 automatic, 1 one kernel per phase, 2 the persistent step."""
     _check(lib().ftts_set_decode_path(path))
+
+
+def decode_path(model, batch: int) -> int:
+    """ftts_decode_path: 1 (one kernel per phase) or 2 (persistent step) for this model and batch."""
+    r = lib().ftts_decode_path(_c.byref(model.c), int(batch))
+    _check(r if r < 0 else 0)
+    return r
 
 
 def check_workspace(ws, stream=None):

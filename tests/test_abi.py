@@ -145,3 +145,20 @@ def test_page_pool_allocator():
         p.alloc(2)
     p.release(a)
     assert len(p.alloc(4)) == 4
+
+
+def test_decode_path_query():
+    """ftts_decode_path answers from host data only: fp32 weights never take the
+    persistent step, a bad batch is refused, and path 1 is always honoured."""
+    L = ftts.lib()
+    w = _fake_weights(ftts.make_config(workload.TINY, ftts.F32))
+    assert L.ftts_decode_path(ctypes.byref(w), 1) == 1
+    assert L.ftts_decode_path(ctypes.byref(w), 0) == -5
+    assert L.ftts_decode_path(ctypes.byref(w), ftts.MAX_BATCH + 1) == -5
+    try:
+        ftts.set_decode_path(ftts.PATH_PERSISTENT)
+        assert L.ftts_decode_path(ctypes.byref(w), 1) == -7
+        ftts.set_decode_path(ftts.PATH_KERNELS)
+        assert L.ftts_decode_path(ctypes.byref(w), 1) == 1
+    finally:
+        ftts.set_decode_path(ftts.PATH_AUTO)
