@@ -50,6 +50,9 @@ def parse():
     p.add_argument("--cpu-steps", type=int, default=16, help="decode steps timed for the CPU oracle baseline")
     p.add_argument("--graph-steps", type=int, default=32, help="decode steps per HIP graph (kernel-per-phase path)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--paged", action="store_true",
+                   help="the batched paged workload instead: --batch sequences (default 32) with prefix lengths "
+                        "~U[128,512], targets ~U[256,768] then STOP, top-k 30 / top-p 0.8 / T 0.8 sampling")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain device copy of known size (scales the rocprofv3 byte counters)")
     return p.parse_args()
@@ -128,6 +131,131 @@ def cpu_baseline(inputs, shape, mode, prefix, n_steps):
                       f"numpy fp32 oracle on the same {mode} weights"}
 
 
+def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
+    """The batched paged workload: one job = ragged prefill of every sequence, then
+    decode steps until every sequence has produced its target length (the last
+    token forced to STOP), sampling with host uniforms.  The decode steps are
+    replayed from HIP graphs of 32 steps; tokens/s counts only tokens of active
+    sequences."""
+    B = args.batch
+    P, Tt = workload.batch_lengths(B, seed=3)
+    T_max = int(Tt.max())
+    adt = ftts.act_dtype(wdtype)
+    prefix = torch.from_numpy(workload.prefix_embeddings(P.tolist(), shape.d_model, seed=1,
+                                                         bf16=(mode != "f32"))).cuda().to(adt)
+    need = [math.ceil((int(p) + int(t)) / 64) for p, t in zip(P, Tt)]
+    max_pages = max(need)
+    n_pages = sum(need)
+    perm = np.random.default_rng(7).permutation(n_pages)  # pages of a shared pool, scattered
+    bt_np = np.full((B, max_pages), -1, np.int32)
+    k = 0
+    for b, n in enumerate(need):
+        bt_np[b, :n] = perm[k:k + n]
+        k += n
+    bt = torch.from_numpy(bt_np).cuda()
+    kv = ftts.KVCache(shape, wdtype, n_pages)
+    logits = torch.empty((B, shape.vocab), dtype=torch.float32, device="cuda")
+    last = torch.empty((B, shape.vocab), dtype=torch.float32, device="cuda")
+    ws = torch.empty(ftts.workspace_bytes(dm.cfg, B, int(P.sum())), dtype=torch.uint8, device="cuda")
+    samp = ftts.Sampling(0.8, 30, 0.8)
+    uni = torch.from_numpy(workload.uniforms(T_max, B, seed=2)).cuda()
+    tokens = torch.empty(B, dtype=torch.int32, device="cuda")
+    positions = torch.empty(B, dtype=torch.int32, device="cuda")
+    seq_lens = torch.empty(B, dtype=torch.int32, device="cuda")
+    sampled = torch.empty(B, dtype=torch.int32, device="cuda")
+    remaining = torch.empty(B, dtype=torch.int32, device="cuda")
+    history = torch.empty((T_max, B), dtype=torch.int32, device="cuda")
+    counter = torch.empty(1, dtype=torch.int32, device="cuda")
+    pt = ftts.PageTableView(bt, seq_lens)
+    pt.seq_lens = seq_lens
+    pt.c = ftts.PageTable(bt.data_ptr(), seq_lens.data_ptr(), max_pages)
+    P_dev = torch.from_numpy(P).cuda()
+    T_dev = torch.from_numpy(Tt).cuda()
+
+    def reset_and_prefill():
+        tokens.fill_(shape.start_token)
+        positions.zero_()
+        seq_lens.copy_(P_dev)
+        remaining.copy_(T_dev)
+        counter.zero_()
+        ftts.prefill(dm, prefix, P.tolist(), pt, kv, last, ws)
+
+    def step(t):
+        ftts.decode_step(dm, tokens, positions, pt, kv, logits, sampled, uni[t], samp, ws)
+        ftts.advance(tokens, positions, seq_lens, sampled, remaining, shape.stop_token, history, counter)
+
+    reset_and_prefill()
+    step(0)
+    torch.cuda.synchronize()
+    # One graph per 32 steps (each step reads its own row of uniforms): a graph of
+    # every step would be a single dependency chain of ~100k kernel nodes.
+    S = 32
+    graphs = []
+    for g0 in range(0, T_max, S):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for t in range(g0, min(g0 + S, T_max)):
+                step(t)
+        graphs.append(g)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    class _All:
+        def replay(self):
+            for g in graphs:
+                g.replay()
+    graph = _All()
+    for _ in range(args.warmup):
+        reset_and_prefill()
+        graph.replay()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for k in range(args.steps):
+        reset_and_prefill()
+        evs[k][0].record(stream)
+        graph.replay()
+        evs[k][1].record(stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    hist = history.cpu().numpy()
+    assert all(hist[int(Tt[b]) - 1, b] == shape.stop_token for b in range(B)), "STOP not forced"
+    job_ms = t0.elapsed_time(t1) / args.steps
+    decode_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    n_tok = int(Tt.sum())
+    kv_elem = 4 if mode == "f32" else 2
+    per_tok_kv = shape.n_layer * 2 * shape.d_model * kv_elem
+    weights = dm.weight_bytes() - (shape.vocab + shape.n_pos) * shape.d_model * kv_elem
+    total_bytes = 0.0
+    for t in range(T_max):
+        act = Tt > t
+        total_bytes += weights + int(((P + t + 1) * act).sum()) * per_tok_kv + int(act.sum()) * (
+            per_tok_kv + 2 * shape.d_model * kv_elem + shape.vocab * 4)
+    achieved = total_bytes / (decode_ms / 1e3) / 1e9
+    return {
+        "metric": METRIC, "value": round(n_tok / (job_ms / 1e3), 2), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(job_ms, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": {"f32": "f32", "bf16": "bf16", "w8a16": "int8-w/bf16",
+                                                          "w4a16": "int4-w/bf16"}[mode],
+        "data": "synthetic: seeded random-init IndexTTS-2-shaped GPT; paged KV from a shared pool",
+        "config": {"workload": f"indextts2-gpt {mode} paged batch={B} prefix~U[128,512] target~U[256,768]+STOP "
+                               f"top-k 30 top-p 0.8 T 0.8", "batch": B, "tokens": n_tok, "decode_steps": T_max,
+                   "decode_path": "kernel-per-phase" if ftts.decode_path(dm, B) == 1 else "persistent"},
+        "decode_tokens_per_s": round(n_tok / (decode_ms / 1e3), 2),
+        "decode_ms_per_step": round(decode_ms / T_max, 4),
+        "prefill_ms": round(job_ms - decode_ms, 3),
+        "wall_s": round(wall, 3),
+        "roofline": {"bound": "hbm", "kernel": f"decode step, kernel per phase ({T_max} steps, 32 per HIP graph)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "algorithmic_bytes_per_step": int(total_bytes / T_max), "traffic": None},
+    }
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -155,6 +283,11 @@ def main():
     else:
         inputs = workload.quantisable_weights(master)
     dm = ftts.DeviceModel(inputs, shape, wdtype)
+    if args.paged:
+        if args.batch == 1:
+            args.batch = 32
+        print(json.dumps(paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs)), flush=True)
+        return
     adt = ftts.act_dtype(wdtype)
     prefix_np = workload.prefix_embeddings([P] * B, shape.d_model, seed=1, bf16=(mode != "f32"))
     prefix = torch.from_numpy(prefix_np).cuda().to(adt)
