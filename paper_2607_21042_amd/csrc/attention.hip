@@ -42,8 +42,12 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_kernel(const Attn
     const int h = blockIdx.x, b = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     float* out = a.o + (size_t)b * a.o_stride + h * kHeadDim;
+    uint16_t* out16 = a.o_bf16 ? a.o_bf16 + (size_t)b * a.o_stride + h * kHeadDim : nullptr;
     if (!a.active[b]) {
-        if (tid < kHeadDim) out[tid] = 0.f;
+        if (tid < kHeadDim) {
+            if (out16) out16[tid] = 0;
+            else out[tid] = 0.f;
+        }
         return;
     }
     const int ctx = a.seq_lens[b] + 1;                 // cached slots incl. the new token
@@ -158,7 +162,9 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_kernel(const Attn
                 acc = fmaf(s_o[i][tid], wgt, acc);
             }
         }
-        out[tid] = L > 0.f ? acc / L : 0.f;
+        const float r = L > 0.f ? acc / L : 0.f;
+        if (out16) out16[tid] = f32_to_bf16(r);
+        else out[tid] = r;
     }
 }
 

@@ -137,6 +137,9 @@ int check_sampling(const ftts_sampling* s, int V, const float* uniforms) {
 struct DecodeWs {
     float *x, *qkv, *o, *h;
     int32_t* active;
+    uint16_t *a16, *o16, *h16;  // batched path: bf16 inputs of the MFMA linears
+    float* part;                // batched path: split-K partials
+    uint32_t* count;            // batched path: arrival counters
 };
 struct PrefillWs {
     float* x;        // [M][d] fp32 residual
@@ -172,6 +175,20 @@ size_t mega_bytes(MegaWs* out, char* base) {
     return off;
 }
 
+// The batched path's largest split-K partial buffer and counter array.
+size_t bgemm_part_floats(const ftts_config& c, int B) {
+    const int d = c.d_model, F = c.d_ff, V = c.vocab, rows = B < 32 ? B : 32;
+    const int NK[5][3] = {{3 * d, d, c.wdtype}, {d, d, c.wdtype}, {F, d, c.wdtype}, {d, F, c.wdtype}, {V, d, FTTS_BF16}};
+    size_t m = 0;
+    for (const auto& t : NK) {
+        if (c.wdtype == FTTS_F32) break;
+        const int S = bgemm_splits(t[2], t[0], t[1]);
+        const size_t n = S > 1 ? (size_t)S * rows * t[0] : 0;
+        m = n > m ? n : m;
+    }
+    return m;
+}
+
 size_t decode_bytes(const ftts_config& c, int B, DecodeWs* out, char* base) {
     size_t off = mega_bytes(nullptr, nullptr);
     auto take = [&](size_t n) { size_t o = off; off += round256(n); return base ? base + o : nullptr; };
@@ -180,7 +197,20 @@ size_t decode_bytes(const ftts_config& c, int B, DecodeWs* out, char* base) {
     char* o = take((size_t)B * c.d_model * 4);
     char* h = take((size_t)B * c.d_ff * 4);
     char* act = take((size_t)B * 4);
-    if (out) *out = DecodeWs{(float*)x, (float*)qkv, (float*)o, (float*)h, (int32_t*)act};
+    const bool batched = B >= kBatchedMin && c.wdtype != FTTS_F32 && bgemm_supported(c.wdtype, c.d_model) &&
+                         bgemm_supported(c.wdtype, c.d_ff) && bgemm_supported(FTTS_BF16, c.d_model);
+    char *a16 = nullptr, *o16 = nullptr, *h16 = nullptr, *part = nullptr, *count = nullptr;
+    if (batched) {
+        a16 = take((size_t)B * c.d_model * 2);
+        o16 = take((size_t)B * c.d_model * 2);
+        h16 = take((size_t)B * c.d_ff * 2);
+        part = take(bgemm_part_floats(c, B) * 4);
+        const int nmax = std::max(std::max(3 * c.d_model, c.d_ff), c.vocab);
+        count = take((size_t)((nmax + 31) / 32) * 4);
+    }
+    if (out)
+        *out = DecodeWs{(float*)x, (float*)qkv, (float*)o, (float*)h, (int32_t*)act, (uint16_t*)a16, (uint16_t*)o16,
+                        (uint16_t*)h16, (float*)part, (uint32_t*)count};
     return off;
 }
 
@@ -280,6 +310,63 @@ GemvArgs gemv_args(const ftts_linear& L, int N, int K, int B, const float* act, 
 }
 
 }  // namespace
+
+// Decode step for batches of kBatchedMin or more (16-bit and quantised weights):
+// LayerNorm to bf16 rows, then the MFMA linears; attention writes bf16 for the
+// out-projection and FC1's GELU output is bf16 for FC2.
+int decode_batched(const ftts_weights* w, int B, const DecodeWs& W, const KvAppend& kva, AttnDecodeArgs at,
+                   float* logits_out, int32_t* sampled_out, const float* uniforms, const ftts_sampling* samp,
+                   hipStream_t st) {
+    const ftts_config& c = w->cfg;
+    const int d = c.d_model, F = c.d_ff, V = c.vocab;
+    hipError_t e;
+    const int nmax = std::max(std::max(3 * d, F), V);
+    if ((e = launch_fill_u32(W.count, (size_t)(nmax + 31) / 32, 0u, st)) != hipSuccess) return hip_fail(e, "counters");
+    auto lin = [&](const ftts_linear& L, int N, int K, const void* act, float* out, void* out16, int stride) {
+        BgemmArgs g{};
+        g.w = L.w;
+        g.scale = reinterpret_cast<const uint16_t*>(L.scale);
+        g.zero = reinterpret_cast<const uint16_t*>(L.zero);
+        g.bias = L.bias;
+        g.N = N;
+        g.K = K;
+        g.B = B;
+        g.act = act;
+        g.out = out;
+        g.out_bf16 = out16;
+        g.out_stride = stride;
+        g.part = W.part;
+        g.count = W.count;
+        return g;
+    };
+    at.o_bf16 = W.o16;
+    for (int l = 0; l < c.n_layer; ++l) {
+        const ftts_layer& L = w->layers[l];
+        if ((e = launch_ln_rows(c.wdtype, W.x, L.ln1_g, L.ln1_b, c.ln_eps, B, d, W.a16, st)) != hipSuccess)
+            return hip_fail(e, "ln1");
+        BgemmArgs g = lin(L.qkv, 3 * d, d, W.a16, W.qkv, nullptr, 3 * d);
+        g.kv = kva;
+        g.kv.layer = l;
+        if ((e = launch_bgemm(c.wdtype, EPI_QKV, g, st)) != hipSuccess) return hip_fail(e, "qkv");
+        at.layer = l;
+        if ((e = launch_attn_decode(c.wdtype, at, B, st)) != hipSuccess) return hip_fail(e, "attention");
+        g = lin(L.out, d, d, W.o16, W.x, nullptr, d);
+        if ((e = launch_bgemm(c.wdtype, EPI_RESID, g, st)) != hipSuccess) return hip_fail(e, "out-proj");
+        if ((e = launch_ln_rows(c.wdtype, W.x, L.ln2_g, L.ln2_b, c.ln_eps, B, d, W.a16, st)) != hipSuccess)
+            return hip_fail(e, "ln2");
+        g = lin(L.fc1, F, d, W.a16, nullptr, W.h16, F);
+        if ((e = launch_bgemm(c.wdtype, EPI_GELU, g, st)) != hipSuccess) return hip_fail(e, "fc1");
+        g = lin(L.fc2, d, F, W.h16, W.x, nullptr, d);
+        if ((e = launch_bgemm(c.wdtype, EPI_RESID, g, st)) != hipSuccess) return hip_fail(e, "fc2");
+    }
+    if ((e = launch_ln_rows(c.wdtype, W.x, w->lnf_g, w->lnf_b, c.ln_eps, B, d, W.a16, st)) != hipSuccess)
+        return hip_fail(e, "ln_f");
+    BgemmArgs g = lin(w->head, V, d, W.a16, logits_out, nullptr, V);
+    if ((e = launch_bgemm(c.wdtype, EPI_STORE, g, st)) != hipSuccess) return hip_fail(e, "lm head");
+    if ((e = launch_sample(logits_out, B, V, *samp, uniforms, W.active, sampled_out, st)) != hipSuccess)
+        return hip_fail(e, "sampler");
+    return FTTS_OK;
+}
 
 extern "C" {
 
@@ -463,6 +550,7 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
     at.active = W.active;
     at.o = W.o;
     at.o_stride = d;
+    if (W.a16) return decode_batched(w, B, W, kva, at, logits_out, sampled_out, uniforms, samp, st);
 
     for (int l = 0; l < c.n_layer; ++l) {
         const ftts_layer& L = w->layers[l];

@@ -172,7 +172,25 @@ struct AttnDecodeArgs {
     const int32_t* active;
     float* o;                // [B][o_stride] fp32 attention output
     int o_stride;
+    uint16_t* o_bf16;        // if set, the output goes here as bf16 instead
 };
+
+// Batched decode linear on the matrix cores (bgemm.hip).
+struct BgemmArgs {
+    const void* w;           // [N][K] weights in the mode's storage
+    const uint16_t* scale;   // W8: [N]; W4: [N][K/128]
+    const uint16_t* zero;    // W4: [N][K/128]
+    const void* bias;        // [N] bf16
+    int N, K, B;
+    const void* act;         // [B][K] bf16 input
+    float* out;              // STORE / QKV: written, RESID: added to; [B][out_stride] fp32
+    void* out_bf16;          // GELU: [B][out_stride] bf16
+    int out_stride;
+    float* part;             // [S][B][N] fp32 split-K partials
+    uint32_t* count;         // [ceil(N/32)] arrival counters, zero between calls
+    KvAppend kv;             // EPI_QKV: decode form (slot = seq_lens[b], only active rows)
+};
+constexpr int kBatchedMin = 8;  // decode batches of at least this many use the MFMA linears
 
 constexpr int kMaxPrefillSeqs = FTTS_MAX_BATCH;
 struct SeqTable {            // packed varlen sequences, passed by value
@@ -221,6 +239,9 @@ hipError_t launch_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens
                           int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,
                           int max_steps, int B, hipStream_t st);
 hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t st);
+hipError_t launch_bgemm(int wdtype, int epi, const BgemmArgs& a, hipStream_t st);
+int bgemm_splits(int wdtype, int N, int K);
+bool bgemm_supported(int wdtype, int K);
 hipError_t launch_act_to_f32(int wdtype, const void* src, int rows, int d, float* dst, hipStream_t st);
 
 namespace mega {

@@ -44,13 +44,16 @@ def tolerance_ok(gpu, ref, wdtype_name):
 
 
 def argmax_agrees(gpu_tok, ref_logits, wdtype_name):
-    """True if the GPU's greedy token matches, or the oracle's top two are a near-tie."""
+    """True if the GPU's greedy token matches the oracle's, or the step is a
+    near-tie: the oracle's top-1 / top-2 gap is at most twice the tolerance
+    (then any token whose oracle logit lies within that band of the maximum is
+    accepted, and the step is counted)."""
     ref = np.asarray(ref_logits, np.float64)
     top = np.argsort(-ref, kind="stable")[:2]
     if int(gpu_tok) == int(top[0]):
         return True, False
     tol = BF16_ABS_TOL if wdtype_name != "f32" else FP32_REL_TOL * np.max(np.abs(ref))
-    near = (ref[top[0]] - ref[top[1]]) <= 2 * tol and int(gpu_tok) == int(top[1])
+    near = (ref[top[0]] - ref[top[1]]) <= 2 * tol and ref[top[0]] - ref[int(gpu_tok)] <= 2 * tol
     return near, near
 
 

@@ -244,6 +244,39 @@ def test_ragged_batch_and_page_placement(torch_cuda, mode):
     del torch
 
 
+@pytest.mark.parametrize("mode,B", [("bf16", 33), ("w8a16", 8), ("w4a16", 33)])
+def test_batched_decode_matrix_core_linears(torch_cuda, mode, B):
+    """Batches of 8 or more take the MFMA linears (33 = a full group of 32 plus a
+    ragged one): ragged prefixes, sequences retiring at different steps, every
+    logit against the oracle, and bit-identical logits with the pages permuted
+    and from run to run (the split-K sums have a fixed order)."""
+    from paper_2607_21042_amd import ftts
+    shape = workload.TINY
+    inputs = model_inputs(shape, mode, workload.master_weights(shape, seed=0))
+    rng = np.random.default_rng(11)
+    lens = [int(x) for x in rng.integers(1, 150, size=B)]
+    flat = workload.prefix_embeddings(lens, shape.d_model, seed=1)
+    prefixes = np.split(flat, np.cumsum(lens)[:-1])
+    T = 6
+    fed = workload.random_tokens(T, B, shape.vocab, seed=4)
+    fed[0, :] = shape.start_token
+    for b in range(0, B, 5):
+        fed[1 + b % 5:, b] = -1                      # some sequences retire early
+    dm = ftts.DeviceModel(inputs, shape, wd(mode))
+    om = ogpt.GPT(helpers.oracle_weights(inputs, mode), shape.n_head, shape.d_head, dtype=np.float32)
+    say(f"batched decode {mode} B={B}")
+    totals = [n + T for n in lens]
+    bt0, n_pages = helpers.make_block_table(totals)
+    r0 = helpers.run_gpu(dm, shape, prefixes, fed, block_table=bt0, n_pages=n_pages)
+    worst, near = compare_run(r0, om, prefixes, fed, mode)
+    say(f"  worst abs err {worst:.3g}, near ties {near}")
+    bt1, _ = helpers.make_block_table(totals, seed=5)
+    r1 = helpers.run_gpu(dm, shape, prefixes, fed, block_table=bt1, n_pages=n_pages)
+    np.testing.assert_array_equal(r0["logits"], r1["logits"])
+    r2 = helpers.run_gpu(dm, shape, prefixes, fed, block_table=bt1, n_pages=n_pages)
+    np.testing.assert_array_equal(r1["logits"], r2["logits"])
+
+
 @pytest.fixture(scope="module")
 def big_master():
     return workload.master_weights(workload.INDEXTTS2, seed=0)
