@@ -51,24 +51,47 @@ template <> struct BChunk<FTTS_W4A16> {
     float s, z;
 };
 
-// Chunks a wave holds in registers at once (its whole share of a K slice).
-template <int WT> struct ChunksPerWave { static constexpr int value = 4; };
-template <> struct ChunksPerWave<FTTS_W4A16> { static constexpr int value = 2; };
+// Chunks a wave holds in registers at once (its whole share of a K slice).  With
+// the LayerNorm input a W4A16 lane holds 64 fp32 inputs per chunk, so one chunk.
+constexpr int kBgemmWaves = 4, kBgemmThreads = kBgemmWaves * 64;
+template <int WT, bool LN> struct ChunksPerWave { static constexpr int value = 4; };
+template <> struct ChunksPerWave<FTTS_W4A16, false> { static constexpr int value = 2; };
+template <> struct ChunksPerWave<FTTS_W4A16, true> { static constexpr int value = 1; };
+
+// The LayerNorm input: 256 threads = 8 tile groups x 32 rows merge the tile
+// statistics; a slice's gains and biases sit in LDS.
+constexpr int kLnGroups = kBgemmThreads / kBgemmRows;
+constexpr int kLnMaxTP = 8;                                  // tiles per group: K <= 2048
+constexpr int kLnMaxK = kLnGroups * kLnMaxTP * kStatTile;
+constexpr int kLnSliceMax = 1024;                            // >= CPW * waves * KC for every mode
+constexpr int kLnGbPer = kLnSliceMax / kBgemmThreads;
+
+template <int WT> struct XChunk { float4 x[BChunk<WT>::KC / 8]; };  // a lane's KC/2 fp32 inputs
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
-template <int WT>
-__device__ __forceinline__ void load_chunk(const BgemmArgs& p, int n, int m, int h, int c, BChunk<WT>& ch) {
+template <int WT, bool LN>
+__device__ __forceinline__ void load_chunk(const BgemmArgs& p, int n, int m, int h, int c, BChunk<WT>& ch,
+                                           XChunk<WT>& xc) {
     using C = BChunk<WT>;
     const int nn = min(n, p.N - 1);
-    const uint16_t* act = reinterpret_cast<const uint16_t*>(p.act);
-    // activation row m (zeros past the batch): 8 x 16 bytes for W4A16, 2 otherwise
     const int ka = c * C::KC + h * (C::KC / 2);
+    // Every load is unconditional (rows past the batch read the last row and are
+    // zeroed afterwards), so the loads of all chunks stay in flight together.
+    const int mr = min(m, p.B - 1);
+    if constexpr (LN) {
+        // fp32 row m, normalised once the statistics are in
+        const float4* xr = reinterpret_cast<const float4*>(p.ln_x + (size_t)mr * p.K + ka);
 #pragma unroll
-    for (int i = 0; i < (int)(sizeof(ch.a) / 16); ++i)
-        ch.a[i] = m < p.B ? *reinterpret_cast<const uint4*>(act + (size_t)m * p.K + ka + i * 8) : make_uint4(0, 0, 0, 0);
+        for (int i = 0; i < C::KC / 8; ++i) xc.x[i] = xr[i];
+    } else {
+        // bf16 row m: 8 x 16 bytes for W4A16, 2 otherwise
+        const uint4* ar = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.act) + (size_t)mr * p.K + ka);
+#pragma unroll
+        for (int i = 0; i < (int)(sizeof(ch.a) / 16); ++i) ch.a[i] = ar[i];
+    }
     if constexpr (WT == FTTS_BF16) {
         const uint4* w = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.w) + (size_t)nn * p.K + ka);
         ch.w[0] = ld_stream(w);
@@ -105,62 +128,184 @@ __device__ __forceinline__ bgemm_bf16x8 w_operand(const BChunk<WT>& ch, int st) 
     return __builtin_bit_cast(bgemm_bf16x8, r);
 }
 
-template <int EPI>
-__device__ __forceinline__ void bgemm_epilogue(const BgemmArgs& p, int m, int n, float v) {
-    v += bf16_to_f32(reinterpret_cast<const uint16_t*>(p.bias)[n]);
-    if constexpr (EPI == EPI_RESID) {
-        p.out[(size_t)m * p.out_stride + n] += v;
-    } else if constexpr (EPI == EPI_GELU) {
-        reinterpret_cast<uint16_t*>(p.out_bf16)[(size_t)m * p.out_stride + n] = f32_to_bf16(gelu_tanh(v));
-    } else {
-        p.out[(size_t)m * p.out_stride + n] = v;
-        if constexpr (EPI == EPI_QKV) {
-            const int d = p.kv.d_model;
-            if (n >= d && p.kv.active[m]) {
-                const int kvsel = n >= 2 * d;
-                const int r = n - d - kvsel * d;
-                const int slot = p.kv.seq_lens[m];
-                const int phys = p.kv.block_table[(size_t)m * p.kv.max_pages + slot / kPage];
-                st_act<false>(p.kv.base,
-                              kv_offset(p.kv.layer, p.kv.n_pages, phys, kvsel, p.kv.n_head, r / kHeadDim, slot % kPage) +
-                                  r % kHeadDim,
-                              v);
-            }
-        }
-    }
-}
+// Everything the epilogue reads that does not depend on the products, loaded at
+// the start so that it arrives while the weights stream in.
+constexpr int kBgemmEpt = kBgemmRows * kBgemmFeat / kBgemmThreads;  // tile elements per thread
+template <int WT, int EPI> struct EpiPre {
+    float bias, scale;
+    float xold[kBgemmEpt];   // EPI_RESID
+    int on[kBgemmEpt];       // EPI_QKV: the row is active (appends its key and value)
+    int slot[kBgemmEpt];     //          at this KV slot
+    int phys[kBgemmEpt];     //          in this physical page
+};
 
-template <int WT, int EPI>
-__global__ __launch_bounds__(256) void bgemm_kernel(const BgemmArgs p) {
+template <int WT, int EPI, bool LN>
+__global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p) {
     using C = BChunk<WT>;
-    constexpr int CPW = ChunksPerWave<WT>::value;
-    __shared__ float s_red[4][kBgemmRows * kBgemmFeat];
+    constexpr int CPW = ChunksPerWave<WT, LN>::value, NT = kBgemmThreads, EPT = kBgemmEpt;
+    static_assert(CPW * kBgemmWaves * C::KC <= kLnSliceMax, "LayerNorm slice does not fit");
+    __shared__ float s_red[kBgemmWaves][kBgemmRows * kBgemmFeat];
     __shared__ int s_last;
+    __shared__ __attribute__((aligned(16))) float s_g[LN ? kLnSliceMax : 4];
+    __shared__ __attribute__((aligned(16))) float s_b[LN ? kLnSliceMax : 4];
+    __shared__ float2 s_gs[LN ? kLnGroups : 1][kBgemmRows];
+    __shared__ float s_mean[kBgemmRows], s_rstd[kBgemmRows];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int f = blockIdx.x, s = blockIdx.y, S = gridDim.y;
     const int n0 = f * kBgemmFeat;
     const int fr = lane & 31, h = lane >> 5;
     const int nchunks = p.K / C::KC;
     const int c0 = s * nchunks / S, c1 = (s + 1) * nchunks / S;
+    // this thread's epilogue elements: feature ne, rows mrow(i)
+    const int ne = min(n0 + (tid & (kBgemmFeat - 1)), p.N - 1);
+    auto mrow = [&](int i) { return (tid >> 5) + (NT / kBgemmFeat) * i; };
 
-    // Every load of this wave goes out first (chunks c0 + wave + 4j; indices past
-    // the slice repeat its last chunk and are not used), then the products.
-    C ch[CPW];
+    // 1. LayerNorm inputs: this thread's (row, tile group) statistics, the slice's gains/biases.
+    const int T = p.K / kStatTile, TP = (T + kLnGroups - 1) / kLnGroups;
+    const int lr = tid & (kBgemmRows - 1), lq = tid >> 5;
+    float2 st[LN ? kLnMaxTP : 1];
+    uint16_t gr[LN ? kLnGbPer : 1], br[LN ? kLnGbPer : 1];
+    const int k0 = c0 * C::KC, kn = (c1 - c0) * C::KC;
+    if constexpr (LN) {
+        const int m = min(lr, p.B - 1);
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) load_chunk<WT>(p, n0 + fr, fr, h, min(c0 + wave + 4 * j, c1 - 1), ch[j]);
+        for (int j = 0; j < kLnMaxTP; ++j) st[j] = p.ln_stats[(size_t)min(lq * TP + j, T - 1) * p.stats_ld + m];
+#pragma unroll
+        for (int j = 0; j < kLnGbPer; ++j) {
+            const int k = min(tid + NT * j, kn - 1);
+            gr[j] = reinterpret_cast<const uint16_t*>(p.ln_g)[k0 + k];
+            br[j] = reinterpret_cast<const uint16_t*>(p.ln_b)[k0 + k];
+        }
+    }
+    // 2. epilogue operands
+    EpiPre<WT, EPI> pre;
+    pre.bias = bf16_to_f32(reinterpret_cast<const uint16_t*>(p.bias)[ne]);
+    pre.scale = WT == FTTS_W8A16 ? bf16_to_f32(p.scale[ne]) : 1.f;
+    if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) pre.xold[i] = p.out[(size_t)min(mrow(i), p.B - 1) * p.out_stride + ne];
+    }
+    const bool kv_col = EPI == EPI_QKV && ne >= p.kv.d_model;
+    if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+            const int m = min(mrow(i), p.B - 1);
+            pre.on[i] = p.kv.active[m];
+            pre.slot[i] = p.kv.seq_lens[m];
+        }
+    }
+    // 3. every input and weight load of this wave (chunks c0 + wave + 4j; indices
+    // past the slice repeat its last chunk and are not used)
+    C ch[CPW];
+    XChunk<WT> xc[LN ? CPW : 1];
+#pragma unroll
+    for (int j = 0; j < CPW; ++j)
+        load_chunk<WT, LN>(p, n0 + fr, fr, h, min(c0 + wave + kBgemmWaves * j, c1 - 1), ch[j], xc[LN ? j : 0]);
+    // Nothing that waits for a load may be scheduled above this point: every load
+    // above is in flight before the first wait.
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+            const int m = min(mrow(i), p.B - 1);
+            // (an inactive row's slot may be anything: the page index is clamped and unused)
+            const int pg = min(max(pre.slot[i], 0) / kPage, p.kv.max_pages - 1);
+            pre.phys[i] = p.kv.block_table[(size_t)m * p.kv.max_pages + pg];
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // 4. LayerNorm: merge the statistics (law of total variance, fixed order), then
+    // normalise the inputs into bf16 operands.
+    if constexpr (LN) {
+        // this group's tiles: lq * TP + j for j < cnt
+        const int cnt = min(max(T - lq * TP, 0), TP);
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < kLnMaxTP; ++j) sum += j < cnt ? st[j].x : 0.f;
+        const float mean_q = sum / (float)(max(cnt, 1) * kStatTile);
+        float m2 = 0.f;
+#pragma unroll
+        for (int j = 0; j < kLnMaxTP; ++j) {
+            const float dm = st[j].x * (1.0f / kStatTile) - mean_q;
+            m2 += j < cnt ? st[j].y + (float)kStatTile * dm * dm : 0.f;
+        }
+        s_gs[lq][lr] = make_float2(sum, m2);
+#pragma unroll
+        for (int j = 0; j < kLnGbPer; ++j)
+            if (tid + NT * j < kn) {
+                s_g[tid + NT * j] = bf16_to_f32(gr[j]);
+                s_b[tid + NT * j] = bf16_to_f32(br[j]);
+            }
+        __syncthreads();
+        if (tid < kBgemmRows) {
+            // every group is read (empty ones hold zeros and weigh nothing): no branches
+            float2 gs[kLnGroups];
+#pragma unroll
+            for (int q = 0; q < kLnGroups; ++q) gs[q] = s_gs[q][tid];
+            float tot = 0.f;
+#pragma unroll
+            for (int q = 0; q < kLnGroups; ++q) tot += gs[q].x;
+            const float mean = tot / (float)p.K;
+            float M2 = 0.f;
+#pragma unroll
+            for (int q = 0; q < kLnGroups; ++q) {
+                const int nq = min(max(T - q * TP, 0), TP) * kStatTile;
+                const float dm = gs[q].x / (float)max(nq, 1) - mean;
+                M2 += nq > 0 ? gs[q].y + (float)nq * dm * dm : 0.f;
+            }
+            s_mean[tid] = mean;
+            s_rstd[tid] = tid < p.B ? 1.0f / sqrtf(M2 / (float)p.K + p.ln_eps) : 0.f;
+        }
+        __syncthreads();
+        const float mean = s_mean[fr], rstd = s_rstd[fr];
+        const bool live = fr < p.B;
+#pragma unroll
+        for (int j = 0; j < CPW; ++j) {
+            // 16-value aligned offset into the slice's gains/biases
+            const int kl = min(c0 + wave + kBgemmWaves * j, c1 - 1) * C::KC + h * (C::KC / 2) - k0;
+#pragma unroll
+            for (int i = 0; i < C::KC / 16; ++i) {
+                const float4 u = xc[j].x[2 * i], v = xc[j].x[2 * i + 1];
+                const float4 g0 = *reinterpret_cast<const float4*>(s_g + kl + 8 * i);
+                const float4 g1 = *reinterpret_cast<const float4*>(s_g + kl + 8 * i + 4);
+                const float4 b0 = *reinterpret_cast<const float4*>(s_b + kl + 8 * i);
+                const float4 b1 = *reinterpret_cast<const float4*>(s_b + kl + 8 * i + 4);
+                const float xs[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};
+                const float gs[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+                const float bs[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+                float y[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float t = (xs[e] - mean) * rstd * gs[e] + bs[e];
+                    y[e] = live ? t : 0.f;
+                }
+                ch[j].a[i] = make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
+                                        pack_bf16x2(y[6], y[7]));
+            }
+        }
+    }
+    if constexpr (!LN) {
+        if (fr >= p.B) {
+#pragma unroll
+            for (int j = 0; j < CPW; ++j)
+#pragma unroll
+                for (int i = 0; i < (int)(sizeof(ch[j].a) / 16); ++i) ch[j].a[i] = make_uint4(0, 0, 0, 0);
+        }
+    }
+    // 5. products
     bgemm_f32x16 acc;
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = 0.f;
 #pragma unroll
     for (int j = 0; j < CPW; ++j) {
-        if (c0 + wave + 4 * j < c1) {
+        if (c0 + wave + kBgemmWaves * j < c1) {
             bgemm_f32x16 part;
 #pragma unroll
             for (int i = 0; i < 16; ++i) part[i] = 0.f;
 #pragma unroll
-            for (int st = 0; st < C::STEPS; ++st) {
-                const bgemm_bf16x8 av = __builtin_bit_cast(bgemm_bf16x8, ch[j].a[st]);
-                part = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, w_operand<WT>(ch[j], st), part, 0, 0, 0);
+            for (int st2 = 0; st2 < C::STEPS; ++st2) {
+                const bgemm_bf16x8 av = __builtin_bit_cast(bgemm_bf16x8, ch[j].a[st2]);
+                part = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, w_operand<WT>(ch[j], st2), part, 0, 0, 0);
             }
             if constexpr (WT == FTTS_W4A16) {
 #pragma unroll
@@ -175,19 +320,22 @@ __global__ __launch_bounds__(256) void bgemm_kernel(const BgemmArgs p) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) s_red[wave][((i >> 2) * 8 + h * 4 + (i & 3)) * kBgemmFeat + fr] = acc[i];
     __syncthreads();
-    float v[4];
+    float v[EPT];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int e = tid + 256 * i;
-        v[i] = (s_red[0][e] + s_red[1][e]) + (s_red[2][e] + s_red[3][e]);
+    for (int i = 0; i < EPT; ++i) {
+        const int e = tid + NT * i;
+        float t = 0.f;
+#pragma unroll
+        for (int w = 0; w < kBgemmWaves; ++w) t += s_red[w][e];
+        v[i] = t;
     }
     if (S > 1) {
         // Partials go out with device-coherent stores and are waited for before the
         // arrival count, so the last group reads them (device-coherent loads) without
         // any cache flush.
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int e = tid + 256 * i, m = e / kBgemmFeat, n = n0 + e % kBgemmFeat;
+        for (int i = 0; i < EPT; ++i) {
+            const int m = mrow(i), n = n0 + (tid & (kBgemmFeat - 1));
             if (m < p.B && n < p.N)
                 __hip_atomic_store(p.part + ((size_t)s * p.B + m) * p.N + n, v[i], __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
@@ -199,18 +347,18 @@ __global__ __launch_bounds__(256) void bgemm_kernel(const BgemmArgs p) {
                      (unsigned)(S - 1);
         __syncthreads();
         if (!s_last) return;
-        // all S x 4 loads go out before the first add (indices clamped, extras unused)
-        float pv[4][kBgemmMaxSplits];
+        // every partial load goes out before the first add (indices clamped, extras unused)
+        float pv[EPT][kBgemmMaxSplits];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int e = tid + 256 * i, m = min(e / kBgemmFeat, p.B - 1), n = min(n0 + e % kBgemmFeat, p.N - 1);
+        for (int i = 0; i < EPT; ++i) {
+            const int m = min(mrow(i), p.B - 1);
 #pragma unroll
             for (int k = 0; k < kBgemmMaxSplits; ++k)
-                pv[i][k] = __hip_atomic_load(p.part + ((size_t)min(k, S - 1) * p.B + m) * p.N + n, __ATOMIC_RELAXED,
+                pv[i][k] = __hip_atomic_load(p.part + ((size_t)min(k, S - 1) * p.B + m) * p.N + ne, __ATOMIC_RELAXED,
                                              __HIP_MEMORY_SCOPE_AGENT);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < EPT; ++i) {
             float t = 0.f;
 #pragma unroll
             for (int k = 0; k < kBgemmMaxSplits; ++k)
@@ -219,53 +367,95 @@ __global__ __launch_bounds__(256) void bgemm_kernel(const BgemmArgs p) {
         }
         if (tid == 0) __hip_atomic_store(p.count + f, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    float rs = 1.f;
+    // 6. epilogue
+    const bool col_ok = n0 + (tid & (kBgemmFeat - 1)) < p.N;
+    float xn[EPT];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int e = tid + 256 * i, m = e / kBgemmFeat, n = n0 + e % kBgemmFeat;
-        if (m < p.B && n < p.N) {
-            if constexpr (WT == FTTS_W8A16) rs = bf16_to_f32(p.scale[n]);
-            bgemm_epilogue<EPI>(p, m, n, v[i] * rs);
+    for (int i = 0; i < EPT; ++i) {
+        const int m = mrow(i);
+        const bool ok = m < p.B && col_ok;
+        const float y = v[i] * pre.scale + pre.bias;
+        xn[i] = 0.f;
+        if (!ok) continue;
+        const size_t o = (size_t)m * p.out_stride + ne;
+        if constexpr (EPI == EPI_RESID) {
+            xn[i] = pre.xold[i] + y;
+            p.out[o] = xn[i];
+        } else if constexpr (EPI == EPI_GELU) {
+            reinterpret_cast<uint16_t*>(p.out_bf16)[o] = f32_to_bf16(gelu_tanh(y));
+        } else {
+            p.out[o] = y;
+            if constexpr (EPI == EPI_QKV) {
+                if (kv_col && pre.on[i]) {
+                    const int d = p.kv.d_model, kvsel = ne >= 2 * d, r = ne - d - kvsel * d;
+                    st_act<false>(p.kv.base,
+                                  kv_offset(p.kv.layer, p.kv.n_pages, pre.phys[i], kvsel, p.kv.n_head, r / kHeadDim,
+                                            pre.slot[i] % kPage) +
+                                      r % kHeadDim,
+                                  y);
+                }
+            }
+        }
+    }
+    if constexpr (EPI == EPI_RESID) {
+        if (p.stats_out) {
+#pragma unroll
+            for (int i = 0; i < EPT; ++i) {
+                const float2 ts = tile_stats32(xn[i]);
+                if ((tid & (kBgemmFeat - 1)) == 0 && mrow(i) < p.B) p.stats_out[(size_t)f * p.stats_ld + mrow(i)] = ts;
+            }
         }
     }
 }
 
-template <int WT>
+template <int WT, bool LN>
 static hipError_t bgemm_by_epi(int epi, const BgemmArgs& a, dim3 g, hipStream_t st) {
+    const dim3 blk(kBgemmThreads);
     switch (epi) {
-        case EPI_STORE: hipLaunchKernelGGL((bgemm_kernel<WT, EPI_STORE>), g, dim3(256), 0, st, a); break;
-        case EPI_QKV: hipLaunchKernelGGL((bgemm_kernel<WT, EPI_QKV>), g, dim3(256), 0, st, a); break;
-        case EPI_GELU: hipLaunchKernelGGL((bgemm_kernel<WT, EPI_GELU>), g, dim3(256), 0, st, a); break;
-        case EPI_RESID: hipLaunchKernelGGL((bgemm_kernel<WT, EPI_RESID>), g, dim3(256), 0, st, a); break;
+        case EPI_STORE: hipLaunchKernelGGL((bgemm_kernel<WT, EPI_STORE, LN>), g, blk, 0, st, a); break;
+        case EPI_QKV: hipLaunchKernelGGL((bgemm_kernel<WT, EPI_QKV, LN>), g, blk, 0, st, a); break;
+        case EPI_GELU: hipLaunchKernelGGL((bgemm_kernel<WT, EPI_GELU, LN>), g, blk, 0, st, a); break;
+        case EPI_RESID:
+            if constexpr (LN) return hipErrorInvalidValue;  // the residual update never normalises its input
+            else hipLaunchKernelGGL((bgemm_kernel<WT, EPI_RESID, false>), g, blk, 0, st, a);
+            break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 // K slices per feature tile: enough that each wave's share fits its registers.
-int bgemm_splits(int wdtype, int N, int K) {
+int bgemm_splits(int wdtype, int N, int K, bool ln) {
     (void)N;
     const int kc = wdtype == FTTS_W4A16 ? 128 : 32;
-    const int per_group = 4 * (wdtype == FTTS_W4A16 ? ChunksPerWave<FTTS_W4A16>::value : ChunksPerWave<FTTS_BF16>::value);
-    const int chunks = K / kc;
+    const int cpw = wdtype == FTTS_W4A16 ? (ln ? ChunksPerWave<FTTS_W4A16, true>::value
+                                               : ChunksPerWave<FTTS_W4A16, false>::value)
+                                         : ChunksPerWave<FTTS_BF16, false>::value;
+    const int chunks = K / kc, per_group = kBgemmWaves * cpw;
     return (chunks + per_group - 1) / per_group;
 }
 
-bool bgemm_supported(int wdtype, int K) {
+bool bgemm_supported(int wdtype, int K, bool ln) {
     if (wdtype == FTTS_F32) return false;
-    return K % (wdtype == FTTS_W4A16 ? 128 : 32) == 0 && bgemm_splits(wdtype, 0, K) <= kBgemmMaxSplits;
+    if (ln && (K % kStatTile != 0 || K > kLnMaxK)) return false;
+    return K % (wdtype == FTTS_W4A16 ? 128 : 32) == 0 && bgemm_splits(wdtype, 0, K, ln) <= kBgemmMaxSplits;
 }
 
 hipError_t launch_bgemm(int wdtype, int epi, const BgemmArgs& in, hipStream_t st) {
     // The LM head is never quantised.
     const int wt = epi == EPI_STORE ? FTTS_BF16 : wdtype;
-    if (!bgemm_supported(wt, in.K)) return hipErrorInvalidValue;
-    const int S = bgemm_splits(wt, in.N, in.K);
+    const bool ln = in.ln_x != nullptr;
+    if (!bgemm_supported(wt, in.K, ln)) return hipErrorInvalidValue;
+    if (epi == EPI_RESID && in.stats_out && in.N % kStatTile != 0) return hipErrorInvalidValue;
+    const int S = bgemm_splits(wt, in.N, in.K, ln);
     const dim3 g((in.N + kBgemmFeat - 1) / kBgemmFeat, S);
     for (int b0 = 0; b0 < in.B; b0 += kBgemmRows) {
         BgemmArgs a = in;
         a.B = in.B - b0 < kBgemmRows ? in.B - b0 : kBgemmRows;
-        a.act = reinterpret_cast<const uint16_t*>(in.act) + (size_t)b0 * in.K;
+        if (in.act) a.act = reinterpret_cast<const uint16_t*>(in.act) + (size_t)b0 * in.K;
+        if (in.ln_x) a.ln_x = in.ln_x + (size_t)b0 * in.K;
+        if (in.ln_stats) a.ln_stats = in.ln_stats + b0;
+        if (in.stats_out) a.stats_out = in.stats_out + b0;
         if (in.out) a.out = in.out + (size_t)b0 * in.out_stride;
         if (in.out_bf16) a.out_bf16 = reinterpret_cast<uint16_t*>(in.out_bf16) + (size_t)b0 * in.out_stride;
         if (epi == EPI_QKV) {
@@ -275,9 +465,9 @@ hipError_t launch_bgemm(int wdtype, int epi, const BgemmArgs& in, hipStream_t st
         }
         hipError_t e;
         switch (wt) {
-            case FTTS_BF16: e = bgemm_by_epi<FTTS_BF16>(epi, a, g, st); break;
-            case FTTS_W8A16: e = bgemm_by_epi<FTTS_W8A16>(epi, a, g, st); break;
-            case FTTS_W4A16: e = bgemm_by_epi<FTTS_W4A16>(epi, a, g, st); break;
+            case FTTS_BF16: e = ln ? bgemm_by_epi<FTTS_BF16, true>(epi, a, g, st) : bgemm_by_epi<FTTS_BF16, false>(epi, a, g, st); break;
+            case FTTS_W8A16: e = ln ? bgemm_by_epi<FTTS_W8A16, true>(epi, a, g, st) : bgemm_by_epi<FTTS_W8A16, false>(epi, a, g, st); break;
+            case FTTS_W4A16: e = ln ? bgemm_by_epi<FTTS_W4A16, true>(epi, a, g, st) : bgemm_by_epi<FTTS_W4A16, false>(epi, a, g, st); break;
             default: return hipErrorInvalidValue;
         }
         if (e != hipSuccess) return e;

@@ -137,7 +137,8 @@ int check_sampling(const ftts_sampling* s, int V, const float* uniforms) {
 struct DecodeWs {
     float *x, *qkv, *o, *h;
     int32_t* active;
-    uint16_t *a16, *o16, *h16;  // batched path: bf16 inputs of the MFMA linears
+    float2* stats;              // batched path: residual tile statistics [d/32][B]
+    uint16_t *o16, *h16;        // batched path: bf16 inputs of the MFMA linears
     float* part;                // batched path: split-K partials
     uint32_t* count;            // batched path: arrival counters
 };
@@ -175,14 +176,22 @@ size_t mega_bytes(MegaWs* out, char* base) {
     return off;
 }
 
-// The batched path's largest split-K partial buffer and counter array.
+// Arrival counters of the batched path: one per 32-feature tile of the widest linear.
+int bgemm_counters(const ftts_config& c) {
+    const int nmax = std::max(std::max(3 * c.d_model, c.d_ff), c.vocab);
+    return (nmax + 31) / 32;
+}
+
+// The batched path's largest split-K partial buffer.  The
+// linears after a LayerNorm (QKV, FC1, head) normalise their input themselves.
 size_t bgemm_part_floats(const ftts_config& c, int B) {
     const int d = c.d_model, F = c.d_ff, V = c.vocab, rows = B < 32 ? B : 32;
-    const int NK[5][3] = {{3 * d, d, c.wdtype}, {d, d, c.wdtype}, {F, d, c.wdtype}, {d, F, c.wdtype}, {V, d, FTTS_BF16}};
+    const int NK[5][4] = {{3 * d, d, c.wdtype, 1}, {d, d, c.wdtype, 0}, {F, d, c.wdtype, 1}, {d, F, c.wdtype, 0},
+                          {V, d, FTTS_BF16, 1}};
     size_t m = 0;
     for (const auto& t : NK) {
         if (c.wdtype == FTTS_F32) break;
-        const int S = bgemm_splits(t[2], t[0], t[1]);
+        const int S = bgemm_splits(t[2], t[0], t[1], t[3] != 0);
         const size_t n = S > 1 ? (size_t)S * rows * t[0] : 0;
         m = n > m ? n : m;
     }
@@ -197,19 +206,19 @@ size_t decode_bytes(const ftts_config& c, int B, DecodeWs* out, char* base) {
     char* o = take((size_t)B * c.d_model * 4);
     char* h = take((size_t)B * c.d_ff * 4);
     char* act = take((size_t)B * 4);
-    const bool batched = B >= kBatchedMin && c.wdtype != FTTS_F32 && bgemm_supported(c.wdtype, c.d_model) &&
-                         bgemm_supported(c.wdtype, c.d_ff) && bgemm_supported(FTTS_BF16, c.d_model);
-    char *a16 = nullptr, *o16 = nullptr, *h16 = nullptr, *part = nullptr, *count = nullptr;
+    const bool batched = B >= kBatchedMin && c.wdtype != FTTS_F32 && c.d_model % 64 == 0 &&
+                         bgemm_supported(c.wdtype, c.d_model, true) && bgemm_supported(c.wdtype, c.d_model, false) &&
+                         bgemm_supported(c.wdtype, c.d_ff, false) && bgemm_supported(FTTS_BF16, c.d_model, true);
+    char *stats = nullptr, *o16 = nullptr, *h16 = nullptr, *part = nullptr, *count = nullptr;
     if (batched) {
-        a16 = take((size_t)B * c.d_model * 2);
+        stats = take((size_t)(c.d_model / kStatTile) * B * sizeof(float2));
         o16 = take((size_t)B * c.d_model * 2);
         h16 = take((size_t)B * c.d_ff * 2);
         part = take(bgemm_part_floats(c, B) * 4);
-        const int nmax = std::max(std::max(3 * c.d_model, c.d_ff), c.vocab);
-        count = take((size_t)((nmax + 31) / 32) * 4);
+        count = take((size_t)bgemm_counters(c) * 4);
     }
     if (out)
-        *out = DecodeWs{(float*)x, (float*)qkv, (float*)o, (float*)h, (int32_t*)act, (uint16_t*)a16, (uint16_t*)o16,
+        *out = DecodeWs{(float*)x, (float*)qkv, (float*)o, (float*)h, (int32_t*)act, (float2*)stats, (uint16_t*)o16,
                         (uint16_t*)h16, (float*)part, (uint32_t*)count};
     return off;
 }
@@ -312,16 +321,15 @@ GemvArgs gemv_args(const ftts_linear& L, int N, int K, int B, const float* act, 
 }  // namespace
 
 // Decode step for batches of kBatchedMin or more (16-bit and quantised weights):
-// LayerNorm to bf16 rows, then the MFMA linears; attention writes bf16 for the
-// out-projection and FC1's GELU output is bf16 for FC2.
+// the MFMA linears, with each LayerNorm folded into the linear that reads it (the
+// residual updates leave per-tile row statistics behind).  Attention writes bf16
+// for the out-projection and FC1's GELU output is bf16 for FC2.
 int decode_batched(const ftts_weights* w, int B, const DecodeWs& W, const KvAppend& kva, AttnDecodeArgs at,
                    float* logits_out, int32_t* sampled_out, const float* uniforms, const ftts_sampling* samp,
                    hipStream_t st) {
     const ftts_config& c = w->cfg;
     const int d = c.d_model, F = c.d_ff, V = c.vocab;
     hipError_t e;
-    const int nmax = std::max(std::max(3 * d, F), V);
-    if ((e = launch_fill_u32(W.count, (size_t)(nmax + 31) / 32, 0u, st)) != hipSuccess) return hip_fail(e, "counters");
     auto lin = [&](const ftts_linear& L, int N, int K, const void* act, float* out, void* out16, int stride) {
         BgemmArgs g{};
         g.w = L.w;
@@ -337,32 +345,37 @@ int decode_batched(const ftts_weights* w, int B, const DecodeWs& W, const KvAppe
         g.out_stride = stride;
         g.part = W.part;
         g.count = W.count;
+        g.stats_ld = B;
+        return g;
+    };
+    auto normed = [&](BgemmArgs g, const void* ln_g, const void* ln_b) {
+        g.ln_x = W.x;
+        g.ln_g = ln_g;
+        g.ln_b = ln_b;
+        g.ln_eps = c.ln_eps;
+        g.ln_stats = W.stats;
         return g;
     };
     at.o_bf16 = W.o16;
     for (int l = 0; l < c.n_layer; ++l) {
         const ftts_layer& L = w->layers[l];
-        if ((e = launch_ln_rows(c.wdtype, W.x, L.ln1_g, L.ln1_b, c.ln_eps, B, d, W.a16, st)) != hipSuccess)
-            return hip_fail(e, "ln1");
-        BgemmArgs g = lin(L.qkv, 3 * d, d, W.a16, W.qkv, nullptr, 3 * d);
+        BgemmArgs g = normed(lin(L.qkv, 3 * d, d, nullptr, W.qkv, nullptr, 3 * d), L.ln1_g, L.ln1_b);
         g.kv = kva;
         g.kv.layer = l;
-        if ((e = launch_bgemm(c.wdtype, EPI_QKV, g, st)) != hipSuccess) return hip_fail(e, "qkv");
+        if ((e = launch_bgemm(c.wdtype, EPI_QKV, g, st)) != hipSuccess) return hip_fail(e, "ln1 + qkv");
         at.layer = l;
         if ((e = launch_attn_decode(c.wdtype, at, B, st)) != hipSuccess) return hip_fail(e, "attention");
         g = lin(L.out, d, d, W.o16, W.x, nullptr, d);
+        g.stats_out = W.stats;
         if ((e = launch_bgemm(c.wdtype, EPI_RESID, g, st)) != hipSuccess) return hip_fail(e, "out-proj");
-        if ((e = launch_ln_rows(c.wdtype, W.x, L.ln2_g, L.ln2_b, c.ln_eps, B, d, W.a16, st)) != hipSuccess)
-            return hip_fail(e, "ln2");
-        g = lin(L.fc1, F, d, W.a16, nullptr, W.h16, F);
-        if ((e = launch_bgemm(c.wdtype, EPI_GELU, g, st)) != hipSuccess) return hip_fail(e, "fc1");
+        g = normed(lin(L.fc1, F, d, nullptr, nullptr, W.h16, F), L.ln2_g, L.ln2_b);
+        if ((e = launch_bgemm(c.wdtype, EPI_GELU, g, st)) != hipSuccess) return hip_fail(e, "ln2 + fc1");
         g = lin(L.fc2, d, F, W.h16, W.x, nullptr, d);
+        g.stats_out = W.stats;
         if ((e = launch_bgemm(c.wdtype, EPI_RESID, g, st)) != hipSuccess) return hip_fail(e, "fc2");
     }
-    if ((e = launch_ln_rows(c.wdtype, W.x, w->lnf_g, w->lnf_b, c.ln_eps, B, d, W.a16, st)) != hipSuccess)
-        return hip_fail(e, "ln_f");
-    BgemmArgs g = lin(w->head, V, d, W.a16, logits_out, nullptr, V);
-    if ((e = launch_bgemm(c.wdtype, EPI_STORE, g, st)) != hipSuccess) return hip_fail(e, "lm head");
+    BgemmArgs g = normed(lin(w->head, V, d, nullptr, logits_out, nullptr, V), w->lnf_g, w->lnf_b);
+    if ((e = launch_bgemm(c.wdtype, EPI_STORE, g, st)) != hipSuccess) return hip_fail(e, "ln_f + lm head");
     if ((e = launch_sample(logits_out, B, V, *samp, uniforms, W.active, sampled_out, st)) != hipSuccess)
         return hip_fail(e, "sampler");
     return FTTS_OK;
@@ -524,8 +537,10 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
     }
 
     (void)hipGetLastError();
+    // the batched path also takes the first LayerNorm's statistics and zeroes its counters here
     hipError_t e = launch_embed(c.wdtype, w->tok_emb, w->pos_emb, V, c.n_pos, d, tokens, positions, pt->seq_lens,
-                                pt->block_table, pt->max_pages, kv->n_pages, B, W.x, W.active, st);
+                                pt->block_table, pt->max_pages, kv->n_pages, B, W.x, W.active, W.stats, W.count,
+                                W.stats ? bgemm_counters(c) : 0, st);
     if (e != hipSuccess) return hip_fail(e, "embed");
 
     KvAppend kva{};
@@ -550,7 +565,7 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
     at.active = W.active;
     at.o = W.o;
     at.o_stride = d;
-    if (W.a16) return decode_batched(w, B, W, kva, at, logits_out, sampled_out, uniforms, samp, st);
+    if (W.stats) return decode_batched(w, B, W, kva, at, logits_out, sampled_out, uniforms, samp, st);
 
     for (int l = 0; l < c.n_layer; ++l) {
         const ftts_layer& L = w->layers[l];

@@ -116,6 +116,17 @@ __device__ __forceinline__ float stride8_max(float v) {
 __device__ __forceinline__ float wave_sum(float v) { return group_sum<kWave>(v); }
 __device__ __forceinline__ float wave_max(float v) { return group_max<kWave>(v); }
 
+// Row statistics of one 32-column tile held by the 32 lanes of a half wave (one
+// value per lane): (sum, sum of squared deviations from the tile's own mean).
+// LayerNorm consumers merge the tiles of a row exactly by the law of total
+// variance, so no pass over the row is needed.  The whole wave must be active.
+constexpr int kStatTile = 32;
+__device__ __forceinline__ float2 tile_stats32(float v) {
+    const float s = group_sum<kStatTile>(v);
+    const float dv = v - s * (1.0f / kStatTile);
+    return make_float2(s, group_sum<kStatTile>(dv * dv));
+}
+
 // GPT-2 tanh GELU.
 __device__ __forceinline__ float gelu_tanh(float u) {
     const float c = 0.7978845608028654f;  // sqrt(2/pi)
@@ -189,6 +200,17 @@ struct BgemmArgs {
     float* part;             // [S][B][N] fp32 split-K partials
     uint32_t* count;         // [ceil(N/32)] arrival counters, zero between calls
     KvAppend kv;             // EPI_QKV: decode form (slot = seq_lens[b], only active rows)
+    // LayerNorm on the input side: when ln_x is set, act is ignored and the input
+    // row m is LN(ln_x[m]) with gain ln_g / bias ln_b, its mean and variance
+    // merged from ln_stats (tile statistics, [K/32][stats_ld], see tile_stats32).
+    const float* ln_x;       // [B][K] fp32
+    const void* ln_g;
+    const void* ln_b;
+    float ln_eps;
+    const float2* ln_stats;
+    // EPI_RESID: tile statistics of the updated rows go to stats_out [N/32][stats_ld].
+    float2* stats_out;
+    int stats_ld;
 };
 constexpr int kBatchedMin = 8;  // decode batches of at least this many use the MFMA linears
 
@@ -222,7 +244,7 @@ struct AttnPrefillArgs {
 hipError_t launch_embed(int wdtype, const void* tok_emb, const void* pos_emb, int vocab, int n_pos, int d,
                         const int32_t* tokens, const int32_t* positions, const int32_t* seq_lens,
                         const int32_t* block_table, int max_pages, int n_pages, int B, float* x,
-                        int32_t* active, hipStream_t st);
+                        int32_t* active, float2* stats, uint32_t* zero, int n_zero, hipStream_t st);
 hipError_t launch_gemv(int wdtype, int epi, bool ln, const GemvArgs& a, hipStream_t st);
 bool gemv_supported(int wdtype, int K, bool ln);
 hipError_t launch_attn_decode(int wdtype, const AttnDecodeArgs& a, int B, hipStream_t st);
@@ -240,8 +262,8 @@ hipError_t launch_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens
                           int max_steps, int B, hipStream_t st);
 hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t st);
 hipError_t launch_bgemm(int wdtype, int epi, const BgemmArgs& a, hipStream_t st);
-int bgemm_splits(int wdtype, int N, int K);
-bool bgemm_supported(int wdtype, int K);
+int bgemm_splits(int wdtype, int N, int K, bool ln);
+bool bgemm_supported(int wdtype, int K, bool ln);
 hipError_t launch_act_to_f32(int wdtype, const void* src, int rows, int d, float* dst, hipStream_t st);
 
 namespace mega {

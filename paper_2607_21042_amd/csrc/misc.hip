@@ -15,8 +15,9 @@ __global__ __launch_bounds__(256) void embed_kernel(const void* tok_emb, const v
                                                     int n_pos, int d, const int32_t* tokens,
                                                     const int32_t* positions, const int32_t* seq_lens,
                                                     const int32_t* block_table, int max_pages, int n_pages,
-                                                    float* x, int32_t* active) {
-    const int b = blockIdx.x;
+                                                    float* x, int32_t* active, float2* stats, uint32_t* zero,
+                                                    int n_zero) {
+    const int b = blockIdx.x, B = gridDim.x;
     const int t = tokens[b], p = positions[b], s = seq_lens[b];
     bool ok = t >= 0 && t < vocab && p >= 0 && p < n_pos && s >= 0 && s < max_pages * kPage;
     if (ok) {
@@ -24,21 +25,32 @@ __global__ __launch_bounds__(256) void embed_kernel(const void* tok_emb, const v
         ok = phys >= 0 && phys < n_pages;
     }
     if (threadIdx.x == 0) active[b] = ok ? 1 : 0;
+    for (int i = b * 256 + threadIdx.x; i < n_zero; i += B * 256) zero[i] = 0u;
     float* xr = x + (size_t)b * d;
-    for (int k = threadIdx.x; k < d; k += blockDim.x)
-        xr[k] = ok ? ld_act<F32>(tok_emb, (size_t)t * d + k) + ld_act<F32>(pos_emb, (size_t)p * d + k) : 0.f;
+    // d is a multiple of 64, so every pass of this loop keeps whole waves active
+    for (int k = threadIdx.x; k < d; k += blockDim.x) {
+        const float v = ok ? ld_act<F32>(tok_emb, (size_t)t * d + k) + ld_act<F32>(pos_emb, (size_t)p * d + k) : 0.f;
+        xr[k] = v;
+        if (stats) {
+            const float2 ts = tile_stats32(v);
+            if ((k & (kStatTile - 1)) == 0) stats[(size_t)(k / kStatTile) * B + b] = ts;
+        }
+    }
 }
 
 hipError_t launch_embed(int wdtype, const void* tok_emb, const void* pos_emb, int vocab, int n_pos, int d,
                         const int32_t* tokens, const int32_t* positions, const int32_t* seq_lens,
                         const int32_t* block_table, int max_pages, int n_pages, int B, float* x,
-                        int32_t* active, hipStream_t st) {
+                        int32_t* active, float2* stats, uint32_t* zero, int n_zero, hipStream_t st) {
+    if (stats && d % 64 != 0) return hipErrorInvalidValue;
     if (wdtype == FTTS_F32)
         hipLaunchKernelGGL(embed_kernel<true>, dim3(B), dim3(256), 0, st, tok_emb, pos_emb, vocab, n_pos, d,
-                           tokens, positions, seq_lens, block_table, max_pages, n_pages, x, active);
+                           tokens, positions, seq_lens, block_table, max_pages, n_pages, x, active, stats, zero,
+                           n_zero);
     else
         hipLaunchKernelGGL(embed_kernel<false>, dim3(B), dim3(256), 0, st, tok_emb, pos_emb, vocab, n_pos, d,
-                           tokens, positions, seq_lens, block_table, max_pages, n_pages, x, active);
+                           tokens, positions, seq_lens, block_table, max_pages, n_pages, x, active, stats, zero,
+                           n_zero);
     return hipGetLastError();
 }
 
@@ -73,8 +85,55 @@ __global__ __launch_bounds__(256) void ln_rows_kernel(const float* x, const void
         st_act<F32>(out, r * d + k, (xr[k] - mean) * rstd * ld_act<F32>(g, k) + ld_act<F32>(bb, k));
 }
 
+// One wave per row for rows of up to 2048 columns that split into float4 lanes:
+// the row stays in registers, both reductions are cross-lane, no barriers.
+template <bool F32>
+__global__ __launch_bounds__(256) void ln_rows_wave_kernel(const float* x, const void* g, const void* bb, float eps,
+                                                           int M, int d, void* out) {
+    constexpr int NMAX = 8;  // float4 per lane: d <= 64 * 4 * 8
+    const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (r >= M) return;
+    const float4* xr = reinterpret_cast<const float4*>(x + (size_t)r * d);
+    const int n4 = d / 4;
+    float4 v[NMAX];
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < NMAX; ++i) {
+        const int j = lane + 64 * i;
+        v[i] = j < n4 ? xr[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+        s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+    }
+    const float mean = wave_sum(s) / (float)d;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < NMAX; ++i) {
+        if (lane + 64 * i < n4) {
+            const float a = v[i].x - mean, b = v[i].y - mean, c = v[i].z - mean, e = v[i].w - mean;
+            q = fmaf(a, a, fmaf(b, b, fmaf(c, c, fmaf(e, e, q))));
+        }
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + eps);
+#pragma unroll
+    for (int i = 0; i < NMAX; ++i) {
+        const int j = lane + 64 * i;
+        if (j < n4) {
+            const float xs[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                st_act<F32>(out, (size_t)r * d + 4 * j + k,
+                            (xs[k] - mean) * rstd * ld_act<F32>(g, 4 * j + k) + ld_act<F32>(bb, 4 * j + k));
+        }
+    }
+}
+
 hipError_t launch_ln_rows(int wdtype, const float* x, const void* g, const void* b, float eps, int M, int d,
                           void* out, hipStream_t st) {
+    if (d % 4 == 0 && d <= 2048) {
+        const dim3 grid((M + 3) / 4);
+        if (wdtype == FTTS_F32) hipLaunchKernelGGL(ln_rows_wave_kernel<true>, grid, dim3(256), 0, st, x, g, b, eps, M, d, out);
+        else hipLaunchKernelGGL(ln_rows_wave_kernel<false>, grid, dim3(256), 0, st, x, g, b, eps, M, d, out);
+        return hipGetLastError();
+    }
     if (wdtype == FTTS_F32) hipLaunchKernelGGL(ln_rows_kernel<true>, dim3(M), dim3(256), 0, st, x, g, b, eps, d, out);
     else hipLaunchKernelGGL(ln_rows_kernel<false>, dim3(M), dim3(256), 0, st, x, g, b, eps, d, out);
     return hipGetLastError();
@@ -118,35 +177,76 @@ hipError_t launch_act_to_f32(int wdtype, const void* src, int rows, int d, float
 }
 
 // ---- sampler ------------------------------------------------------------------------------
-// Winner of two (value, index) candidates: larger value, lower index on ties; NaN never wins.
+// One 256-thread workgroup per sequence; thread t holds the tempered logits of
+// indices t, t + 256, ... in registers.  Order is by (value, index): the larger
+// value first, the lower index on ties.  NaN logits count as -inf.
+//
+// Top-k without k sequential block reductions: each wave finds the k-th largest
+// of its 64 lane maxima, t_w; at least k entries are >= t_w, so with t = max_w t_w
+// every one of the k best entries is >= t.  The entries >= t (typically a few
+// times k) are compacted into LDS and each is ranked by counting the candidates
+// that beat it; ranks below k fill the ordered top-k list.  Rows with more than
+// kSampCand candidates (massive exact ties) take k rounds of block argmax instead.
+constexpr int kSampThreads = 256, kSampWaves = kSampThreads / kWave, kSampPer = 64;  // vocab <= 16384
+constexpr int kSampCand = 1024;
+
 __device__ __forceinline__ bool beats(float v, int i, float bv, int bi) {
     return v > bv || (v == bv && i < bi);
 }
 
-__device__ __forceinline__ void wave_best(float& v, int& i) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const float ov = __shfl_xor(v, o, kWave);
-        const int oi = __shfl_xor(i, o, kWave);
-        if (beats(ov, oi, v, i)) {
-            v = ov;
-            i = oi;
-        }
+template <int CTRL>
+__device__ __forceinline__ int dpp_mov_int(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+__device__ __forceinline__ int wave_min_int(int v) {
+    v = min(v, dpp_mov_int<kDppQuadSwap1>(v));
+    v = min(v, dpp_mov_int<kDppQuadSwap2>(v));
+    v = min(v, dpp_mov_int<kDppHalfMirror>(v));
+    v = min(v, dpp_mov_int<kDppMirror>(v));
+    {
+        const auto r = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+        v = min((int)r[0], (int)r[1]);
     }
+    {
+        const auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+        v = min((int)r[0], (int)r[1]);
+    }
+    return v;
 }
 
-// Block-wide best of every thread's candidate; all threads receive the winner.
+// Best (value, index) of the wave, in every lane: the largest value, then the
+// lowest index holding it.  Lanes with nothing to offer pass (-inf, INT_MAX).
+__device__ __forceinline__ void wave_best(float& v, int& i) {
+    const float m = wave_max(v);
+    i = wave_min_int(v == m ? i : INT_MAX);
+    v = m;
+}
+
+// Best untaken entry of this lane (indices increase with the slot, so the
+// first of equal values wins).
+__device__ __forceinline__ void lane_best(const float (&z)[kSampPer], uint64_t taken, float& bv, int& bi) {
+    bv = -INFINITY;
+    bi = INT_MAX;
+#pragma unroll
+    for (int j = 0; j < kSampPer; ++j)
+        if (!((taken >> j) & 1u) && (z[j] > bv || bi == INT_MAX)) {
+            bv = z[j];
+            bi = (int)threadIdx.x + kSampThreads * j;
+        }
+}
+
+// Block-wide best; every thread receives it.
 __device__ __forceinline__ void block_best(float& v, int& i, float* rv, int* ri) {
     wave_best(v, i);
-    const int w = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) {
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
         rv[w] = v;
         ri[w] = i;
     }
     __syncthreads();
     v = rv[0];
     i = ri[0];
-    for (int j = 1; j < 4; ++j)
+    for (int j = 1; j < kSampWaves; ++j)
         if (beats(rv[j], ri[j], v, i)) {
             v = rv[j];
             i = ri[j];
@@ -154,95 +254,142 @@ __device__ __forceinline__ void block_best(float& v, int& i, float* rv, int* ri)
     __syncthreads();
 }
 
-__global__ __launch_bounds__(256) void sample_kernel(const float* logits, int V, float temperature, int top_k,
-                                                     float top_p, const float* uniforms, const int32_t* active,
-                                                     int32_t* out) {
-    extern __shared__ float sz[];   // [V] tempered logits (top_k > 1)
-    __shared__ float rv[4];
-    __shared__ int ri[4];
+__global__ __launch_bounds__(kSampThreads) void sample_kernel(const float* logits, int V, float temperature,
+                                                              int top_k, float top_p, const float* uniforms,
+                                                              const int32_t* active, int32_t* out) {
+    __shared__ float cand_v[kSampCand];
+    __shared__ int cand_i[kSampCand];
     __shared__ float selv[FTTS_MAX_TOP_K];
     __shared__ int seli[FTTS_MAX_TOP_K];
-    const int b = blockIdx.x, tid = threadIdx.x;
+    __shared__ float rv[kSampWaves];
+    __shared__ int ri[kSampWaves];
+    __shared__ int s_cnt[kSampWaves];
+    const int b = blockIdx.x, tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
     if (active && !active[b]) {
         if (tid == 0) out[b] = -1;
         return;
     }
     const float* row = logits + (size_t)b * V;
-    if (top_k == 1) {
-        float bv = -INFINITY;
-        int bi = INT_MAX;
-        for (int i = tid; i < V; i += 256) {
-            const float v = row[i];
-            if (beats(v, i, bv, bi)) {
-                bv = v;
-                bi = i;
-            }
-        }
+    const bool greedy = top_k == 1;
+    float z[kSampPer];
+#pragma unroll
+    for (int j = 0; j < kSampPer; ++j) {
+        const int i = tid + kSampThreads * j;
+        float v = i < V ? row[i] : -INFINITY;
+        v = greedy ? v : v / temperature;
+        z[j] = v != v ? -INFINITY : v;
+    }
+    if (greedy) {
+        float bv;
+        int bi;
+        lane_best(z, 0, bv, bi);
         block_best(bv, bi, rv, ri);
         if (tid == 0) out[b] = bi < V ? bi : 0;
         return;
     }
-    for (int i = tid; i < V; i += 256) sz[i] = row[i] / temperature;
-    __syncthreads();
-    // Each thread keeps the best of its own (strided) indices; taken entries become NaN.
-    float cv = -INFINITY;
-    int ci = INT_MAX;
-    for (int i = tid; i < V; i += 256)
-        if (beats(sz[i], i, cv, ci)) {
-            cv = sz[i];
-            ci = i;
-        }
-    for (int r = 0; r < top_k; ++r) {
-        float wv = cv;
-        int wi = ci;
-        block_best(wv, wi, rv, ri);
-        if (tid == 0) {
-            selv[r] = wv;
-            seli[r] = wi;
-        }
-        if (wi == ci && ci < V) {  // this thread owned the winner: drop it and rescan
-            sz[wi] = __int_as_float(0x7FC00000);
-            cv = -INFINITY;
-            ci = INT_MAX;
-            for (int i = tid; i < V; i += 256)
-                if (beats(sz[i], i, cv, ci)) {
-                    cv = sz[i];
-                    ci = i;
-                }
-        }
+    // wave threshold: the k-th largest lane maximum (ties: lower lane first)
+    float lm = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kSampPer; ++j) lm = fmaxf(lm, z[j]);
+    int rank = 0;
+#pragma unroll
+    for (int l = 0; l < kWave; ++l) {
+        const float o = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lm), l));
+        rank += (o > lm || (o == lm && l < lane)) ? 1 : 0;
     }
+    const uint64_t hit = __ballot(rank == top_k - 1);
+    const float tw = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lm), (int)__builtin_ctzll(hit)));
+    if (lane == 0) rv[wave] = tw;
     __syncthreads();
-    if (tid == 0) {
-        // Sequential fp32 part: weights, running sums, nucleus cut, inverse-CDF draw.
-        const float z1 = selv[0];
-        float acc = 0.f;
-        for (int i = 0; i < top_k; ++i) {
-            acc = acc + expf(selv[i] - z1);
-            selv[i] = acc;  // cumulative sums replace the values
-        }
-        const float thresh = top_p * selv[top_k - 1];
-        int n = top_k;
-        for (int i = 0; i < top_k; ++i)
-            if (selv[i] >= thresh) {
-                n = i + 1;
-                break;
-            }
-        const float rr = uniforms[b] * selv[n - 1];
-        int j = n - 1;
-        for (int i = 0; i < n; ++i)
-            if (selv[i] > rr) {
-                j = i;
-                break;
-            }
-        out[b] = seli[j] < V ? seli[j] : 0;
+    float t = rv[0];
+    for (int w = 1; w < kSampWaves; ++w) t = fmaxf(t, rv[w]);
+    // candidates: count, exclusive offsets (wave scan, then wave totals), compaction
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < kSampPer; ++j) cnt += z[j] >= t ? 1 : 0;
+    int incl = cnt;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int u = __shfl_up(incl, o, kWave);
+        incl += lane >= o ? u : 0;
     }
+    if (lane == kWave - 1) s_cnt[wave] = incl;
+    __syncthreads();
+    int off = incl - cnt, total = 0;
+    for (int w = 0; w < kSampWaves; ++w) {
+        off += w < wave ? s_cnt[w] : 0;
+        total += s_cnt[w];
+    }
+    if (total <= kSampCand) {
+#pragma unroll
+        for (int j = 0; j < kSampPer; ++j)
+            if (z[j] >= t) {
+                cand_v[off] = z[j];
+                cand_i[off] = tid + kSampThreads * j;
+                ++off;
+            }
+        __syncthreads();
+        for (int c = tid; c < total; c += kSampThreads) {
+            const float cv = cand_v[c];
+            const int ci = cand_i[c];
+            int r = 0;
+            for (int c2 = 0; c2 < total; ++c2) r += beats(cand_v[c2], cand_i[c2], cv, ci) ? 1 : 0;
+            if (r < top_k) {
+                selv[r] = cv;
+                seli[r] = ci;
+            }
+        }
+        __syncthreads();
+    } else {
+        uint64_t taken = 0;
+        float bv;
+        int bi;
+        lane_best(z, taken, bv, bi);
+        for (int r = 0; r < top_k; ++r) {
+            float wv = bv;
+            int wi = bi;
+            block_best(wv, wi, rv, ri);
+            if (tid == 0) {
+                selv[r] = wv;
+                seli[r] = wi;
+            }
+            if (wi == bi && (wi - tid) % kSampThreads == 0) {  // this thread held the winner
+                taken |= 1ull << ((wi - tid) / kSampThreads);
+                lane_best(z, taken, bv, bi);
+            }
+        }
+        __syncthreads();
+    }
+    if (tid != 0) return;
+    // Sequential fp32 part: weights, running sums, nucleus cut, inverse-CDF draw.
+    const float z1 = selv[0];
+    float acc = 0.f;
+    for (int i = 0; i < top_k; ++i) {
+        acc = acc + expf(selv[i] - z1);
+        selv[i] = acc;  // cumulative sums replace the values
+    }
+    const float thresh = top_p * selv[top_k - 1];
+    int n = top_k;
+    for (int i = 0; i < top_k; ++i)
+        if (selv[i] >= thresh) {
+            n = i + 1;
+            break;
+        }
+    const float rr = uniforms[b] * selv[n - 1];
+    int j = n - 1;
+    for (int i = 0; i < n; ++i)
+        if (selv[i] > rr) {
+            j = i;
+            break;
+        }
+    out[b] = seli[j] < V ? seli[j] : 0;
 }
 
 hipError_t launch_sample(const float* logits, int B, int V, const ftts_sampling& s, const float* uniforms,
                          const int32_t* active, int32_t* out, hipStream_t st) {
-    const size_t lds = s.top_k == 1 ? 0 : (size_t)V * sizeof(float);
-    hipLaunchKernelGGL(sample_kernel, dim3(B), dim3(256), lds, st, logits, V, s.temperature, s.top_k, s.top_p,
-                       uniforms, active, out);
+    if (V > kSampThreads * kSampPer || s.top_k < 1 || s.top_k > FTTS_MAX_TOP_K) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(sample_kernel, dim3(B), dim3(kSampThreads), 0, st, logits, V, s.temperature, s.top_k,
+                       s.top_p, uniforms, active, out);
     return hipGetLastError();
 }
 

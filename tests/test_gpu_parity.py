@@ -129,6 +129,8 @@ def test_sampler_matches_oracle(torch_cuda):
     logits[:8, 100:110] = logits[:8, 100:101]       # exact ties across several indices
     logits[8:16, :] = np.float32(-1.0)
     logits[8:16, 7] = 5.0
+    logits[16:24, :] = np.float32(0.25)              # the whole row tied: lowest indices win
+    logits[24:32, 3000:] = -np.inf                   # masked tail
     us = workload.uniforms(1, B, seed=42)[0]
     lt = torch.from_numpy(logits).cuda()
     ut = torch.from_numpy(us).cuda()
