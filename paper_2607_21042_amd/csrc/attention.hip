@@ -11,9 +11,15 @@
 // are merged in LDS with the log-sum-exp rule.  The walk follows logical
 // pages, so the result does not depend on where pages live in the pool.
 //
-// Prefill (causal attention over each prefix, queries in tiles of 64): one
-// thread per query row keeps q and the output in registers and streams 64-key
-// tiles of K and V through LDS.
+// Prefill (causal attention over each prefix).  16-bit activations run on the
+// matrix cores: a workgroup of 4 waves takes 128 queries of one head, each wave
+// 32 of them, and walks 32-key tiles.  A wave forms S^T = K Q^T (keys as rows,
+// so every lane ends up holding 16 scores of its own query), applies the online
+// softmax per lane, and accumulates O^T = V^T P^T with the probabilities taken
+// straight from its score registers: the MFMA k order is a permutation shared by
+// both operands, so P needs no reshuffle.  V is transposed through LDS (double
+// buffered, one barrier per tile).  fp32 activations keep a VALU kernel: one
+// thread per query row streams 64-key tiles of K and V through LDS.
 #include "kv_page.hpp"
 
 namespace ftts {
@@ -249,10 +255,148 @@ __global__ __launch_bounds__(64) void attn_prefill_kernel(const AttnPrefillArgs 
         st_act<F32>(a.o, (size_t)(row0 + qi) * a.d_model + h * kHeadDim + j, o[j] * inv);
 }
 
+typedef __bf16 pf_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float pf_f32x16 __attribute__((ext_vector_type(16)));
+constexpr int kPfWaves = 4, kPfQ = kPfWaves * 32;  // queries per workgroup
+constexpr int kPfK = 32;                           // keys per tile
+constexpr int kVtStride = kPfK + 8;                // bf16 per transposed-V row (one head dim)
+
+__device__ __forceinline__ pf_bf16x8 pf_op(uint4 v) { return __builtin_bit_cast(pf_bf16x8, v); }
+
+__global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const AttnPrefillArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t vt[2][kHeadDim][kVtStride];
+    const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int gt = blockIdx.x, sq = 0;
+    while (sq + 1 < a.seqs.n && a.tiles_cu[sq + 1] <= gt) ++sq;
+    const int tile = gt - a.tiles_cu[sq];
+    const int row0 = a.seqs.cu[sq], len = a.seqs.cu[sq + 1] - row0;
+    if (len <= 0) return;
+    const size_t ld = 3 * (size_t)a.d_model;
+    const uint16_t* qkv = reinterpret_cast<const uint16_t*>(a.qkv);
+    const int ql = lane & 31, hh = lane >> 5;
+    const int qw = tile * kPfQ + wave * 32;  // this wave's first query
+    const int qi = qw + ql;                  // this lane's query (a column of S^T)
+    // exp2 domain: scores scaled by 1/sqrt(64) * log2(e)
+    const float kScale = 0.125f * 1.44269504088896340736f;
+
+    // Q as the B operand of S^T = K Q^T: lane (q, hh) holds dims kk*16 + hh*8 .. +7.
+    uint4 qr[4];
+    {
+        const uint16_t* qrow = qkv + (size_t)(row0 + min(qi, len - 1)) * ld + h * kHeadDim;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qr[kk] = *reinterpret_cast<const uint4*>(qrow + kk * 16 + hh * 8);
+    }
+    // V tile staging: thread t carries key t / 8, dims (t % 8) * 8 .. +7.
+    const int vkey = tid >> 3, vd0 = (tid & 7) * 8;
+    auto load_v = [&](int t) {
+        const int key = min(t * kPfK + vkey, len - 1);
+        return *reinterpret_cast<const uint4*>(qkv + (size_t)(row0 + key) * ld + 2 * a.d_model + h * kHeadDim + vd0);
+    };
+    auto store_v = [&](uint4 v, int buf) {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            vt[buf][vd0 + 2 * i][vkey] = (uint16_t)(w[i] & 0xFFFFu);
+            vt[buf][vd0 + 2 * i + 1][vkey] = (uint16_t)(w[i] >> 16);
+        }
+    };
+
+    pf_f32x16 o0, o1;  // O^T, dims 0..31 and 32..63: o[i] is dim (i/4)*8 + hh*4 + i%4 of query qi
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o0[i] = o1[i] = 0.f;
+    float m = -INFINITY, l = 0.f;
+    const int kend = min(len, tile * kPfQ + kPfQ);  // keys any query of this workgroup sees
+    const int ntiles = (kend + kPfK - 1) / kPfK;
+    store_v(load_v(0), 0);
+    __syncthreads();
+    for (int t = 0; t < ntiles; ++t) {
+        const int buf = t & 1, k0 = t * kPfK;
+        uint4 vnext = make_uint4(0, 0, 0, 0);
+        if (t + 1 < ntiles) vnext = load_v(t + 1);
+        if (k0 <= qw + 31 && qw < len) {  // some query of this wave sees a key of this tile
+            // K as the A operand: lane (key k0 + ql, hh) holds dims kk*16 + hh*8 .. +7
+            const uint16_t* krow = qkv + (size_t)(row0 + min(k0 + ql, len - 1)) * ld + a.d_model + h * kHeadDim;
+            uint4 kr[4];
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) kr[kk] = *reinterpret_cast<const uint4*>(krow + kk * 16 + hh * 8);
+            pf_f32x16 s;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) s[i] = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(kr[kk]), pf_op(qr[kk]), s, 0, 0, 0);
+            // s[i]: key k0 + (i/4)*8 + hh*4 + i%4 of query qi; causal and length masks
+            float tmax = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int key = k0 + (i >> 2) * 8 + hh * 4 + (i & 3);
+                s[i] = key <= qi && key < len ? s[i] * kScale : -INFINITY;
+                tmax = fmaxf(tmax, s[i]);
+            }
+            {
+                const RowPair pr = swap32(tmax);  // the other 16 keys of this query
+                tmax = fmaxf(pr.a, pr.b);
+            }
+            const float mn = fmaxf(m, tmax);
+            const float ms = mn == -INFINITY ? 0.f : mn;
+            const float alpha = exp2f(m - ms);
+            m = mn;
+            // probabilities, rounded to bf16 once: the same values feed P V and the row sum
+            uint32_t pw[8];
+            float rs = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; i += 2) {
+                const uint16_t lo = f32_to_bf16(exp2f(s[i] - ms)), hi = f32_to_bf16(exp2f(s[i + 1] - ms));
+                rs += bf16_to_f32(lo) + bf16_to_f32(hi);
+                pw[i / 2] = (uint32_t)lo | ((uint32_t)hi << 16);
+            }
+            {
+                const RowPair pr = swap32(rs);
+                rs = pr.a + pr.b;
+            }
+            l = l * alpha + rs;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                o0[i] *= alpha;
+                o1[i] *= alpha;
+            }
+            // O^T += V^T P^T.  k slots hh*8 .. +7 of step st carry keys
+            // st*16 + hh*4 + 0..3 and st*16 + 8 + hh*4 + 0..3 on both operands.
+#pragma unroll
+            for (int st2 = 0; st2 < 2; ++st2) {
+                const pf_bf16x8 pb = pf_op(make_uint4(pw[4 * st2], pw[4 * st2 + 1], pw[4 * st2 + 2], pw[4 * st2 + 3]));
+                const int c = st2 * 16 + hh * 4;
+                const uint2 a0 = *reinterpret_cast<const uint2*>(&vt[buf][ql][c]);
+                const uint2 a1 = *reinterpret_cast<const uint2*>(&vt[buf][ql][c + 8]);
+                const uint2 b0 = *reinterpret_cast<const uint2*>(&vt[buf][32 + ql][c]);
+                const uint2 b1 = *reinterpret_cast<const uint2*>(&vt[buf][32 + ql][c + 8]);
+                o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(make_uint4(a0.x, a0.y, a1.x, a1.y)), pb, o0, 0, 0, 0);
+                o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(make_uint4(b0.x, b0.y, b1.x, b1.y)), pb, o1, 0, 0, 0);
+            }
+        }
+        if (t + 1 < ntiles) store_v(vnext, buf ^ 1);  // that buffer was last read before the previous barrier
+        __syncthreads();
+    }
+    if (qi >= len) return;
+    const float inv = 1.0f / l;
+    uint16_t* orow = reinterpret_cast<uint16_t*>(a.o) + (size_t)(row0 + qi) * a.d_model + h * kHeadDim;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const int dd = g * 8 + hh * 4;
+        *reinterpret_cast<uint2*>(orow + dd) =
+            make_uint2((uint32_t)f32_to_bf16(o0[4 * g] * inv) | ((uint32_t)f32_to_bf16(o0[4 * g + 1] * inv) << 16),
+                       (uint32_t)f32_to_bf16(o0[4 * g + 2] * inv) | ((uint32_t)f32_to_bf16(o0[4 * g + 3] * inv) << 16));
+        *reinterpret_cast<uint2*>(orow + 32 + dd) =
+            make_uint2((uint32_t)f32_to_bf16(o1[4 * g] * inv) | ((uint32_t)f32_to_bf16(o1[4 * g + 1] * inv) << 16),
+                       (uint32_t)f32_to_bf16(o1[4 * g + 2] * inv) | ((uint32_t)f32_to_bf16(o1[4 * g + 3] * inv) << 16));
+    }
+}
+
+int prefill_tile_rows(int wdtype) { return wdtype == FTTS_F32 ? 64 : kPfQ; }
+
 hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_tiles, hipStream_t st) {
     const dim3 g(total_tiles, a.n_head);
     if (wdtype == FTTS_F32) hipLaunchKernelGGL(attn_prefill_kernel<true>, g, dim3(64), 0, st, a);
-    else hipLaunchKernelGGL(attn_prefill_kernel<false>, g, dim3(64), 0, st, a);
+    else hipLaunchKernelGGL(attn_prefill_mfma_kernel, g, dim3(kPfWaves * 64), 0, st, a);
     return hipGetLastError();
 }
 

@@ -621,7 +621,7 @@ int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* l
         M += lens[b];
         if (M > (1 << 24)) return fail(FTTS_E_RANGE, "total prefix rows too large");
         seqs.cu[b + 1] = (int)M;
-        ap.tiles_cu[b + 1] = ap.tiles_cu[b] + (lens[b] + 63) / 64;
+        ap.tiles_cu[b + 1] = ap.tiles_cu[b] + (lens[b] + prefill_tile_rows(c.wdtype) - 1) / prefill_tile_rows(c.wdtype);
     }
     const size_t need = prefill_bytes(c, B, (int)M, nullptr, nullptr);
     if (ws_bytes < need) return fail(FTTS_E_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);

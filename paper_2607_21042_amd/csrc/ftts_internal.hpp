@@ -237,7 +237,7 @@ struct AttnPrefillArgs {
     void* o;                 // [M][d] activation dtype
     int d_model, n_head;
     SeqTable seqs;
-    int tiles_cu[kMaxPrefillSeqs + 1];  // prefix sums of 64-row query tiles per sequence
+    int tiles_cu[kMaxPrefillSeqs + 1];  // prefix sums of query tiles (prefill_tile_rows) per sequence
 };
 
 // ---- launchers (each returns a hipError_t from the launch) --------------------------
@@ -256,6 +256,7 @@ hipError_t launch_ln_rows(int wdtype, const float* x, const void* g, const void*
                           void* out, hipStream_t st);
 hipError_t launch_gemm(int wdtype, int epi, const GemmArgs& a, hipStream_t st);
 hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_tiles, hipStream_t st);
+int prefill_tile_rows(int wdtype);  // queries per prefill-attention workgroup
 hipError_t launch_gather_rows(const float* x, int d, const SeqTable& seqs, float* out, hipStream_t st);
 hipError_t launch_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled,
                           int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,

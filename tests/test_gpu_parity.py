@@ -246,6 +246,27 @@ def test_ragged_batch_and_page_placement(torch_cuda, mode):
     del torch
 
 
+@pytest.mark.parametrize("mode", ["bf16", "w8a16"])
+def test_prefill_lengths_across_attention_tiles(torch_cuda, mode):
+    """Prefix lengths on both sides of the prefill attention's 32-key and
+    128-query tile edges; the prefill logits and two decode steps over the
+    cache it wrote match the oracle."""
+    from paper_2607_21042_amd import ftts
+    shape = workload.TINY
+    inputs = model_inputs(shape, mode, workload.master_weights(shape, seed=0))
+    lens = [31, 32, 33, 127, 128, 129, 257]
+    flat = workload.prefix_embeddings(lens, shape.d_model, seed=5, bf16=True)
+    prefixes = np.split(flat, np.cumsum(lens)[:-1])
+    fed = workload.random_tokens(2, len(lens), shape.vocab, seed=6)
+    fed[0, :] = shape.start_token
+    om = ogpt.GPT(helpers.oracle_weights(inputs, mode), shape.n_head, shape.d_head, dtype=np.float32)
+    say(f"prefill tile edges {mode}")
+    dm = ftts.DeviceModel(inputs, shape, wd(mode))
+    res = helpers.run_gpu(dm, shape, prefixes, fed)
+    worst, _ = compare_run(res, om, prefixes, fed, mode, check_sampled=False)
+    say(f"  worst err {worst:.3g}")
+
+
 @pytest.mark.parametrize("mode,B", [("bf16", 33), ("w8a16", 8), ("w4a16", 33)])
 def test_batched_decode_matrix_core_linears(torch_cuda, mode, B):
     """Batches of 8 or more take the MFMA linears (33 = a full group of 32 plus a
