@@ -131,6 +131,23 @@ def cpu_baseline(inputs, shape, mode, prefix, n_steps):
                       f"numpy fp32 oracle on the same {mode} weights"}
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
+
+
+def prefill_report(shape, lens, ms):
+    """Prefill throughput against the dense bf16 matrix peak: the four linears
+    of every layer over all prefix rows, causal attention (Q K^T and P V over
+    the lower triangle) and the LM head on each sequence's last row."""
+    d, F, H = shape.d_model, shape.d_ff, shape.n_head
+    rows = int(sum(lens))
+    lin = 2 * rows * (3 * d * d + d * d + 2 * d * F)
+    att = sum(2 * 2 * (int(p) * (int(p) + 1) // 2) * shape.d_head * H for p in lens)
+    flops = shape.n_layer * (lin + att) + 2 * len(lens) * d * shape.vocab
+    tflops = flops / (ms / 1e3) / 1e12
+    return {"ms": round(ms, 3), "rows": rows, "gflop": round(flops / 1e9, 1), "tflops": round(tflops, 1),
+            "peak_tflops": MFMA_BF16_PEAK_TFLOPS, "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4)}
+
+
 def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
     """The batched paged workload: one job = ragged prefill of every sequence, then
     decode steps until every sequence has produced its target length (the last
@@ -172,13 +189,17 @@ def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
     P_dev = torch.from_numpy(P).cuda()
     T_dev = torch.from_numpy(Tt).cuda()
 
-    def reset_and_prefill():
+    def reset_and_prefill(pev=None):
         tokens.fill_(shape.start_token)
         positions.zero_()
         seq_lens.copy_(P_dev)
         remaining.copy_(T_dev)
         counter.zero_()
+        if pev is not None:
+            pev[0].record(torch.cuda.current_stream())
         ftts.prefill(dm, prefix, P.tolist(), pt, kv, last, ws)
+        if pev is not None:
+            pev[1].record(torch.cuda.current_stream())
 
     def step(t):
         ftts.decode_step(dm, tokens, positions, pt, kv, logits, sampled, uni[t], samp, ws)
@@ -210,12 +231,13 @@ def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
         graph.replay()
     torch.cuda.synchronize()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    pevs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     wall0 = time.perf_counter()
     t0.record(stream)
     for k in range(args.steps):
-        reset_and_prefill()
+        reset_and_prefill(pevs[k])
         evs[k][0].record(stream)
         graph.replay()
         evs[k][1].record(stream)
@@ -248,6 +270,7 @@ def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
         "decode_tokens_per_s": round(n_tok / (decode_ms / 1e3), 2),
         "decode_ms_per_step": round(decode_ms / T_max, 4),
         "prefill_ms": round(job_ms - decode_ms, 3),
+        "prefill": prefill_report(shape, P, float(np.mean([a.elapsed_time(b) for a, b in pevs]))),
         "wall_s": round(wall, 3),
         "roofline": {"bound": "hbm", "kernel": f"decode step, kernel per phase ({T_max} steps, 32 per HIP graph)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -343,9 +366,13 @@ def main():
                 step_advance()
         torch.cuda.synchronize()
 
-    def job(evs=None):
+    def job(evs=None, pev=None):
         reset()
+        if pev is not None:
+            pev[0].record(stream)
         ftts.prefill(dm, prefix, [P] * B, pt, kv, last, ws)
+        if pev is not None:
+            pev[1].record(stream)
         if persistent:
             for t in range(T):
                 if evs is not None:
@@ -368,13 +395,14 @@ def main():
     n_units = T if persistent else T // S
     evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_units)]
            for _ in range(args.steps)]
+    pevs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t_start.record(stream)
     for k in range(args.steps):
-        job(evs[k])
+        job(evs[k], pevs[k])
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -406,6 +434,7 @@ def main():
                    "decode_path": "persistent" if persistent else "kernel-per-phase"},
         "decode_ms_per_token_step": round(decode_ms / T, 4),
         "prefill_ms": round(job_ms - decode_ms, 3),
+        "prefill": prefill_report(shape, [P] * B, float(np.mean([a.elapsed_time(b) for a, b in pevs]))),
         "wall_s": round(wall, 3),
         "roofline": {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),

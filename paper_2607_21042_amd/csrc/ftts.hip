@@ -149,6 +149,8 @@ struct PrefillWs {
     void* h;         // [M][d_ff]
     float* xlast;    // [B][d]
     int32_t* active; // [B] all ones (head GEMV reads no flags; kept for symmetry)
+    float* part;     // split-K partial tiles of the GEMMs (16-bit modes, short prefixes)
+    uint32_t* count; // their per-tile arrival counters
 };
 
 // The persistent decode step's control words and exchange buffers sit at the
@@ -223,6 +225,32 @@ size_t decode_bytes(const ftts_config& c, int B, DecodeWs* out, char* base) {
     return off;
 }
 
+// Split-K scratch of the prefill GEMMs for any row count up to M: the largest
+// S * rows * N partial buffer and the largest tile count (the split depends on
+// the row count, and a smaller call may split where a larger one does not).
+void gemm_scratch(const ftts_config& c, int M, size_t* part_floats, size_t* counters) {
+    size_t pf = 0, cn = 0;
+    if (c.wdtype != FTTS_F32 && M > 0) {
+        const int d = c.d_model, F = c.d_ff;
+        const int NK[4][2] = {{3 * d, d}, {d, d}, {F, d}, {d, F}};
+        for (int step = 64;; step += 64) {
+            const int rows = std::min(step, M);
+            bool split = false;
+            for (const auto& t : NK) {
+                const GemmPlan p = gemm_plan(rows, t[0], t[1]);
+                if (p.splits > 1) {
+                    split = true;
+                    pf = std::max(pf, (size_t)p.splits * rows * t[0]);
+                    cn = std::max(cn, (size_t)p.tiles_m * p.tiles_n);
+                }
+            }
+            if (rows >= M || !split) break;  // more rows only add tiles
+        }
+    }
+    *part_floats = pf;
+    *counters = cn;
+}
+
 size_t prefill_bytes(const ftts_config& c, int B, int M, PrefillWs* out, char* base) {
     const size_t e = act_bytes(c);
     size_t off = mega_bytes(nullptr, nullptr);
@@ -233,7 +261,11 @@ size_t prefill_bytes(const ftts_config& c, int B, int M, PrefillWs* out, char* b
     char* h = take((size_t)M * c.d_ff * e);
     char* xl = take((size_t)B * c.d_model * 4);
     char* act = take((size_t)B * 4);
-    if (out) *out = PrefillWs{(float*)x, a, qkv, h, (float*)xl, (int32_t*)act};
+    size_t pf, cn;
+    gemm_scratch(c, M, &pf, &cn);
+    char* part = pf ? take(pf * 4) : nullptr;
+    char* count = cn ? take(cn * 4) : nullptr;
+    if (out) *out = PrefillWs{(float*)x, a, qkv, h, (float*)xl, (int32_t*)act, (float*)part, (uint32_t*)count};
     return off;
 }
 
@@ -634,6 +666,11 @@ int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* l
     (void)hipGetLastError();
     hipError_t e = launch_act_to_f32(c.wdtype, prefix_emb, Mi, d, P.x, st);
     if (e != hipSuccess) return hip_fail(e, "prefix copy");
+    if (P.count) {
+        size_t pf, cn;
+        gemm_scratch(c, Mi, &pf, &cn);
+        if ((e = launch_fill_u32(P.count, cn, 0u, st)) != hipSuccess) return hip_fail(e, "gemm counters");
+    }
 
     KvAppend kva{};
     kva.base = kv->base;
@@ -654,6 +691,8 @@ int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* l
         if ((e = launch_ln_rows(c.wdtype, P.x, L.ln1_g, L.ln1_b, c.ln_eps, Mi, d, P.a, st)) != hipSuccess)
             return hip_fail(e, "ln1");
         GemmArgs g{};
+        g.part = P.part;
+        g.count = P.count;
         g.a = P.a;
         g.w = L.qkv.w;
         g.scale = (const uint16_t*)L.qkv.scale;

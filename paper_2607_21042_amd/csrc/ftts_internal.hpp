@@ -230,7 +230,14 @@ struct GemmArgs {
     void* out;               // STORE/QKV/GELU: [M][N] activation dtype; RESID: fp32 [M][N] in place
     KvAppend kv;             // QKV epilogue (prefill form: slot = position within the sequence)
     SeqTable seqs;
+    float* part;             // split K: [S][M][N] fp32 partial tiles
+    uint32_t* count;         // split K: per-tile arrival counters, zero between calls
 };
+struct GemmPlan {            // 16-bit-mode prefill GEMM launch shape
+    int mt;                  // 64-row blocks per tile (1 or 2)
+    int tiles_m, tiles_n, splits;
+};
+GemmPlan gemm_plan(int M, int N, int K);
 
 struct AttnPrefillArgs {
     const void* qkv;         // [M][3d] activation dtype
