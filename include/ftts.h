@@ -250,6 +250,25 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
                      int32_t B, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * ftts_decode_step that also hands out the step's last-layer hidden state,
+ * which the model's mel stage takes as a condition next to the semantic tokens
+ * (Sec. II-A; yielding it per step is the fourth serving adaptation of Sec.
+ * II-C).
+ *   hidden_out  [B][d_model] fp32, 16-byte aligned: row b is LN_f of sequence
+ *               b's new last-layer row, i.e. exactly the input the LM head
+ *               multiplies (fp32, before any rounding to the activation dtype).
+ *               Rows of inactive slots are unspecified.  NULL is allowed and
+ *               makes the call identical to ftts_decode_step.
+ * Every other argument, the errors and the graph-capture safety are those of
+ * ftts_decode_step; FTTS_E_ALIGN if hidden_out is misaligned.
+ */
+int ftts_decode_step_hidden(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
+                            const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out,
+                            float* hidden_out, int32_t* sampled_out, const float* uniforms,
+                            const ftts_sampling* samp, int32_t B, void* ws, size_t ws_bytes,
+                            void* stream);
+
+/*
  * Bookkeeping between two decode steps, done on the device so that a step can
  * be replayed from a captured HIP graph with fixed pointers (the generation loop
  * of the serving engine: one token per sequence per step, Sec. II-C).  For each

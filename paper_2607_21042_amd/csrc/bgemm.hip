@@ -279,6 +279,11 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
                     const float t = (xs[e] - mean) * rstd * gs[e] + bs[e];
                     y[e] = live ? t : 0.f;
                 }
+                if (p.hidden && f == 0 && live) {  // feature tile 0 of each slice covers the slice's columns
+                    float4* hd = reinterpret_cast<float4*>(p.hidden + (size_t)fr * p.K + k0 + kl + 8 * i);
+                    hd[0] = make_float4(y[0], y[1], y[2], y[3]);
+                    hd[1] = make_float4(y[4], y[5], y[6], y[7]);
+                }
                 ch[j].a[i] = make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
                                         pack_bf16x2(y[6], y[7]));
             }
@@ -454,6 +459,7 @@ hipError_t launch_bgemm(int wdtype, int epi, const BgemmArgs& in, hipStream_t st
         a.B = in.B - b0 < kBgemmRows ? in.B - b0 : kBgemmRows;
         if (in.act) a.act = reinterpret_cast<const uint16_t*>(in.act) + (size_t)b0 * in.K;
         if (in.ln_x) a.ln_x = in.ln_x + (size_t)b0 * in.K;
+        if (in.hidden) a.hidden = in.hidden + (size_t)b0 * in.K;
         if (in.ln_stats) a.ln_stats = in.ln_stats + b0;
         if (in.stats_out) a.stats_out = in.stats_out + b0;
         if (in.out) a.out = in.out + (size_t)b0 * in.out_stride;

@@ -826,6 +826,10 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
     layer_norm<BMAX, false>(s_x, s_in, s_xs, ln, a.eps, B);
     bar();  // s_in complete; the copy wave has waited for the head share
     MEGA_MARK(2 + a.n_layer * kMarksPerLayer);
+    if (a.hidden && wg == 0) {  // the step's last-layer hidden state (every group holds the same rows)
+        for (int i = tid; i < B * D / 4; i += NC)
+            reinterpret_cast<float4*>(a.hidden)[i] = reinterpret_cast<const float4*>(s_in)[i];
+    }
     {
         float acc[BMAX];
         ph.template dot<BMAX>(s_in, s_xs, B, acc);

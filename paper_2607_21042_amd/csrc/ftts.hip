@@ -357,8 +357,8 @@ GemvArgs gemv_args(const ftts_linear& L, int N, int K, int B, const float* act, 
 // residual updates leave per-tile row statistics behind).  Attention writes bf16
 // for the out-projection and FC1's GELU output is bf16 for FC2.
 int decode_batched(const ftts_weights* w, int B, const DecodeWs& W, const KvAppend& kva, AttnDecodeArgs at,
-                   float* logits_out, int32_t* sampled_out, const float* uniforms, const ftts_sampling* samp,
-                   hipStream_t st) {
+                   float* logits_out, float* hidden_out, int32_t* sampled_out, const float* uniforms,
+                   const ftts_sampling* samp, hipStream_t st) {
     const ftts_config& c = w->cfg;
     const int d = c.d_model, F = c.d_ff, V = c.vocab;
     hipError_t e;
@@ -407,6 +407,7 @@ int decode_batched(const ftts_weights* w, int B, const DecodeWs& W, const KvAppe
         if ((e = launch_bgemm(c.wdtype, EPI_RESID, g, st)) != hipSuccess) return hip_fail(e, "fc2");
     }
     BgemmArgs g = normed(lin(w->head, V, d, nullptr, logits_out, nullptr, V), w->lnf_g, w->lnf_b);
+    g.hidden = hidden_out;
     if ((e = launch_bgemm(c.wdtype, EPI_STORE, g, st)) != hipSuccess) return hip_fail(e, "ln_f + lm head");
     if ((e = launch_sample(logits_out, B, V, *samp, uniforms, W.active, sampled_out, st)) != hipSuccess)
         return hip_fail(e, "sampler");
@@ -510,11 +511,12 @@ int ftts_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t
     return FTTS_OK;
 }
 
-int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
-                     const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out, int32_t* sampled_out,
-                     const float* uniforms, const ftts_sampling* samp, int32_t B, void* ws, size_t ws_bytes,
-                     void* stream) {
+static int decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
+                       const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out, float* hidden_out,
+                       int32_t* sampled_out, const float* uniforms, const ftts_sampling* samp, int32_t B, void* ws,
+                       size_t ws_bytes, void* stream) {
     TRY(check_weights(w));
+    if (reinterpret_cast<uintptr_t>(hidden_out) % 16) return fail(FTTS_E_ALIGN, "hidden_out must be 16-byte aligned");
     const ftts_config& c = w->cfg;
     if (B < 1 || B > FTTS_MAX_BATCH) return fail(FTTS_E_SHAPE, "B must be in [1, %d]", FTTS_MAX_BATCH);
     if (!tokens || !positions) return fail(FTTS_E_INVALID_ARG, "tokens/positions is NULL");
@@ -549,6 +551,7 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
         ma.block_table = pt->block_table;
         ma.kv = kv->base;
         ma.logits = logits_out;
+        ma.hidden = hidden_out;
         ma.sampled = sampled_out;
         ma.active_out = W.active;
         ma.ex_x = M.x;
@@ -597,7 +600,7 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
     at.active = W.active;
     at.o = W.o;
     at.o_stride = d;
-    if (W.stats) return decode_batched(w, B, W, kva, at, logits_out, sampled_out, uniforms, samp, st);
+    if (W.stats) return decode_batched(w, B, W, kva, at, logits_out, hidden_out, sampled_out, uniforms, samp, st);
 
     for (int l = 0; l < c.n_layer; ++l) {
         const ftts_layer& L = w->layers[l];
@@ -624,10 +627,27 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
     g.ln_g = w->lnf_g;
     g.ln_b = w->lnf_b;
     g.eps = c.ln_eps;
+    g.hidden = hidden_out;
     if ((e = launch_gemv(c.wdtype, EPI_STORE, true, g, st)) != hipSuccess) return hip_fail(e, "lm head");
     if ((e = launch_sample(logits_out, B, V, *samp, uniforms, W.active, sampled_out, st)) != hipSuccess)
         return hip_fail(e, "sampler");
     return FTTS_OK;
+}
+
+int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
+                     const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out, int32_t* sampled_out,
+                     const float* uniforms, const ftts_sampling* samp, int32_t B, void* ws, size_t ws_bytes,
+                     void* stream) {
+    return decode_step(w, tokens, positions, pt, kv, logits_out, nullptr, sampled_out, uniforms, samp, B, ws,
+                       ws_bytes, stream);
+}
+
+int ftts_decode_step_hidden(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
+                            const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out, float* hidden_out,
+                            int32_t* sampled_out, const float* uniforms, const ftts_sampling* samp, int32_t B,
+                            void* ws, size_t ws_bytes, void* stream) {
+    return decode_step(w, tokens, positions, pt, kv, logits_out, hidden_out, sampled_out, uniforms, samp, B, ws,
+                       ws_bytes, stream);
 }
 
 int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* lens, int32_t B,

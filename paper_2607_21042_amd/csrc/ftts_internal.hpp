@@ -171,6 +171,7 @@ struct GemvArgs {
     float* out;              // [B][out_stride] fp32
     int out_stride;
     KvAppend kv;
+    float* hidden;           // LayerNorm rows: [B][K] copy of the normalised input (LM head), or null
 };
 
 struct AttnDecodeArgs {
@@ -211,6 +212,7 @@ struct BgemmArgs {
     // EPI_RESID: tile statistics of the updated rows go to stats_out [N/32][stats_ld].
     float2* stats_out;
     int stats_ld;
+    float* hidden;           // with ln_x: [B][K] copy of the normalised rows (LM head), or null
 };
 constexpr int kBatchedMin = 8;  // decode batches of at least this many use the MFMA linears
 
@@ -293,6 +295,7 @@ struct Args {
     const int32_t *tokens, *positions, *seq_lens, *block_table;
     void* kv;
     float* logits;
+    float* hidden;           // [B][d] LN_f output of the step (the LM head's input), or null
     int32_t* sampled;
     int32_t* active_out;
     uint64_t *ex_x, *ex_qkv, *ex_o, *ex_h, *ex_arg;

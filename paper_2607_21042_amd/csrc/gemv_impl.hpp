@@ -223,7 +223,11 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvArgs a) {
                 if (k < PK) {
 #pragma unroll
                     for (int b = 0; b < BMAX; ++b)
-                        if (b < B) s_act[b * PK + k] = (s_act[b * PK + k] - s_mean[b]) * s_rstd[b] * lg[i] + lb[i];
+                        if (b < B) {
+                            const float y = (s_act[b * PK + k] - s_mean[b]) * s_rstd[b] * lg[i] + lb[i];
+                            s_act[b * PK + k] = y;
+                            if (a.hidden && blockIdx.x == 0) a.hidden[(size_t)b * PK + k] = y;
+                        }
                 }
             }
             lds_barrier();

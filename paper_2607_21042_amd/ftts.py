@@ -89,6 +89,9 @@ def lib():
         L.ftts_decode_step.restype = _c.c_int
         L.ftts_decode_step.argtypes = [P(Weights), vp, vp, P(PageTable), P(KvPool), vp, vp, vp, P(Sampling), i32,
                                        vp, _c.c_size_t, vp]
+        L.ftts_decode_step_hidden.restype = _c.c_int
+        L.ftts_decode_step_hidden.argtypes = [P(Weights), vp, vp, P(PageTable), P(KvPool), vp, vp, vp, vp,
+                                              P(Sampling), i32, vp, _c.c_size_t, vp]
         L.ftts_set_decode_path.restype = _c.c_int
         L.ftts_set_decode_path.argtypes = [i32]
         L.ftts_check_workspace.restype = _c.c_int
@@ -172,13 +175,21 @@ def prefill(model, prefix_emb, lens, page_table, kv, last_logits, ws, stream=Non
 
 
 def decode_step(model, tokens, positions, page_table, kv, logits_out, sampled_out, uniforms, sampling: Sampling,
-                ws, stream=None):
-    """ftts_decode_step for B = tokens.numel() sequences."""
+                ws, stream=None, hidden_out=None):
+    """ftts_decode_step for B = tokens.numel() sequences; with hidden_out ([B][d_model]
+    fp32) it is ftts_decode_step_hidden."""
     B = tokens.numel()
-    _check(lib().ftts_decode_step(_c.byref(model.c), _ptr(tokens), _ptr(positions), _c.byref(page_table.c),
-                                  _c.byref(kv.c), _ptr(logits_out), _ptr(sampled_out), _ptr(uniforms),
-                                  _c.byref(sampling), B, _ptr(ws), ws.numel() * ws.element_size(),
-                                  _stream(stream)))
+    if hidden_out is None:
+        _check(lib().ftts_decode_step(_c.byref(model.c), _ptr(tokens), _ptr(positions), _c.byref(page_table.c),
+                                      _c.byref(kv.c), _ptr(logits_out), _ptr(sampled_out), _ptr(uniforms),
+                                      _c.byref(sampling), B, _ptr(ws), ws.numel() * ws.element_size(),
+                                      _stream(stream)))
+    else:
+        _check(lib().ftts_decode_step_hidden(_c.byref(model.c), _ptr(tokens), _ptr(positions),
+                                             _c.byref(page_table.c), _c.byref(kv.c), _ptr(logits_out),
+                                             _ptr(hidden_out), _ptr(sampled_out), _ptr(uniforms),
+                                             _c.byref(sampling), B, _ptr(ws), ws.numel() * ws.element_size(),
+                                             _stream(stream)))
 
 
 PATH_AUTO, PATH_KERNELS, PATH_PERSISTENT = 0, 1, 2

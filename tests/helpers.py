@@ -27,10 +27,13 @@ def oracle_weights(inputs: dict, wdtype_name: str) -> dict:
     return oquant.dequantized_model(inputs, "w8" if wdtype_name == "w8a16" else "w4")
 
 
-def oracle_teacher_forced(model: ogpt.GPT, prefix: np.ndarray, fed: np.ndarray):
-    """Logits of the last prefix row and of every decoded row, by one full causal forward."""
-    logits, _ = model.full_forward(model.rows(prefix, fed))
+def oracle_teacher_forced(model: ogpt.GPT, prefix: np.ndarray, fed: np.ndarray, with_hidden=False):
+    """Logits of the last prefix row and of every decoded row, by one full causal
+    forward (and, with_hidden, the decoded rows' final hidden states LN_f(x))."""
+    logits, hid = model.full_forward(model.rows(prefix, fed))
     P = prefix.shape[0]
+    if with_hidden:
+        return logits[P - 1], logits[P:P + len(fed)], hid[P:P + len(fed)]
     return logits[P - 1], logits[P:P + len(fed)]
 
 
@@ -78,7 +81,7 @@ def make_block_table(lens_total, seed=None, spare=0):
 
 
 def run_gpu(dev_model, shape, prefixes, fed, sampling=None, uniforms=None, block_table=None, n_pages=None,
-            pool_fill=None, graph=False):
+            pool_fill=None, graph=False, hidden=False):
     """Prefill every prefix, then feed fed[t] (int32 [T][B]) at step t.
 
     Returns dict(prefill [B][V], logits [T][B][V], sampled [T][B], kv, page table).
@@ -108,6 +111,7 @@ def run_gpu(dev_model, shape, prefixes, fed, sampling=None, uniforms=None, block
     pos = torch.empty(B, dtype=torch.int32, device="cuda")
     u = torch.zeros(B, dtype=torch.float32, device="cuda")
     logits = torch.empty((T, B, V), dtype=torch.float32, device="cuda")
+    hid = torch.empty((T, B, shape.d_model), dtype=torch.float32, device="cuda") if hidden else None
     sampled = torch.empty((T, B), dtype=torch.int32, device="cuda")
     fed_d = torch.from_numpy(np.ascontiguousarray(fed, dtype=np.int32)).cuda()
     un_d = torch.from_numpy(np.ascontiguousarray(uniforms, dtype=np.float32)).cuda() if uniforms is not None else None
@@ -116,8 +120,9 @@ def run_gpu(dev_model, shape, prefixes, fed, sampling=None, uniforms=None, block
         pos.fill_(t)
         if un_d is not None:
             u.copy_(un_d[t])
-        ftts.decode_step(dev_model, tok, pos, pt, kv, logits[t], sampled[t], u, sampling, ws)
+        ftts.decode_step(dev_model, tok, pos, pt, kv, logits[t], sampled[t], u, sampling, ws,
+                         hidden_out=hid[t] if hidden else None)
         pt.seq_lens.add_((fed_d[t] >= 0).to(torch.int32))
     torch.cuda.synchronize()
     return {"prefill": last.cpu().numpy(), "logits": logits.cpu().numpy(), "sampled": sampled.cpu().numpy(),
-            "kv": kv, "pt": pt, "lens": lens, "ws": ws}
+            "hidden": hid.cpu().numpy() if hidden else None, "kv": kv, "pt": pt, "lens": lens, "ws": ws}

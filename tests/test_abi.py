@@ -89,6 +89,14 @@ def test_decode_argument_errors():
     w.head.w = FAKE + 8
     assert _decode(w) == -4
     w.head.w = FAKE
+    # the hidden-state variant takes the same checks, plus the alignment of hidden_out
+    pt, kv, samp = ftts.PageTable(FAKE, FAKE, 4), ftts.KvPool(FAKE, 16), ftts.Sampling(1.0, 1, 1.0)
+    hid = ftts.lib().ftts_decode_step_hidden
+    args = lambda h, B: (ctypes.byref(w), FAKE, FAKE, ctypes.byref(pt), ctypes.byref(kv), FAKE, h, FAKE,  # noqa: E731
+                         FAKE, ctypes.byref(samp), B, FAKE, 1 << 30, None)
+    assert hid(*args(FAKE + 8, 1)) == -4
+    assert "hidden_out" in ftts.lib().ftts_last_error().decode()
+    assert hid(*args(FAKE, 0)) == -2
     w.layers[1].fc2.bias = None
     assert _decode(w) == -1
 

@@ -482,6 +482,38 @@ def test_persistent_step_matches_oracle(torch_cuda, decode_path, mid_master, mod
         assert np.all(res["sampled"][7:, 0] == -1)
 
 
+@pytest.mark.parametrize("mode,path,B", [("bf16", "persistent", 1), ("w4a16", "persistent", 2),
+                                         ("bf16", "kernels", 3), ("w8a16", "kernels", 9), ("bf16", "kernels", 9)])
+def test_hidden_state_output(torch_cuda, decode_path, mid_master, mode, path, B):
+    """ftts_decode_step_hidden hands out LN_f of each new row (the LM head's
+    input) on every decode path: the persistent step (B <= 2), the per-phase
+    GEMVs (B < 8) and the batched matrix-core linears (B >= 8).  It matches the
+    oracle's final hidden state, and asking for it changes no logit bit."""
+    from paper_2607_21042_amd import ftts
+    decode_path(ftts.PATH_PERSISTENT if path == "persistent" else ftts.PATH_KERNELS)
+    inputs = model_inputs(MID, mode, mid_master)
+    lens = [70, 130, 33, 64, 65, 1, 100, 127, 20][:B]
+    flat = workload.prefix_embeddings(lens, MID.d_model, seed=1)
+    prefixes = np.split(flat, np.cumsum(lens)[:-1])
+    T = 6
+    fed = workload.random_tokens(T, B, MID.vocab, seed=4)
+    fed[0, :] = MID.start_token
+    say(f"hidden state {mode} {path} B={B}")
+    dm = ftts.DeviceModel(inputs, MID, wd(mode))
+    res = helpers.run_gpu(dm, MID, prefixes, fed, hidden=True)
+    plain = helpers.run_gpu(dm, MID, prefixes, fed)
+    np.testing.assert_array_equal(res["logits"], plain["logits"])
+    om = ogpt.GPT(helpers.oracle_weights(inputs, mode), MID.n_head, MID.d_head, dtype=np.float32)
+    worst = 0.0
+    for b in range(B):
+        _, ref_logits, ref_hid = helpers.oracle_teacher_forced(om, prefixes[b], fed[:, b], with_hidden=True)
+        for t in range(T):
+            ok, err = helpers.tolerance_ok(res["hidden"][t, b], ref_hid[t], mode)
+            worst = max(worst, err)
+            assert ok, ("hidden", t, b, err)
+    say(f"  worst hidden err {worst:.3g}")
+
+
 @pytest.mark.parametrize("mode,lens", [("bf16", [900]), ("bf16", [600, 900]), ("w4a16", [600, 900])])
 def test_persistent_step_split_attention(torch_cuda, decode_path, mid_master, mode, lens):
     """Contexts long enough that each (sequence, head) is attended by two
