@@ -226,6 +226,34 @@ int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* l
                  float* last_logits, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * ftts_prefill that assembles the model's own input from ids (the serving
+ * adaptations of Sec. II-C): sequence b's prefix is its cond_lens[b]
+ * conditioning rows (speaker latents, emotion and speed embeddings -- 34 rows
+ * in IndexTTS-2 -- used as given, with no position embedding), followed by its
+ * text_lens[b] text tokens, text row i being
+ *     tok_emb[vocab + text_ids[i]] + pos_emb[text_pos0 + i]:
+ * text and semantic codes share one token table, the text block after the
+ * vocab semantic rows (text ids shifted by the semantic vocabulary size), and
+ * the text tokens take their own range of the position table starting at
+ * text_pos0 (the semantic tokens' range is the caller's choice of `positions`
+ * in ftts_decode_step).
+ *   cond_emb   [sum cond_lens][d_model] activation dtype (NULL if all are 0).
+ *   cond_lens, text_lens  [host][B] int32 >= 0, cond_lens[b] + text_lens[b] >= 1.
+ *   text_ids   [sum text_lens] device int32, packed in sequence order; ids
+ *              outside [0, text_vocab) read as a zero token row.
+ *   text_vocab rows of the text block: tok_emb holds vocab + text_vocab rows.
+ *   text_pos0  first position row of the text range; text_pos0 + text_lens[b]
+ *              <= n_pos (FTTS_E_RANGE otherwise).
+ * Writes KV slots 0 .. cond_lens[b] + text_lens[b] - 1 and, if last_logits is
+ * not NULL, the logits of each sequence's last prefix row; every other rule is
+ * that of ftts_prefill.
+ */
+int ftts_prefill_ids(const ftts_weights* w, const void* cond_emb, const int32_t* cond_lens,
+                     const int32_t* text_ids, const int32_t* text_lens, int32_t text_vocab,
+                     int32_t text_pos0, int32_t B, const ftts_page_table* pt, const ftts_kv_pool* kv,
+                     float* last_logits, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * One decode step for B sequences (the per-token generation step of the
  * autoregressive GPT, Sec. II-A / II-C).
  *   tokens      [B] int32 token ids; a negative id marks an inactive slot.

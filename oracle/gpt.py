@@ -112,6 +112,19 @@ class GPT:
         positions = np.asarray(positions)
         return self.tok_emb[tokens] + self.pos_emb[positions]
 
+    def assemble_prefix(self, cond, text_ids, text_pos0):
+        """The model's own prefix from ids (Sec. II-C, the first three serving
+        adaptations): the conditioning rows as given, with no position
+        embedding, then one row per text token.  Text and semantic codes share
+        one token table with the text block after the semantic vocabulary (its
+        size: the LM head's rows), so text id t is row vocab + t; text token i
+        takes position row text_pos0 + i, the text range of the position table."""
+        cond = np.asarray(cond, dtype=self.dtype).reshape(-1, self.d_model)
+        text_ids = np.asarray(text_ids, dtype=np.int64)
+        vocab = self.w_head.shape[0]
+        text = self.tok_emb[vocab + text_ids] + self.pos_emb[text_pos0 + np.arange(len(text_ids))]
+        return np.concatenate([cond, text.reshape(-1, self.d_model)], axis=0)
+
     def rows(self, prefix, tokens=(), positions=None):
         """Prefix rows (as given, no positions) followed by decoded-token rows."""
         prefix = np.asarray(prefix, dtype=self.dtype)

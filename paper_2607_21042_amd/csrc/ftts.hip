@@ -650,14 +650,20 @@ int ftts_decode_step_hidden(const ftts_weights* w, const int32_t* tokens, const 
                        ws_bytes, stream);
 }
 
-int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* lens, int32_t B,
-                 const ftts_page_table* pt, const ftts_kv_pool* kv, float* last_logits, void* ws, size_t ws_bytes,
-                 void* stream) {
-    TRY(check_weights(w));
+// Where the prefill's input rows come from: ready embeddings, or the model's
+// own input assembly (conditioning rows, then text ids through the merged table).
+struct PrefixSource {
+    const void* emb;             // [sum lens][d] activation dtype, or null
+    const void* cond;            // [sum cond_lens][d] activation dtype
+    const int32_t* cond_lens;    // [host][B]
+    const int32_t* text_ids;     // [sum text_lens] device
+    int text_vocab, text_pos0;
+};
+
+static int prefill(const ftts_weights* w, const PrefixSource& src, const int32_t* lens, int32_t B,
+                   const ftts_page_table* pt, const ftts_kv_pool* kv, float* last_logits, void* ws, size_t ws_bytes,
+                   void* stream) {
     const ftts_config& c = w->cfg;
-    if (B < 1 || B > FTTS_MAX_BATCH) return fail(FTTS_E_SHAPE, "B must be in [1, %d]", FTTS_MAX_BATCH);
-    TRY(check_ptr(prefix_emb, "prefix_emb"));
-    if (!lens) return fail(FTTS_E_INVALID_ARG, "lens is NULL");
     TRY(check_kv(pt, kv, false));
     TRY(check_ptr(ws, "workspace"));
     SeqTable seqs{};
@@ -684,8 +690,25 @@ int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* l
     const int d = c.d_model, F = c.d_ff, V = c.vocab, Mi = (int)M;
 
     (void)hipGetLastError();
-    hipError_t e = launch_act_to_f32(c.wdtype, prefix_emb, Mi, d, P.x, st);
-    if (e != hipSuccess) return hip_fail(e, "prefix copy");
+    hipError_t e;
+    if (src.emb) {
+        if ((e = launch_act_to_f32(c.wdtype, src.emb, Mi, d, P.x, st)) != hipSuccess) return hip_fail(e, "prefix copy");
+    } else {
+        AssembleArgs as{};
+        as.seqs = seqs;
+        as.cond_cu[0] = 0;
+        for (int b = 0; b < B; ++b) as.cond_cu[b + 1] = as.cond_cu[b] + src.cond_lens[b];
+        as.cond = src.cond;
+        as.text_ids = src.text_ids;
+        as.tok_emb = w->tok_emb;
+        as.pos_emb = w->pos_emb;
+        as.d = d;
+        as.vocab = V;
+        as.text_vocab = src.text_vocab;
+        as.text_pos0 = src.text_pos0;
+        as.x = P.x;
+        if ((e = launch_assemble_prefix(c.wdtype, as, Mi, st)) != hipSuccess) return hip_fail(e, "input assembly");
+    }
     if (P.count) {
         size_t pf, cn;
         gemm_scratch(c, Mi, &pf, &cn);
@@ -770,6 +793,53 @@ int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* l
         if ((e = launch_gemv(c.wdtype, EPI_STORE, true, g, st)) != hipSuccess) return hip_fail(e, "lm head");
     }
     return FTTS_OK;
+}
+
+int ftts_prefill(const ftts_weights* w, const void* prefix_emb, const int32_t* lens, int32_t B,
+                 const ftts_page_table* pt, const ftts_kv_pool* kv, float* last_logits, void* ws, size_t ws_bytes,
+                 void* stream) {
+    TRY(check_weights(w));
+    if (B < 1 || B > FTTS_MAX_BATCH) return fail(FTTS_E_SHAPE, "B must be in [1, %d]", FTTS_MAX_BATCH);
+    TRY(check_ptr(prefix_emb, "prefix_emb"));
+    if (!lens) return fail(FTTS_E_INVALID_ARG, "lens is NULL");
+    PrefixSource src{};
+    src.emb = prefix_emb;
+    return prefill(w, src, lens, B, pt, kv, last_logits, ws, ws_bytes, stream);
+}
+
+int ftts_prefill_ids(const ftts_weights* w, const void* cond_emb, const int32_t* cond_lens, const int32_t* text_ids,
+                     const int32_t* text_lens, int32_t text_vocab, int32_t text_pos0, int32_t B,
+                     const ftts_page_table* pt, const ftts_kv_pool* kv, float* last_logits, void* ws,
+                     size_t ws_bytes, void* stream) {
+    TRY(check_weights(w));
+    const ftts_config& c = w->cfg;
+    if (B < 1 || B > FTTS_MAX_BATCH) return fail(FTTS_E_SHAPE, "B must be in [1, %d]", FTTS_MAX_BATCH);
+    if (!cond_lens || !text_lens) return fail(FTTS_E_INVALID_ARG, "cond_lens/text_lens is NULL");
+    if (text_pos0 < 0) return fail(FTTS_E_RANGE, "text_pos0 must be >= 0");
+    int32_t lens[FTTS_MAX_BATCH];
+    int64_t n_cond = 0, n_text = 0;
+    for (int b = 0; b < B; ++b) {
+        if (cond_lens[b] < 0 || text_lens[b] < 0)
+            return fail(FTTS_E_RANGE, "cond_lens[%d] / text_lens[%d] must be >= 0", b, b);
+        if ((int64_t)text_pos0 + text_lens[b] > c.n_pos)
+            return fail(FTTS_E_RANGE, "text positions of sequence %d run past n_pos", b);
+        if ((int64_t)cond_lens[b] + text_lens[b] > (1 << 24)) return fail(FTTS_E_RANGE, "prefix too long");
+        lens[b] = cond_lens[b] + text_lens[b];
+        n_cond += cond_lens[b];
+        n_text += text_lens[b];
+    }
+    if (n_cond > 0) TRY(check_ptr(cond_emb, "cond_emb"));
+    if (n_text > 0) {
+        if (!text_ids) return fail(FTTS_E_INVALID_ARG, "text_ids is NULL");
+        if (text_vocab < 1) return fail(FTTS_E_RANGE, "text_vocab must be >= 1");
+    }
+    PrefixSource src{};
+    src.cond = cond_emb;
+    src.cond_lens = cond_lens;
+    src.text_ids = text_ids;
+    src.text_vocab = text_vocab;
+    src.text_pos0 = text_pos0;
+    return prefill(w, src, lens, B, pt, kv, last_logits, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -249,6 +249,21 @@ struct AttnPrefillArgs {
     int tiles_cu[kMaxPrefillSeqs + 1];  // prefix sums of query tiles (prefill_tile_rows) per sequence
 };
 
+// Prefill input assembly: sequence b's rows are its cond_lens[b] conditioning
+// rows as given (no position embedding), then its text rows
+// tok_emb[vocab + id] + pos_emb[text_pos0 + i] (merged token table, text range
+// of the position table).
+struct AssembleArgs {
+    SeqTable seqs;                        // row offsets of the assembled prefixes
+    int cond_cu[kMaxPrefillSeqs + 1];     // prefix sums of the conditioning rows
+    const void* cond;                     // [sum cond][d] activation dtype
+    const int32_t* text_ids;              // [sum text] (text row i of b at seqs.cu[b] - cond_cu[b] + i)
+    const void* tok_emb;
+    const void* pos_emb;
+    int d, vocab, text_vocab, text_pos0;
+    float* x;                             // [sum lens][d] fp32 out
+};
+
 // ---- launchers (each returns a hipError_t from the launch) --------------------------
 hipError_t launch_embed(int wdtype, const void* tok_emb, const void* pos_emb, int vocab, int n_pos, int d,
                         const int32_t* tokens, const int32_t* positions, const int32_t* seq_lens,
@@ -275,6 +290,7 @@ hipError_t launch_bgemm(int wdtype, int epi, const BgemmArgs& a, hipStream_t st)
 int bgemm_splits(int wdtype, int N, int K, bool ln);
 bool bgemm_supported(int wdtype, int K, bool ln);
 hipError_t launch_act_to_f32(int wdtype, const void* src, int rows, int d, float* dst, hipStream_t st);
+hipError_t launch_assemble_prefix(int wdtype, const AssembleArgs& a, int rows, hipStream_t st);
 
 namespace mega {
 constexpr int D = 1280, FF = 5120, NH = 20;

@@ -176,6 +176,39 @@ hipError_t launch_act_to_f32(int wdtype, const void* src, int rows, int d, float
     return hipGetLastError();
 }
 
+// ---- prefill input assembly -----------------------------------------------------------------
+// One workgroup per assembled row.  Text ids outside [0, text_vocab) read as a
+// zero token row (only the position embedding remains); no access leaves the tables.
+template <bool F32>
+__global__ __launch_bounds__(256) void assemble_prefix_kernel(const AssembleArgs a) {
+    const int r = blockIdx.x;
+    int lo = 0, hi = a.seqs.n - 1;  // the sequence holding row r
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (a.seqs.cu[mid] <= r) lo = mid;
+        else hi = mid - 1;
+    }
+    const int j = r - a.seqs.cu[lo], nc = a.cond_cu[lo + 1] - a.cond_cu[lo];
+    float* xr = a.x + (size_t)r * a.d;
+    if (j < nc) {
+        const size_t src = (size_t)(a.cond_cu[lo] + j) * a.d;
+        for (int k = threadIdx.x; k < a.d; k += blockDim.x) xr[k] = ld_act<F32>(a.cond, src + k);
+        return;
+    }
+    const int i = j - nc;                                 // text position within the sequence
+    const int id = a.text_ids[a.seqs.cu[lo] - a.cond_cu[lo] + i];
+    const bool ok = id >= 0 && id < a.text_vocab;
+    const size_t tr = (size_t)(a.vocab + (ok ? id : 0)) * a.d, pr = (size_t)(a.text_pos0 + i) * a.d;
+    for (int k = threadIdx.x; k < a.d; k += blockDim.x)
+        xr[k] = (ok ? ld_act<F32>(a.tok_emb, tr + k) : 0.f) + ld_act<F32>(a.pos_emb, pr + k);
+}
+
+hipError_t launch_assemble_prefix(int wdtype, const AssembleArgs& a, int rows, hipStream_t st) {
+    if (wdtype == FTTS_F32) hipLaunchKernelGGL(assemble_prefix_kernel<true>, dim3(rows), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL(assemble_prefix_kernel<false>, dim3(rows), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
 // ---- sampler ------------------------------------------------------------------------------
 // One 256-thread workgroup per sequence; thread t holds the tempered logits of
 // indices t, t + 256, ... in registers.  Order is by (value, index): the larger

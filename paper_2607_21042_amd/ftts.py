@@ -89,6 +89,9 @@ def lib():
         L.ftts_decode_step.restype = _c.c_int
         L.ftts_decode_step.argtypes = [P(Weights), vp, vp, P(PageTable), P(KvPool), vp, vp, vp, P(Sampling), i32,
                                        vp, _c.c_size_t, vp]
+        L.ftts_prefill_ids.restype = _c.c_int
+        L.ftts_prefill_ids.argtypes = [P(Weights), vp, P(i32), vp, P(i32), i32, i32, i32, P(PageTable), P(KvPool),
+                                       vp, vp, _c.c_size_t, vp]
         L.ftts_decode_step_hidden.restype = _c.c_int
         L.ftts_decode_step_hidden.argtypes = [P(Weights), vp, vp, P(PageTable), P(KvPool), vp, vp, vp, vp,
                                               P(Sampling), i32, vp, _c.c_size_t, vp]
@@ -172,6 +175,17 @@ def prefill(model, prefix_emb, lens, page_table, kv, last_logits, ws, stream=Non
     _check(lib().ftts_prefill(_c.byref(model.c), _ptr(prefix_emb), lens_arr, B, _c.byref(page_table.c),
                               _c.byref(kv.c), _ptr(last_logits), _ptr(ws), ws.numel() * ws.element_size(),
                               _stream(stream)))
+
+
+def prefill_ids(model, cond_emb, cond_lens, text_ids, text_lens, text_vocab, text_pos0, page_table, kv, last_logits,
+                ws, stream=None):
+    """ftts_prefill_ids; `cond_lens` and `text_lens` are host sequences."""
+    B = len(cond_lens)
+    cl = (i32 * B)(*[int(x) for x in cond_lens])
+    tl = (i32 * B)(*[int(x) for x in text_lens])
+    _check(lib().ftts_prefill_ids(_c.byref(model.c), _ptr(cond_emb), cl, _ptr(text_ids), tl, int(text_vocab),
+                                  int(text_pos0), B, _c.byref(page_table.c), _c.byref(kv.c), _ptr(last_logits),
+                                  _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def decode_step(model, tokens, positions, page_table, kv, logits_out, sampled_out, uniforms, sampling: Sampling,

@@ -185,6 +185,18 @@ def batch_lengths(batch: int, seed: int = 3, prefix=(128, 512), target=(256, 768
     return p, t
 
 
+def text_table(shape: ModelShape, n_text: int, seed: int = 9) -> np.ndarray:
+    """Rows of a text-token embedding block [n_text, d_model] ~N(0, 0.02), bf16-representable.
+    Appended after the semantic rows of tok_emb it forms the merged token table."""
+    rng = np.random.default_rng(seed)
+    return bf16_round(rng.standard_normal((n_text, shape.d_model), dtype=np.float32) * np.float32(INIT_STD))
+
+
+def text_ids(lens, n_text: int, seed: int = 10) -> np.ndarray:
+    """Packed text-token ids in [0, n_text) for sequences of the given lengths."""
+    return np.random.default_rng(seed).integers(0, n_text, size=int(np.sum(lens))).astype(np.int32)
+
+
 def random_tokens(n_steps: int, batch: int, vocab: int, seed: int = 4) -> np.ndarray:
     """Teacher-forcing token ids in [0, vocab - 2) (no special codes), shape [n_steps, batch]."""
     return np.random.default_rng(seed).integers(0, vocab - 2, size=(n_steps, batch)).astype(np.int32)

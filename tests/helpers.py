@@ -27,10 +27,10 @@ def oracle_weights(inputs: dict, wdtype_name: str) -> dict:
     return oquant.dequantized_model(inputs, "w8" if wdtype_name == "w8a16" else "w4")
 
 
-def oracle_teacher_forced(model: ogpt.GPT, prefix: np.ndarray, fed: np.ndarray, with_hidden=False):
+def oracle_teacher_forced(model: ogpt.GPT, prefix: np.ndarray, fed: np.ndarray, with_hidden=False, pos0=0):
     """Logits of the last prefix row and of every decoded row, by one full causal
     forward (and, with_hidden, the decoded rows' final hidden states LN_f(x))."""
-    logits, hid = model.full_forward(model.rows(prefix, fed))
+    logits, hid = model.full_forward(model.rows(prefix, fed, pos0 + np.arange(len(fed))))
     P = prefix.shape[0]
     if with_hidden:
         return logits[P - 1], logits[P:P + len(fed)], hid[P:P + len(fed)]
@@ -81,9 +81,11 @@ def make_block_table(lens_total, seed=None, spare=0):
 
 
 def run_gpu(dev_model, shape, prefixes, fed, sampling=None, uniforms=None, block_table=None, n_pages=None,
-            pool_fill=None, graph=False, hidden=False):
-    """Prefill every prefix, then feed fed[t] (int32 [T][B]) at step t.
+            pool_fill=None, graph=False, hidden=False, from_ids=None, pos0=0):
+    """Prefill every prefix, then feed fed[t] (int32 [T][B]) at step t (position pos0 + t).
 
+    With from_ids = dict(cond, cond_lens, text_ids, text_lens, n_text, text_pos0)
+    the prefill is ftts_prefill_ids and `prefixes` only gives the prefix lengths.
     Returns dict(prefill [B][V], logits [T][B][V], sampled [T][B], kv, page table).
     """
     import torch
@@ -103,7 +105,14 @@ def run_gpu(dev_model, shape, prefixes, fed, sampling=None, uniforms=None, block
     ws = torch.empty(ftts.workspace_bytes(dev_model.cfg, B, sum(lens)), dtype=torch.uint8, device="cuda")
     V = shape.vocab
     last = torch.empty((B, V), dtype=torch.float32, device="cuda")
-    ftts.prefill(dev_model, prefix, lens, pt, kv, last, ws)
+    if from_ids is None:
+        ftts.prefill(dev_model, prefix, lens, pt, kv, last, ws)
+    else:
+        f = from_ids
+        cond = torch.from_numpy(np.ascontiguousarray(f["cond"], np.float32)).cuda().to(adt)
+        ids = torch.from_numpy(np.ascontiguousarray(f["text_ids"], np.int32)).cuda()
+        ftts.prefill_ids(dev_model, cond, f["cond_lens"], ids, f["text_lens"], f["n_text"], f["text_pos0"], pt, kv,
+                         last, ws)
     pt.seq_lens.copy_(torch.tensor(lens, dtype=torch.int32))
     if sampling is None:
         sampling = ftts.Sampling(1.0, 1, 1.0)
@@ -117,7 +126,7 @@ def run_gpu(dev_model, shape, prefixes, fed, sampling=None, uniforms=None, block
     un_d = torch.from_numpy(np.ascontiguousarray(uniforms, dtype=np.float32)).cuda() if uniforms is not None else None
     for t in range(T):
         tok.copy_(fed_d[t])
-        pos.fill_(t)
+        pos.fill_(pos0 + t)
         if un_d is not None:
             u.copy_(un_d[t])
         ftts.decode_step(dev_model, tok, pos, pt, kv, logits[t], sampled[t], u, sampling, ws,

@@ -129,6 +129,21 @@ def test_prefill_argument_errors():
     assert L.ftts_prefill(ctypes.byref(w), FAKE, None, 1, ctypes.byref(pt), ctypes.byref(kv), FAKE, FAKE,
                           1 << 30, None) == -1
 
+    def ids(cond_lens, text_lens, text_vocab=50, text_pos0=0, text_ids=FAKE, cond=FAKE):
+        cl = (ctypes.c_int32 * len(cond_lens))(*cond_lens)
+        tl = (ctypes.c_int32 * len(text_lens))(*text_lens)
+        return L.ftts_prefill_ids(ctypes.byref(w), cond, cl, text_ids, tl, text_vocab, text_pos0, len(cond_lens),
+                                  ctypes.byref(pt), ctypes.byref(kv), FAKE, FAKE, 1 << 30, None)
+
+    assert ids([0], [0]) == -5                          # an empty prefix
+    assert ids([-1], [3]) == -5
+    assert ids([2], [3], text_pos0=-1) == -5
+    assert ids([2], [3], text_pos0=workload.TINY.n_pos - 2) == -5   # text positions past n_pos
+    assert ids([2], [3], text_ids=None) == -1
+    assert ids([2], [3], text_vocab=0) == -5
+    assert ids([2], [0], cond=None) == -1
+    assert ids([40], [30]) == -5                        # 70 rows > max_pages * 64
+
 
 def test_quantize_and_sample_argument_errors():
     L = ftts.lib()

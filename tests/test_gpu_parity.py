@@ -267,6 +267,49 @@ def test_prefill_lengths_across_attention_tiles(torch_cuda, mode):
     say(f"  worst err {worst:.3g}")
 
 
+@pytest.mark.parametrize("mode", ["f32", "bf16", "w4a16"])
+def test_prefill_from_ids(torch_cuda, mode):
+    """ftts_prefill_ids assembles the prefix itself: conditioning rows, then text
+    ids through the merged token table with their own position range (Sec. II-C).
+    Prefill logits and decode steps whose semantic positions use another range
+    match the oracle; in fp32 the logits equal those of ftts_prefill on the same
+    rows assembled on the host, bit for bit."""
+    from paper_2607_21042_amd import ftts
+    shape = workload.TINY
+    n_text, text_pos0, sem_pos0 = 50, 0, 400
+    inputs = dict(model_inputs(shape, mode, workload.master_weights(shape, seed=0)))
+    inputs["tok_emb"] = np.concatenate([inputs["tok_emb"], workload.text_table(shape, n_text)])
+    cond_lens, text_lens = [34, 0, 34, 5], [20, 70, 0, 129]
+    cond = workload.prefix_embeddings(cond_lens, shape.d_model, seed=1, bf16=(mode != "f32"))
+    ids = workload.text_ids(text_lens, n_text)
+    om = ogpt.GPT(helpers.oracle_weights(inputs, mode), shape.n_head, shape.d_head, dtype=np.float32)
+    cc, tc = np.cumsum([0] + cond_lens), np.cumsum([0] + text_lens)
+    prefixes = [om.assemble_prefix(cond[cc[b]:cc[b + 1]], ids[tc[b]:tc[b + 1]], text_pos0)
+                for b in range(len(cond_lens))]
+    T = 3
+    fed = workload.random_tokens(T, len(cond_lens), shape.vocab, seed=4)
+    fed[0, :] = shape.start_token
+    say(f"prefill from ids {mode}")
+    dm = ftts.DeviceModel(inputs, shape, wd(mode))
+    src = dict(cond=cond, cond_lens=cond_lens, text_ids=ids, text_lens=text_lens, n_text=n_text,
+               text_pos0=text_pos0)
+    res = helpers.run_gpu(dm, shape, prefixes, fed, from_ids=src, pos0=sem_pos0)
+    worst = 0.0
+    for b, pre in enumerate(prefixes):
+        ref_pre, ref = helpers.oracle_teacher_forced(om, pre, fed[:, b], pos0=sem_pos0)
+        ok, err = helpers.tolerance_ok(res["prefill"][b], ref_pre, mode)
+        assert ok, ("prefill", b, err)
+        for t in range(T):
+            ok, err = helpers.tolerance_ok(res["logits"][t, b], ref[t], mode)
+            worst = max(worst, err)
+            assert ok, ("step", t, b, err)
+    say(f"  worst err {worst:.3g}")
+    if mode == "f32":
+        ref_run = helpers.run_gpu(dm, shape, prefixes, fed, pos0=sem_pos0)
+        np.testing.assert_array_equal(res["prefill"], ref_run["prefill"])
+        np.testing.assert_array_equal(res["logits"], ref_run["logits"])
+
+
 @pytest.mark.parametrize("mode,B", [("bf16", 33), ("w8a16", 8), ("w4a16", 33)])
 def test_batched_decode_matrix_core_linears(torch_cuda, mode, B):
     """Batches of 8 or more take the MFMA linears (33 = a full group of 32 plus a

@@ -170,6 +170,32 @@ def test_full_forward_matches_hf_gpt2():
     np.testing.assert_array_equal(rows[:10], prefix)
 
 
+def test_input_assembly_merged_table_and_position_ranges():
+    """Sec. II-C adaptations 1-3: conditioning rows pass through with no position
+    embedding; a text id shifted past the semantic vocabulary into the merged
+    table reads the separate text table's row; text positions start at text_pos0;
+    semantic ids still read the semantic block."""
+    w, _ = small_model()
+    d, V = SMALL.d_model, SMALL.vocab
+    rng = np.random.default_rng(3)
+    text = rng.standard_normal((7, d))
+    merged = dict(w)
+    merged["tok_emb"] = np.concatenate([w["tok_emb"], text])
+    m = gpt.GPT(merged, SMALL.n_head, SMALL.d_head, dtype=np.float64)
+    cond = rng.standard_normal((3, d))
+    ids = np.array([4, 0, 6, 4])
+    rows = m.assemble_prefix(cond, ids, text_pos0=5)
+    assert rows.shape == (3 + len(ids), d)
+    np.testing.assert_array_equal(rows[:3], cond)
+    for i, t in enumerate(ids):
+        np.testing.assert_array_equal(rows[3 + i], text[t] + w["pos_emb"][5 + i])
+    np.testing.assert_array_equal(m.embed([V - 1], [2])[0],
+                                  w["tok_emb"][V - 1].astype(np.float64) + w["pos_emb"][2].astype(np.float64))
+    # no text: the prefix is the conditioning alone; no conditioning: text rows alone
+    np.testing.assert_array_equal(m.assemble_prefix(cond, [], 0), cond)
+    np.testing.assert_array_equal(m.assemble_prefix(np.zeros((0, d)), [6], 0)[0], text[6] + w["pos_emb"][0])
+
+
 @pytest.mark.parametrize("dtype,tol", [(np.float64, 1e-12), (np.float32, 1e-5)])
 def test_prefill_then_decode_equals_full_forward(dtype, tol):
     w, model = small_model(dtype)
