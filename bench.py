@@ -53,6 +53,10 @@ def parse():
     p.add_argument("--paged", action="store_true",
                    help="the batched paged workload instead: --batch sequences (default 32) with prefix lengths "
                         "~U[128,512], targets ~U[256,768] then STOP, top-k 30 / top-p 0.8 / T 0.8 sampling")
+    p.add_argument("--serve", action="store_true",
+                   help="continuous batching instead: --requests utterances (default 64) with the --paged length "
+                        "mix through --batch decode slots (default 32), chunks of 16 steps, top-k 30 sampling")
+    p.add_argument("--requests", type=int, default=64)
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain device copy of known size (scales the rocprofv3 byte counters)")
     return p.parse_args()
@@ -279,6 +283,52 @@ def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
     }
 
 
+def serve_run(args, torch, ftts, workload, shape, dm, mode):
+    """Continuous batching: more utterances than decode slots, admitted as slots
+    and pages free up; ids streamed in chunks.  Times whole runs (prefills,
+    decode chunks and the host's bookkeeping between them)."""
+    from paper_2607_21042_amd import serve
+    R, S = args.requests, args.batch
+    P, Tt = workload.batch_lengths(R, seed=3)
+    flat = workload.prefix_embeddings(P.tolist(), shape.d_model, seed=1, bf16=(mode != "f32"))
+    prefixes = np.split(flat, np.cumsum(P)[:-1])
+    uni = workload.uniforms(int(Tt.max()), R, seed=2)
+    max_ctx = int((P + Tt).max())
+    n_pages = S * ((max_ctx + 63) // 64) + 8
+    samp = ftts.Sampling(0.8, 30, 0.8)
+
+    def one_run():
+        sch = serve.Scheduler(dm, shape, max_slots=S, n_pages=n_pages, max_ctx=max_ctx, sampling=samp, chunk=16,
+                              overlap=4, max_prefill_rows=S * 512)
+        reqs = [sch.submit(serve.Request(prefix=p, max_new=int(t), uniforms=uni[:, i]))
+                for i, (p, t) in enumerate(zip(prefixes, Tt))]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        sch.run()
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        assert all(r.done and len(r.tokens) == r.max_new and r.tokens[-1] == shape.stop_token for r in reqs)
+        return dt, sch.n_chunks
+
+    for _ in range(args.warmup):
+        one_run()
+    runs = [one_run() for _ in range(args.steps)]
+    dt = float(np.mean([r[0] for r in runs]))
+    n_tok = int(Tt.sum())
+    return {
+        "metric": METRIC, "value": round(n_tok / dt, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(dt * 1e3, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": {"f32": "f32", "bf16": "bf16", "w8a16": "int8-w/bf16",
+                                       "w4a16": "int4-w/bf16"}[mode],
+        "data": "synthetic: seeded random-init IndexTTS-2-shaped GPT; continuous batching over a shared page pool",
+        "config": {"workload": f"indextts2-gpt {mode} continuous batching: {R} utterances, {S} slots, "
+                               f"prefix~U[128,512] target~U[256,768]+STOP, chunks of 16 (overlap 4), "
+                               f"top-k 30 top-p 0.8 T 0.8", "requests": R, "slots": S, "tokens": n_tok,
+                   "chunks": runs[-1][1]},
+        "wall_s": round(dt, 3),
+    }
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -310,6 +360,11 @@ def main():
         if args.batch == 1:
             args.batch = 32
         print(json.dumps(paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs)), flush=True)
+        return
+    if args.serve:
+        if args.batch == 1:
+            args.batch = 32
+        print(json.dumps(serve_run(args, torch, ftts, workload, shape, dm, mode)), flush=True)
         return
     adt = ftts.act_dtype(wdtype)
     prefix_np = workload.prefix_embeddings([P] * B, shape.d_model, seed=1, bf16=(mode != "f32"))
