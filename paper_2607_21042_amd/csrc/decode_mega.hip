@@ -59,8 +59,8 @@ template <> struct Tiles<FTTS_BF16> {
 template <> struct Tiles<FTTS_W8A16> {
     static constexpr int QL = 16, QC = 5, OL = 16, OC = 5, AL = 16, AC = 5, BL = 64, BC = 5;
 };
-template <> struct Tiles<FTTS_W4A16> {
-    static constexpr int QL = 8, QC = 5, OL = 8, OC = 5, AL = 8, AC = 5, BL = 32, BC = 5;
+template <> struct Tiles<FTTS_W4A16> {  // 4-byte chunks (8 codes): many more lanes per row than 16-byte ones
+    static constexpr int QL = 16, QC = 10, OL = 32, OC = 5, AL = 16, AC = 10, BL = 64, BC = 10;
 };
 constexpr int HL = 8, HC = 20;  // LM head (bf16)
 
@@ -261,11 +261,43 @@ __device__ __forceinline__ bool follow(Sync& sy) {
 // One phase's share of a weight matrix: rows [r0, r0 + R) in an LDS buffer
 // (copied there by the copy wave); per-row bias and quantisation parameters of
 // this thread's row in registers.
+// W4A16 dot of one 4-byte chunk (8 codes, columns 8c .. 8c+7, one quantisation
+// group): the zero-point enters through the chunk's own activation sum.
+template <int B_>
+__device__ __forceinline__ void dot_w4_word(uint32_t word, const float* xs, int stride, int B, float (&acc)[B_],
+                                            float s4, float z4) {
+    float wf[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) wf[i] = (float)((word >> (4 * i)) & 0xFu);
+#pragma unroll
+    for (int b = 0; b < B_; ++b) {
+        if (b < B) {
+            const float4 x0 = *reinterpret_cast<const float4*>(xs + b * stride);
+            const float4 x1 = *reinterpret_cast<const float4*>(xs + b * stride + 4);
+            float t = 0.f;
+            t = fmaf(wf[0], x0.x, t);
+            t = fmaf(wf[1], x0.y, t);
+            t = fmaf(wf[2], x0.z, t);
+            t = fmaf(wf[3], x0.w, t);
+            t = fmaf(wf[4], x1.x, t);
+            t = fmaf(wf[5], x1.y, t);
+            t = fmaf(wf[6], x1.z, t);
+            t = fmaf(wf[7], x1.w, t);
+            const float sx = ((x0.x + x0.y) + (x0.z + x0.w)) + ((x1.x + x1.y) + (x1.z + x1.w));
+            acc[b] = fmaf(s4, fmaf(-z4, sx, t), acc[b]);
+        }
+    }
+}
+
 template <int WT, int LPR, int NCH, int K>
 struct Share {
     static constexpr int ROW_BYTES = row_bytes<WT, K>();
-    static_assert(LPR * NCH * 16 == ROW_BYTES, "tiling must cover a row");
-    float s4[NCH], z4[NCH];
+    // bytes per chunk: 16 (one uint4) for 16-bit and int8 weights, 4 (8 codes) for W4A16
+    static constexpr int CB = WT == FTTS_W4A16 ? 4 : 16;
+    static constexpr int EPC = WT == FTTS_W4A16 ? 8 : WInfo<WT>::EPC;  // weights per chunk
+    static_assert(LPR * NCH * CB == ROW_BYTES, "tiling must cover a row");
+    static_assert(WT != FTTS_W4A16 || NCH * EPC <= 128, "a W4A16 lane must stay within two groups");
+    float s4[2], z4[2];
     float rs, bias;
     int R;
     const char* buf;
@@ -278,12 +310,14 @@ struct Share {
         bias = bf16_to_f32(reinterpret_cast<const uint16_t*>(bias_p)[row]);
         rs = 1.f;
         if constexpr (WT == FTTS_W8A16) rs = bf16_to_f32(reinterpret_cast<const uint16_t*>(S)[row]);
+        // W4A16: a lane takes NCH consecutive 4-byte chunks (at most 128 columns), so
+        // it meets at most two quantisation groups: g0 and g0 + 1.
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) {
+        for (int i = 0; i < 2; ++i) {
             s4[i] = 0.f;
             z4[i] = 0.f;
             if constexpr (WT == FTTS_W4A16) {
-                const int g = ((li + i * LPR) * 32) >> 7;
+                const int g = min(((li * NCH * EPC) >> 7) + i, K / 128 - 1);
                 s4[i] = bf16_to_f32(reinterpret_cast<const uint16_t*>(S)[(size_t)row * (K / 128) + g]);
                 z4[i] = bf16_to_f32(reinterpret_cast<const uint16_t*>(Z)[(size_t)row * (K / 128) + g]);
             }
@@ -292,17 +326,27 @@ struct Share {
     // acc[b] = dot product of this thread's row with s_in[b] (+ bias); every lane of the row gets it.
     template <int B_>
     __device__ __forceinline__ void dot(const float* s_in, const float* s_xs, int B, float (&acc)[B_]) const {
-        constexpr int EPC = WInfo<WT>::EPC;
         const int t = fresh_tid();
         const int li = t & (LPR - 1);
         const int slot = min(t / LPR, R - 1);
-        const uint4* wrow = reinterpret_cast<const uint4*>(buf + slot * ROW_BYTES);
 #pragma unroll
         for (int b = 0; b < B_; ++b) acc[b] = 0.f;
+        if constexpr (WT == FTTS_W4A16) {
+            const uint32_t* wrow = reinterpret_cast<const uint32_t*>(buf + slot * ROW_BYTES);
+            const int g0 = (li * NCH * EPC) >> 7;
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-            const int c = li + i * LPR;
-            dot_chunk<WT, B_>(wrow[c], s_in + c * EPC, K, B, acc, s4[i], z4[i], s_xs + c, K / 32);
+            for (int i = 0; i < NCH; ++i) {
+                const int c = li * NCH + i;
+                const bool second = ((c * EPC) >> 7) != g0;
+                dot_w4_word<B_>(wrow[c], s_in + c * EPC, K, B, acc, second ? s4[1] : s4[0], second ? z4[1] : z4[0]);
+            }
+        } else {
+            const uint4* wrow = reinterpret_cast<const uint4*>(buf + slot * ROW_BYTES);
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) {
+                const int c = li + i * LPR;
+                dot_chunk<WT, B_>(wrow[c], s_in + c * EPC, K, B, acc, 0.f, 0.f, s_xs + c, K / 32);
+            }
         }
 #pragma unroll
         for (int b = 0; b < B_; ++b) acc[b] = fmaf(group_sum<LPR>(acc[b]), rs, bias);
