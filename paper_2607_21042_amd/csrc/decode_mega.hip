@@ -325,7 +325,7 @@ struct Share {
     }
     // acc[b] = dot product of this thread's row with s_in[b] (+ bias); every lane of the row gets it.
     template <int B_>
-    __device__ __forceinline__ void dot(const float* s_in, const float* s_xs, int B, float (&acc)[B_]) const {
+    __device__ __forceinline__ void dot(const float* s_in, int B, float (&acc)[B_]) const {
         const int t = fresh_tid();
         const int li = t & (LPR - 1);
         const int slot = min(t / LPR, R - 1);
@@ -345,7 +345,7 @@ struct Share {
 #pragma unroll
             for (int i = 0; i < NCH; ++i) {
                 const int c = li + i * LPR;
-                dot_chunk<WT, B_>(wrow[c], s_in + c * EPC, K, B, acc, 0.f, 0.f, s_xs + c, K / 32);
+                dot_chunk<WT, B_>(wrow[c], s_in + c * EPC, K, B, acc, 0.f, 0.f, nullptr, 0);
             }
         }
 #pragma unroll
@@ -363,14 +363,12 @@ struct LnCols {
     }
 };
 
-// LayerNorm of the B rows of s_x into s_in (and, for W4A16, the 32-column sums
-// of the result into s_xs).  Thread t < 320 (waves 0-4) normalises columns
+// LayerNorm of the B rows of s_x into s_in.  Thread t < 320 (waves 0-4) normalises columns
 // 4t .. 4t+3 of every row, so consecutive lanes touch consecutive LDS words;
 // each of those waves forms every row's mean and variance itself, so no
 // barrier is needed until the result is complete.
-template <int BMAX, bool SUMS>
-__device__ __forceinline__ void layer_norm(const float* s_x, float* s_in, float* s_xs, const LnCols& ln, float eps,
-                                           int B) {
+template <int BMAX>
+__device__ __forceinline__ void layer_norm(const float* s_x, float* s_in, const LnCols& ln, float eps, int B) {
     const int tid = fresh_tid(), lane = tid & 63;
     if (tid >= D / 4) return;  // whole waves
 #pragma unroll
@@ -402,24 +400,10 @@ __device__ __forceinline__ void layer_norm(const float* s_x, float* s_in, float*
             y.z = fmaf((v.z - m) * r, bf16lo(ln.g.y), bf16lo(ln.b.y));
             y.w = fmaf((v.w - m) * r, bf16hi(ln.g.y), bf16hi(ln.b.y));
             *reinterpret_cast<float4*>(s_in + b * D + tid * 4) = y;
-            if constexpr (SUMS) {
-                const float cs = group_sum<8>((y.x + y.y) + (y.z + y.w));
-                if ((lane & 7) == 0) s_xs[b * (D / 32) + (tid >> 3)] = cs;
-            }
         }
     }
 }
 
-// Per-32-column sums of the gathered activations (W4A16 only): eight
-// consecutive lanes hold one chunk's eight float4s.
-__device__ __forceinline__ void chunk_sums(const float* src, float* xs, int K, int B) {
-    const int total = B * K / 4;  // a multiple of 64
-    for (int i = fresh_tid(); i < total; i += NC) {
-        const float4 t = reinterpret_cast<const float4*>(src)[i];
-        const float cs = group_sum<8>((t.x + t.y) + (t.z + t.w));
-        if ((i & 7) == 0) xs[i >> 3] = cs;
-    }
-}
 
 // Online-softmax update of one wave's (m, lsum, o) with one 64-token page of
 // keys and values (page p of the sequence).  Slots at or past ncache, or of an
@@ -483,7 +467,6 @@ __device__ __forceinline__ void copy_wave(const Args& a, char* s_w, Sync& sy) {
     const int v0 = a.V * wg / G, nv = a.V * (wg + 1) / G - v0;
     const int nA = min(nv, kBuf / (2 * D));
     const bool is_att = wg < B * NH * a.att_split;
-    constexpr bool W4 = WT == FTTS_W4A16;
     constexpr int RD = row_bytes<WT, D>(), RF = row_bytes<WT, FF>();
 
     dma_rows(a.qkv_w.at(0), RD, q0, 3 * D / G, s_w);
@@ -513,7 +496,6 @@ __device__ __forceinline__ void copy_wave(const Args& a, char* s_w, Sync& sy) {
         MEGA_LMARK(l, 3);
         if (!follow(sy)) goto out;
         bar();  // attention partials merged
-        if constexpr (W4) bar();
         // P3
         bar();
         MEGA_LMARK(l, 4);
@@ -534,7 +516,6 @@ __device__ __forceinline__ void copy_wave(const Args& a, char* s_w, Sync& sy) {
             dma_rows(a.head_w, 2 * D, v0, nA, s_w);
         }
         if (!follow(sy)) goto out;
-        if constexpr (W4) bar();
     }
     // head
     bar();
@@ -553,11 +534,9 @@ out:
 template <int WT, int BMAX>
 __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
     using T = Tiles<WT>;
-    constexpr bool W4 = WT == FTTS_W4A16;
     __shared__ __attribute__((aligned(1024))) char s_w[2 * kBuf];     // weight shares, two buffers
     __shared__ __attribute__((aligned(16))) float s_in[BMAX * FF];    // phase input (normalised for LN phases)
     __shared__ __attribute__((aligned(16))) float s_x[BMAX * D];      // residual stream as last gathered
-    __shared__ __attribute__((aligned(16))) float s_xs[BMAX * FF / 32];  // W4A16 chunk sums
     __shared__ __attribute__((aligned(16))) float s_q[3 * 64];        // attention: q, k, v of the new token
     __shared__ float s_pm[NWC], s_pl[NWC], s_po[NWC][64];             // attention wave partials
     __shared__ float s_cv[BMAX][NC / HL];                             // head: per-slot best value
@@ -650,13 +629,13 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
             return;
         }
         MEGA_LMARK(l, 1);
-        layer_norm<BMAX, W4>(s_x, s_in, s_xs, ln, a.eps, B);
+        layer_norm<BMAX>(s_x, s_in, ln, a.eps, B);
         MEGA_LMARK(l, 13);
         bar();  // s_in complete; the copy wave has waited for the q/k/v share
         MEGA_LMARK(l, 2);
         {
             float acc[BMAX];
-            pq.template dot<BMAX>(s_in, s_xs, B, acc);
+            pq.template dot<BMAX>(s_in, B, acc);
             const int row = q0 + sq;
             const int li = tid & (T::QL - 1);
             if (sq < q1 - q0) {
@@ -799,13 +778,9 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         }
         bar();
         MEGA_LMARK(l, 6);
-        if constexpr (W4) {
-            chunk_sums(s_in, s_xs, D, B);
-            bar();
-        }
         {
             float acc[BMAX];
-            po.template dot<BMAX>(s_in, s_xs, B, acc);
+            po.template dot<BMAX>(s_in, B, acc);
             const int row = d0 + so;
             const int li = tid & (T::OL - 1);
             if (so < d1 - d0) {
@@ -821,12 +796,12 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         p2.params(a.fc2_s.at(l), a.fc2_z.at(l), a.fc2_b.at(l), d0, d1 - d0, s_w + kBuf);
         if (!gather<ux<BMAX>()>(a.ex_x, B * D, Flat{}, E(5 * l + 3), s_x, a.ctl, sy)) return;
         MEGA_LMARK(l, 8);
-        layer_norm<BMAX, W4>(s_x, s_in, s_xs, ln, a.eps, B);
+        layer_norm<BMAX>(s_x, s_in, ln, a.eps, B);
         bar();  // s_in complete; the copy wave has waited for the FC1 share
         MEGA_LMARK(l, 9);
         {
             float acc[BMAX];
-            p1.template dot<BMAX>(s_in, s_xs, B, acc);
+            p1.template dot<BMAX>(s_in, B, acc);
             const int row = f0 + s1;
             const int li = tid & (T::AL - 1);
             if (s1 < f1 - f0) {
@@ -842,13 +817,9 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
             pq.params(a.qkv_s.at(l + 1), a.qkv_z.at(l + 1), a.qkv_b.at(l + 1), q0, q1 - q0, s_w);
         if (!gather<uh<BMAX>()>(a.ex_h, B * FF, Flat{}, E(5 * l + 4), s_in, a.ctl, sy)) return;
         MEGA_LMARK(l, 11);
-        if constexpr (W4) {
-            chunk_sums(s_in, s_xs, FF, B);
-            bar();
-        }
         {
             float acc[BMAX];
-            p2.template dot<BMAX>(s_in, s_xs, B, acc);
+            p2.template dot<BMAX>(s_in, B, acc);
             const int row = d0 + s2;
             const int li = tid & (T::BL - 1);
             if (s2 < d1 - d0) {
@@ -867,7 +838,7 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
     ln.load(a.lnf_g, a.lnf_b);
     if (!gather<ux<BMAX>()>(a.ex_x, B * D, Flat{}, E(5 * a.n_layer), s_x, a.ctl, sy)) return;
     MEGA_MARK(1 + a.n_layer * kMarksPerLayer);
-    layer_norm<BMAX, false>(s_x, s_in, s_xs, ln, a.eps, B);
+    layer_norm<BMAX>(s_x, s_in, ln, a.eps, B);
     bar();  // s_in complete; the copy wave has waited for the head share
     MEGA_MARK(2 + a.n_layer * kMarksPerLayer);
     if (a.hidden && wg == 0) {  // the step's last-layer hidden state (every group holds the same rows)
@@ -876,7 +847,7 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
     }
     {
         float acc[BMAX];
-        ph.template dot<BMAX>(s_in, s_xs, B, acc);
+        ph.template dot<BMAX>(s_in, B, acc);
         const int row = v0 + sh;
         const int li = tid & (HL - 1);
         const bool mine = sh < v1 - v0;
