@@ -5,14 +5,16 @@
 // and is bound by HBM, but the per-row dot products of the GEMV family would
 // re-stage all activations in every workgroup and run 8-32 FMAs per weight on
 // the VALU.  Here each wave computes a 32 (sequences) x 32 (features) tile with
-// v_mfma_f32_32x32x16_bf16 over a range of K, reading its weight rows straight
-// from HBM into registers (no reuse, so no LDS staging) and the bf16 activations
-// (a few tens of KB, L2-resident) alongside.
+// v_mfma_f32_32x32x16_bf16 over a range of K: its weight rows come in through
+// coalesced direct-to-LDS loads (whole row runs per instruction; an operand read
+// in MFMA layout touches 32 rows, which as a global load would cost the address
+// units far more than the bytes), the bf16 activations (a few tens of KB,
+// L2-resident) straight into registers.
 //
 // Work split: a workgroup (4 waves) owns 32 features and one of S slices of K;
-// its waves take the slice's 32-column chunks (128 for W4A16, one quantisation
-// group) round robin, issue every load of their share at once (S is chosen so
-// that a share fits the registers), and add their tiles in LDS.  With S > 1 every workgroup
+// each wave takes a run of consecutive 32-column chunks (128 for W4A16, one
+// quantisation group) of the slice, issues every load of its share at once (S is
+// chosen so that a share fits), and the waves add their tiles in LDS.  With S > 1 every workgroup
 // stores its partial tile, and the last of the S to arrive (a per-tile counter)
 // adds the S partials in slice order -- the same order whatever the arrival
 // order, so results are reproducible -- and applies the epilogue; it also
@@ -35,17 +37,17 @@ constexpr int kBgemmMaxSplits = 12;  // K slices per feature tile (K <= 6144 for
 
 template <int WT> struct BChunk;  // one lane's share of one chunk
 template <> struct BChunk<FTTS_BF16> {
-    static constexpr int KC = 32, STEPS = 2;
+    static constexpr int KC = 32, STEPS = 2, CB = 64;  // CB: bytes of one weight row per chunk
     uint4 w[2];
     uint4 a[2];
 };
 template <> struct BChunk<FTTS_W8A16> {
-    static constexpr int KC = 32, STEPS = 2;
+    static constexpr int KC = 32, STEPS = 2, CB = 32;
     uint4 w[1];
     uint4 a[2];
 };
 template <> struct BChunk<FTTS_W4A16> {
-    static constexpr int KC = 128, STEPS = 8;
+    static constexpr int KC = 128, STEPS = 8, CB = 64;
     uint4 w[2];
     uint4 a[8];
     float s, z;
@@ -92,19 +94,55 @@ __device__ __forceinline__ void load_chunk(const BgemmArgs& p, int n, int m, int
 #pragma unroll
         for (int i = 0; i < (int)(sizeof(ch.a) / 16); ++i) ch.a[i] = ar[i];
     }
-    if constexpr (WT == FTTS_BF16) {
-        const uint4* w = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.w) + (size_t)nn * p.K + ka);
-        ch.w[0] = ld_stream(w);
-        ch.w[1] = ld_stream(w + 1);
-    } else if constexpr (WT == FTTS_W8A16) {
-        ch.w[0] = ld_stream(reinterpret_cast<const uint4*>(reinterpret_cast<const int8_t*>(p.w) + (size_t)nn * p.K + ka));
-    } else {
-        const uint4* w = reinterpret_cast<const uint4*>(reinterpret_cast<const uint32_t*>(p.w) + (size_t)nn * (p.K / 8) +
-                                                        c * 16 + h * 8);
-        ch.w[0] = ld_stream(w);
-        ch.w[1] = ld_stream(w + 1);
+    if constexpr (WT == FTTS_W4A16) {
         ch.s = bf16_to_f32(p.scale[(size_t)nn * (p.K / 128) + c]);
         ch.z = bf16_to_f32(p.zero[(size_t)nn * (p.K / 128) + c]);
+    }
+}
+
+// Weight staging.  A wave's chunks are consecutive, so each of its 32 rows is
+// one run of RB = CPW * CB bytes; direct-to-LDS loads bring the runs in with
+// 16 lanes (or fewer) per run and several whole runs per 1 KB instruction, and
+// the products read their operands from LDS.  The 16-byte pieces of row r are
+// stored XOR-swizzled by r (piece p at slot p ^ (r % pieces)) so that the 32
+// rows of one operand read fall into different banks.
+typedef __attribute__((address_space(3))) char bgemm_lds_char;
+__device__ __forceinline__ void lds_dma16(const char* src, char* dst) {
+    __builtin_amdgcn_global_load_lds(src, (bgemm_lds_char*)dst, 16, 0, 0);
+}
+template <int WT, bool LN> struct WStageShape {
+    static constexpr int RB = ChunksPerWave<WT, LN>::value * BChunk<WT>::CB;  // bytes per row
+    static constexpr int PIECES = RB / 16, BYTES = kBgemmRows * RB, OPS = BYTES / 1024;
+    static_assert(BYTES % 1024 == 0 && (PIECES & (PIECES - 1)) == 0, "staging shape");
+};
+
+template <int WT, bool LN>
+__device__ __forceinline__ void stage_weights(const BgemmArgs& p, int n0, int cw0, int c1, char* dst) {
+    using C = BChunk<WT>;
+    using SH = WStageShape<WT, LN>;
+    constexpr int PPC = C::CB / 16;  // pieces per chunk
+    const int lane = threadIdx.x & 63;
+    const size_t row_bytes = WT == FTTS_W4A16 ? (size_t)p.K / 2 : WT == FTTS_W8A16 ? (size_t)p.K : (size_t)p.K * 2;
+    const char* wb = reinterpret_cast<const char*>(p.w);
+#pragma unroll
+    for (int i = 0; i < SH::OPS; ++i) {
+        const int off = i * 1024 + lane * 16, r = off / SH::RB, q = (off % SH::RB) / 16;
+        const int pc = q ^ (r & (SH::PIECES - 1));                // the piece that lands in slot q
+        const int c = min(cw0 + pc / PPC, c1 - 1);                 // its chunk (past the slice: a repeat)
+        const int n = min(n0 + r, p.N - 1);
+        lds_dma16(wb + (size_t)n * row_bytes + (size_t)c * C::CB + (pc % PPC) * 16, dst + i * 1024);
+    }
+}
+
+// This lane's weight operands of local chunk j (row fr, k half h) from the staged rows.
+template <int WT, bool LN>
+__device__ __forceinline__ void read_weights(const char* src, int fr, int h, int j, BChunk<WT>& ch) {
+    using SH = WStageShape<WT, LN>;
+    constexpr int NW = (int)(sizeof(ch.w) / 16), PPC = BChunk<WT>::CB / 16;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        const int pc = j * PPC + h * NW + i, q = pc ^ (fr & (SH::PIECES - 1));
+        ch.w[i] = *reinterpret_cast<const uint4*>(src + fr * SH::RB + q * 16);
     }
 }
 
@@ -150,6 +188,7 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
     __shared__ __attribute__((aligned(16))) float s_b[LN ? kLnSliceMax : 4];
     __shared__ float2 s_gs[LN ? kLnGroups : 1][kBgemmRows];
     __shared__ float s_mean[kBgemmRows], s_rstd[kBgemmRows];
+    __shared__ __attribute__((aligned(1024))) char s_wt[kBgemmWaves][WStageShape<WT, LN>::BYTES];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int f = blockIdx.x, s = blockIdx.y, S = gridDim.y;
     const int n0 = f * kBgemmFeat;
@@ -194,13 +233,14 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
             pre.slot[i] = p.kv.seq_lens[m];
         }
     }
-    // 3. every input and weight load of this wave (chunks c0 + wave + 4j; indices
-    // past the slice repeat its last chunk and are not used)
+    // 3. every weight and input load of this wave: its chunks are c0 + wave * CPW + j
+    // (indices past the slice repeat its last chunk and are not used)
+    const int cw0 = c0 + wave * CPW;
+    stage_weights<WT, LN>(p, n0, cw0, c1, s_wt[wave]);
     C ch[CPW];
     XChunk<WT> xc[LN ? CPW : 1];
 #pragma unroll
-    for (int j = 0; j < CPW; ++j)
-        load_chunk<WT, LN>(p, n0 + fr, fr, h, min(c0 + wave + kBgemmWaves * j, c1 - 1), ch[j], xc[LN ? j : 0]);
+    for (int j = 0; j < CPW; ++j) load_chunk<WT, LN>(p, n0 + fr, fr, h, min(cw0 + j, c1 - 1), ch[j], xc[LN ? j : 0]);
     // Nothing that waits for a load may be scheduled above this point: every load
     // above is in flight before the first wait.
     __builtin_amdgcn_sched_barrier(0);
@@ -262,7 +302,7 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
 #pragma unroll
         for (int j = 0; j < CPW; ++j) {
             // 16-value aligned offset into the slice's gains/biases
-            const int kl = min(c0 + wave + kBgemmWaves * j, c1 - 1) * C::KC + h * (C::KC / 2) - k0;
+            const int kl = min(cw0 + j, c1 - 1) * C::KC + h * (C::KC / 2) - k0;
 #pragma unroll
             for (int i = 0; i < C::KC / 16; ++i) {
                 const float4 u = xc[j].x[2 * i], v = xc[j].x[2 * i + 1];
@@ -303,7 +343,8 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
     for (int i = 0; i < 16; ++i) acc[i] = 0.f;
 #pragma unroll
     for (int j = 0; j < CPW; ++j) {
-        if (c0 + wave + kBgemmWaves * j < c1) {
+        if (cw0 + j < c1) {
+            read_weights<WT, LN>(s_wt[wave], fr, h, j, ch[j]);
             bgemm_f32x16 part;
 #pragma unroll
             for (int i = 0; i < 16; ++i) part[i] = 0.f;
