@@ -393,22 +393,25 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
                      (unsigned)(S - 1);
         __syncthreads();
         if (!s_last) return;
-        // every partial load goes out before the first add (indices clamped, extras unused)
+        // Every partial load goes out before the first add; only the S slices that
+        // exist are read (uniform branches), the rest stay zero and add nothing.
         float pv[EPT][kBgemmMaxSplits];
 #pragma unroll
-        for (int i = 0; i < EPT; ++i) {
-            const int m = min(mrow(i), p.B - 1);
+        for (int k = 0; k < kBgemmMaxSplits; ++k) {
 #pragma unroll
-            for (int k = 0; k < kBgemmMaxSplits; ++k)
-                pv[i][k] = __hip_atomic_load(p.part + ((size_t)min(k, S - 1) * p.B + m) * p.N + ne, __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_AGENT);
+            for (int i = 0; i < EPT; ++i) pv[i][k] = 0.f;
+            if (k < S) {
+#pragma unroll
+                for (int i = 0; i < EPT; ++i)
+                    pv[i][k] = __hip_atomic_load(p.part + ((size_t)k * p.B + min(mrow(i), p.B - 1)) * p.N + ne,
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
         }
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
             float t = 0.f;
 #pragma unroll
-            for (int k = 0; k < kBgemmMaxSplits; ++k)
-                if (k < S) t += pv[i][k];
+            for (int k = 0; k < kBgemmMaxSplits; ++k) t += pv[i][k];
             v[i] = t;
         }
         if (tid == 0) __hip_atomic_store(p.count + f, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
