@@ -174,10 +174,153 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_kernel(const Attn
     }
 }
 
+// 16-bit KV cache.  Same walk and merge as above with a register budget that lets
+// two workgroups share a CU (at most 128 VGPRs): a page's K and V live in one set
+// of registers each, and the next page's K is requested as soon as the scores are
+// formed, its V as soon as the products are accumulated.  The activity flag, the
+// length, this wave's page ids and the query are requested together at the start
+// (nothing waits for the flag).  Scores use bf16 pair dot products against the
+// query split into hi + lo bf16 halves (about 16 significant bits), in the exp2
+// domain (query prescaled by 1/sqrt(64) * log2 e).
+__device__ __forceinline__ float dot8_bf16(const uint4 k, const uint32_t (&hi)[4], const uint32_t (&lo)[4], float t) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const uint32_t kw[4] = {k.x, k.y, k.z, k.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, kw[e]), __builtin_bit_cast(bf16x2, lo[e]), t,
+                                            false);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, kw[e]), __builtin_bit_cast(bf16x2, hi[e]), t,
+                                            false);
+    return t;
+}
+
+__device__ __forceinline__ void load_half_page(const uint16_t* base, size_t off, int lane, uint4 (&r)[8]) {
+    const uint4* p = reinterpret_cast<const uint4*>(base + off);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = p[i * 64 + lane];
+}
+
+__global__ __launch_bounds__(kAttnWaves * 64, 4) void attn_decode_bf16_kernel(const AttnDecodeArgs a) {
+    __shared__ float s_m[kAttnWaves], s_l[kAttnWaves];
+    __shared__ float s_o[kAttnWaves][kHeadDim];
+    const int h = blockIdx.x, b = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int grp = lane >> 3, sub = lane & 7;
+    const uint16_t* kvb = reinterpret_cast<const uint16_t*>(a.kv_base);
+    // independent loads, all in flight together
+    const int act = a.active[b];
+    const int len = a.seq_lens[b];
+    const int lp = w + kAttnWaves * lane;  // lane j: logical page w + 8 j
+    const int phys_l = a.block_table[(size_t)b * a.max_pages + min(lp, a.max_pages - 1)];
+    const float4* qp = reinterpret_cast<const float4*>(a.qkv + (size_t)b * a.qkv_stride + h * kHeadDim + sub * 8);
+    const float4 qa = qp[0], qb = qp[1];
+
+    const int ctx = act ? len + 1 : 0;      // cached slots incl. the new token
+    const int npg = (ctx + kPage - 1) / kPage;
+    const int my_pages = npg > w ? (npg - w + kAttnWaves - 1) / kAttnWaves : 0;
+    uint32_t qh[4], ql[4];
+    {
+        const float kScale = 0.125f * 1.44269504088896340736f;
+        const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float x0 = qv[2 * e] * kScale, x1 = qv[2 * e + 1] * kScale;
+            const uint16_t h0 = f32_to_bf16(x0), h1 = f32_to_bf16(x1);
+            qh[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+            ql[e] = (uint32_t)f32_to_bf16(x0 - bf16_to_f32(h0)) | ((uint32_t)f32_to_bf16(x1 - bf16_to_f32(h1)) << 16);
+        }
+    }
+    auto page_off = [&](int j, int kv, bool& ok) {
+        int phys = __shfl(phys_l, j, kWave);
+        ok = phys >= 0 && phys < a.n_pages;
+        phys = ok ? phys : 0;
+        return kv_offset(a.layer, a.n_pages, phys, kv, a.n_head, h, 0);
+    };
+    float m = -INFINITY, l = 0.f, o[8];
+#pragma unroll
+    for (int d = 0; d < 8; ++d) o[d] = 0.f;
+    uint4 K[8], V[8];
+    bool ok_k = false, ok_v = false;
+    if (my_pages > 0) {
+        load_half_page(kvb, page_off(0, 0, ok_k), lane, K);
+        load_half_page(kvb, page_off(0, 1, ok_v), lane, V);
+    }
+    for (int j = 0; j < my_pages; ++j) {
+        const int p = w + kAttnWaves * j;
+        const bool ok = ok_k;
+        float sc[8];
+        float pm = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const float t = group_sum<8>(dot8_bf16(K[i], qh, ql, 0.f));
+            const int tok = p * kPage + i * 8 + grp;
+            sc[i] = (ok && tok < ctx) ? t : -INFINITY;
+            pm = fmaxf(pm, sc[i]);
+        }
+        if (j + 1 < my_pages) load_half_page(kvb, page_off(j + 1, 0, ok_k), lane, K);
+        pm = stride8_max(pm);
+        if (pm > -INFINITY) {
+            const float mn = fmaxf(m, pm);
+            const float alpha = exp2f(m - mn);  // 0 on this wave's first valid page
+            m = mn;
+            l *= alpha;
+#pragma unroll
+            for (int d = 0; d < 8; ++d) o[d] *= alpha;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                // slots past the context (or of an invalid page) may hold anything:
+                // keep them out of the sum (0 * NaN would poison it)
+                if (sc[i] > -INFINITY) {
+                    const float pr = exp2f(sc[i] - m);
+                    float vv[8];
+                    vv[0] = bf16lo(V[i].x); vv[1] = bf16hi(V[i].x); vv[2] = bf16lo(V[i].y); vv[3] = bf16hi(V[i].y);
+                    vv[4] = bf16lo(V[i].z); vv[5] = bf16hi(V[i].z); vv[6] = bf16lo(V[i].w); vv[7] = bf16hi(V[i].w);
+                    l += pr;
+#pragma unroll
+                    for (int d = 0; d < 8; ++d) o[d] = fmaf(pr, vv[d], o[d]);
+                }
+            }
+        }
+        if (j + 1 < my_pages) load_half_page(kvb, page_off(j + 1, 1, ok_v), lane, V);
+    }
+#pragma unroll
+    for (int d = 0; d < 8; ++d) o[d] = stride8_sum(o[d]);
+    l = stride8_sum(l);
+    if (lane < 8) {
+#pragma unroll
+        for (int d = 0; d < 8; ++d) s_o[w][lane * 8 + d] = o[d];
+    }
+    if (lane == 0) {
+        s_m[w] = m;
+        s_l[w] = l;
+    }
+    __syncthreads();
+    if (tid < kHeadDim) {                   // log-sum-exp merge of the wave partials (exp2 domain)
+        float M = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < kAttnWaves; ++i) M = fmaxf(M, s_m[i]);
+        float L = 0.f, acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < kAttnWaves; ++i) {
+            if (s_m[i] > -INFINITY) {
+                const float wgt = exp2f(s_m[i] - M);
+                L = fmaf(s_l[i], wgt, L);
+                acc = fmaf(s_o[i][tid], wgt, acc);
+            }
+        }
+        const float r = L > 0.f ? acc / L : 0.f;
+        const size_t oi = (size_t)b * a.o_stride + h * kHeadDim + tid;
+        if (a.o_bf16) a.o_bf16[oi] = f32_to_bf16(r);
+        else a.o[oi] = r;
+    }
+}
+
 hipError_t launch_attn_decode(int wdtype, const AttnDecodeArgs& a, int B, hipStream_t st) {
     const dim3 g(a.n_head, B);
     if (wdtype == FTTS_F32) hipLaunchKernelGGL(attn_decode_kernel<true>, g, dim3(kAttnWaves * 64), 0, st, a);
-    else hipLaunchKernelGGL(attn_decode_kernel<false>, g, dim3(kAttnWaves * 64), 0, st, a);
+    else hipLaunchKernelGGL(attn_decode_bf16_kernel, g, dim3(kAttnWaves * 64), 0, st, a);
     return hipGetLastError();
 }
 
