@@ -53,10 +53,11 @@ template <> struct BChunk<FTTS_W4A16> {
     float s, z;
 };
 
-// Chunks a wave holds in registers at once (its whole share of a K slice).  With
-// the LayerNorm input a W4A16 lane holds 64 fp32 inputs per chunk, so one chunk.
+// Chunks per wave (its whole share of a K slice).  A LayerNorm input is staged as
+// fp32 rows in LDS (32 rows x 64 columns per wave, 128 for W4A16), which keeps
+// three workgroups per CU.
 constexpr int kBgemmWaves = 4, kBgemmThreads = kBgemmWaves * 64;
-template <int WT, bool LN> struct ChunksPerWave { static constexpr int value = 4; };
+template <int WT, bool LN> struct ChunksPerWave { static constexpr int value = LN ? 2 : 4; };
 template <> struct ChunksPerWave<FTTS_W4A16, false> { static constexpr int value = 2; };
 template <> struct ChunksPerWave<FTTS_W4A16, true> { static constexpr int value = 1; };
 
@@ -65,30 +66,21 @@ template <> struct ChunksPerWave<FTTS_W4A16, true> { static constexpr int value 
 constexpr int kLnGroups = kBgemmThreads / kBgemmRows;
 constexpr int kLnMaxTP = 8;                                  // tiles per group: K <= 2048
 constexpr int kLnMaxK = kLnGroups * kLnMaxTP * kStatTile;
-constexpr int kLnSliceMax = 1024;                            // >= CPW * waves * KC for every mode
-constexpr int kLnGbPer = kLnSliceMax / kBgemmThreads;
 
-template <int WT> struct XChunk { float4 x[BChunk<WT>::KC / 8]; };  // a lane's KC/2 fp32 inputs
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
 template <int WT, bool LN>
-__device__ __forceinline__ void load_chunk(const BgemmArgs& p, int n, int m, int h, int c, BChunk<WT>& ch,
-                                           XChunk<WT>& xc) {
+__device__ __forceinline__ void load_chunk(const BgemmArgs& p, int n, int m, int h, int c, BChunk<WT>& ch) {
     using C = BChunk<WT>;
     const int nn = min(n, p.N - 1);
     const int ka = c * C::KC + h * (C::KC / 2);
     // Every load is unconditional (rows past the batch read the last row and are
     // zeroed afterwards), so the loads of all chunks stay in flight together.
     const int mr = min(m, p.B - 1);
-    if constexpr (LN) {
-        // fp32 row m, normalised once the statistics are in
-        const float4* xr = reinterpret_cast<const float4*>(p.ln_x + (size_t)mr * p.K + ka);
-#pragma unroll
-        for (int i = 0; i < C::KC / 8; ++i) xc.x[i] = xr[i];
-    } else {
+    if constexpr (!LN) {
         // bf16 row m: 8 x 16 bytes for W4A16, 2 otherwise
         const uint4* ar = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.act) + (size_t)mr * p.K + ka);
 #pragma unroll
@@ -146,6 +138,38 @@ __device__ __forceinline__ void read_weights(const char* src, int fr, int h, int
     }
 }
 
+// LayerNorm input staging: this wave's 32 fp32 rows over its CPW chunks, RBX bytes
+// a row, by the same 1 KB direct-to-LDS loads and the same XOR swizzle of 16-byte
+// pieces.  Rows past the batch repeat the last row (their outputs are zeroed).
+template <int WT> struct XStageShape {
+    static constexpr int RBX = ChunksPerWave<WT, true>::value * BChunk<WT>::KC * 4;
+    static constexpr int PIECES = RBX / 16, BYTES = kBgemmRows * RBX, OPS = BYTES / 1024;
+    static_assert(BYTES % 1024 == 0 && (PIECES & (PIECES - 1)) == 0, "input staging shape");
+};
+
+template <int WT>
+__device__ __forceinline__ void stage_x(const BgemmArgs& p, int cw0, int c1, char* dst) {
+    using SH = XStageShape<WT>;
+    constexpr int KC = BChunk<WT>::KC;
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < SH::OPS; ++i) {
+        const int off = i * 1024 + lane * 16, r = off / SH::RBX, q = (off % SH::RBX) / 16;
+        const int pc = q ^ (r & (SH::PIECES - 1));  // the piece that lands in slot q: columns pc*4 .. +3
+        const int c = min(cw0 + pc * 4 / KC, c1 - 1);
+        const float* src = p.ln_x + (size_t)min(r, p.B - 1) * p.K + (size_t)c * KC + (pc * 4) % KC;
+        lds_dma16(reinterpret_cast<const char*>(src), dst + i * 1024);
+    }
+}
+
+// Four consecutive fp32 inputs of row fr at column kl of this wave's staged run.
+template <int WT>
+__device__ __forceinline__ float4 read_x4(const char* src, int fr, int kl) {
+    using SH = XStageShape<WT>;
+    const int q = (kl >> 2) ^ (fr & (SH::PIECES - 1));
+    return *reinterpret_cast<const float4*>(src + fr * SH::RBX + q * 16);
+}
+
 // The weight operand of MFMA step st (8 bf16; quantised codes expanded exactly).
 template <int WT>
 __device__ __forceinline__ bgemm_bf16x8 w_operand(const BChunk<WT>& ch, int st) {
@@ -181,11 +205,13 @@ template <int WT, int EPI, bool LN>
 __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p) {
     using C = BChunk<WT>;
     constexpr int CPW = ChunksPerWave<WT, LN>::value, NT = kBgemmThreads, EPT = kBgemmEpt;
-    static_assert(CPW * kBgemmWaves * C::KC <= kLnSliceMax, "LayerNorm slice does not fit");
-    __shared__ float s_red[kBgemmWaves][kBgemmRows * kBgemmFeat];
+    constexpr int SLICE = CPW * kBgemmWaves * C::KC, GBPER = (SLICE + NT - 1) / NT;  // columns of a K slice
+    // the wave tiles are added in LDS: in the staged inputs once those are read
+    __shared__ float s_red[LN ? 1 : kBgemmWaves][LN ? 1 : kBgemmRows * kBgemmFeat];
+    __shared__ __attribute__((aligned(1024))) char s_xs[LN ? kBgemmWaves : 1][LN ? XStageShape<WT>::BYTES : 16];
     __shared__ int s_last;
-    __shared__ __attribute__((aligned(16))) float s_g[LN ? kLnSliceMax : 4];
-    __shared__ __attribute__((aligned(16))) float s_b[LN ? kLnSliceMax : 4];
+    __shared__ __attribute__((aligned(16))) float s_g[LN ? SLICE : 4];
+    __shared__ __attribute__((aligned(16))) float s_b[LN ? SLICE : 4];
     __shared__ float2 s_gs[LN ? kLnGroups : 1][kBgemmRows];
     __shared__ float s_mean[kBgemmRows], s_rstd[kBgemmRows];
     __shared__ __attribute__((aligned(1024))) char s_wt[kBgemmWaves][WStageShape<WT, LN>::BYTES];
@@ -203,14 +229,14 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
     const int T = p.K / kStatTile, TP = (T + kLnGroups - 1) / kLnGroups;
     const int lr = tid & (kBgemmRows - 1), lq = tid >> 5;
     float2 st[LN ? kLnMaxTP : 1];
-    uint16_t gr[LN ? kLnGbPer : 1], br[LN ? kLnGbPer : 1];
+    uint16_t gr[LN ? GBPER : 1], br[LN ? GBPER : 1];
     const int k0 = c0 * C::KC, kn = (c1 - c0) * C::KC;
     if constexpr (LN) {
         const int m = min(lr, p.B - 1);
 #pragma unroll
         for (int j = 0; j < kLnMaxTP; ++j) st[j] = p.ln_stats[(size_t)min(lq * TP + j, T - 1) * p.stats_ld + m];
 #pragma unroll
-        for (int j = 0; j < kLnGbPer; ++j) {
+        for (int j = 0; j < GBPER; ++j) {
             const int k = min(tid + NT * j, kn - 1);
             gr[j] = reinterpret_cast<const uint16_t*>(p.ln_g)[k0 + k];
             br[j] = reinterpret_cast<const uint16_t*>(p.ln_b)[k0 + k];
@@ -237,10 +263,10 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
     // (indices past the slice repeat its last chunk and are not used)
     const int cw0 = c0 + wave * CPW;
     stage_weights<WT, LN>(p, n0, cw0, c1, s_wt[wave]);
+    if constexpr (LN) stage_x<WT>(p, cw0, c1, s_xs[wave]);
     C ch[CPW];
-    XChunk<WT> xc[LN ? CPW : 1];
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) load_chunk<WT, LN>(p, n0 + fr, fr, h, min(cw0 + j, c1 - 1), ch[j], xc[LN ? j : 0]);
+    for (int j = 0; j < CPW; ++j) load_chunk<WT, LN>(p, n0 + fr, fr, h, min(cw0 + j, c1 - 1), ch[j]);
     // Nothing that waits for a load may be scheduled above this point: every load
     // above is in flight before the first wait.
     __builtin_amdgcn_sched_barrier(0);
@@ -271,7 +297,7 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
         }
         s_gs[lq][lr] = make_float2(sum, m2);
 #pragma unroll
-        for (int j = 0; j < kLnGbPer; ++j)
+        for (int j = 0; j < GBPER; ++j)
             if (tid + NT * j < kn) {
                 s_g[tid + NT * j] = bf16_to_f32(gr[j]);
                 s_b[tid + NT * j] = bf16_to_f32(br[j]);
@@ -303,9 +329,11 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
         for (int j = 0; j < CPW; ++j) {
             // 16-value aligned offset into the slice's gains/biases
             const int kl = min(cw0 + j, c1 - 1) * C::KC + h * (C::KC / 2) - k0;
+            const int kx = j * C::KC + h * (C::KC / 2);  // the same column in this wave's staged run
 #pragma unroll
             for (int i = 0; i < C::KC / 16; ++i) {
-                const float4 u = xc[j].x[2 * i], v = xc[j].x[2 * i + 1];
+                const float4 u = read_x4<WT>(s_xs[wave], fr, kx + 8 * i);
+                const float4 v = read_x4<WT>(s_xs[wave], fr, kx + 8 * i + 4);
                 const float4 g0 = *reinterpret_cast<const float4*>(s_g + kl + 8 * i);
                 const float4 g1 = *reinterpret_cast<const float4*>(s_g + kl + 8 * i + 4);
                 const float4 b0 = *reinterpret_cast<const float4*>(s_b + kl + 8 * i);
@@ -363,8 +391,12 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
         }
     }
     // acc[i] holds (sequence m, feature n0 + fr): m = (i / 4) * 8 + h * 4 + i % 4
+    auto red = [&](int w) { return LN ? reinterpret_cast<float*>(s_xs[w]) : s_red[LN ? 0 : w]; };
+    {
+        float* r = red(wave);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s_red[wave][((i >> 2) * 8 + h * 4 + (i & 3)) * kBgemmFeat + fr] = acc[i];
+        for (int i = 0; i < 16; ++i) r[((i >> 2) * 8 + h * 4 + (i & 3)) * kBgemmFeat + fr] = acc[i];
+    }
     __syncthreads();
     float v[EPT];
 #pragma unroll
@@ -372,7 +404,7 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
         const int e = tid + NT * i;
         float t = 0.f;
 #pragma unroll
-        for (int w = 0; w < kBgemmWaves; ++w) t += s_red[w][e];
+        for (int w = 0; w < kBgemmWaves; ++w) t += red(w)[e];
         v[i] = t;
     }
     if (S > 1) {
@@ -479,7 +511,8 @@ int bgemm_splits(int wdtype, int N, int K, bool ln) {
     const int kc = wdtype == FTTS_W4A16 ? 128 : 32;
     const int cpw = wdtype == FTTS_W4A16 ? (ln ? ChunksPerWave<FTTS_W4A16, true>::value
                                                : ChunksPerWave<FTTS_W4A16, false>::value)
-                                         : ChunksPerWave<FTTS_BF16, false>::value;
+                                         : (ln ? ChunksPerWave<FTTS_BF16, true>::value
+                                               : ChunksPerWave<FTTS_BF16, false>::value);
     const int chunks = K / kc, per_group = kBgemmWaves * cpw;
     return (chunks + per_group - 1) / per_group;
 }

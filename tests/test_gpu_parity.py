@@ -316,9 +316,13 @@ def test_batched_decode_matrix_core_linears(torch_cuda, mode, B):
     ragged one): ragged prefixes, sequences retiring at different steps, every
     logit against the oracle, and bit-identical logits with the pages permuted
     and from run to run (the split-K sums have a fixed order)."""
-    from paper_2607_21042_amd import ftts
     shape = workload.TINY
-    inputs = model_inputs(shape, mode, workload.master_weights(shape, seed=0))
+    batched_case(shape, workload.master_weights(shape, seed=0), mode, B)
+
+
+def batched_case(shape, master, mode, B):
+    from paper_2607_21042_amd import ftts
+    inputs = model_inputs(shape, mode, master)
     rng = np.random.default_rng(11)
     lens = [int(x) for x in rng.integers(1, 150, size=B)]
     flat = workload.prefix_embeddings(lens, shape.d_model, seed=1)
@@ -498,6 +502,13 @@ def decode_path():
 @pytest.fixture(scope="module")
 def mid_master():
     return workload.master_weights(MID, seed=0)
+
+
+@pytest.mark.parametrize("mode,B", [("bf16", 33), ("w8a16", 9), ("w4a16", 33)])
+def test_batched_decode_model_width(torch_cuda, mid_master, mode, B):
+    """The batched linears at d=1280 / FFN 5120 (several K slices per feature tile
+    and the split-K fixup on every linear): the same checks as for the tiny model."""
+    batched_case(MID, mid_master, mode, B)
 
 
 @pytest.mark.parametrize("mode", ["bf16", "w8a16", "w4a16"])
