@@ -32,7 +32,7 @@ typedef __bf16 bgemm_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float bgemm_f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kBgemmRows = 32;  // sequences per launch
-constexpr int kBgemmFeat = 32;  // features per workgroup
+constexpr int kBgemmFeat = 32;  // features per MFMA tile (a workgroup owns FT tiles)
 constexpr int kBgemmMaxSplits = 12;  // K slices per feature tile (K <= 6144 for bf16 / W8A16)
 
 template <int WT> struct BChunk;  // one lane's share of one chunk
@@ -102,16 +102,16 @@ typedef __attribute__((address_space(3))) char bgemm_lds_char;
 __device__ __forceinline__ void lds_dma16(const char* src, char* dst) {
     __builtin_amdgcn_global_load_lds(src, (bgemm_lds_char*)dst, 16, 0, 0);
 }
-template <int WT, bool LN> struct WStageShape {
+template <int WT, bool LN, int FT> struct WStageShape {
     static constexpr int RB = ChunksPerWave<WT, LN>::value * BChunk<WT>::CB;  // bytes per row
-    static constexpr int PIECES = RB / 16, BYTES = kBgemmRows * RB, OPS = BYTES / 1024;
+    static constexpr int PIECES = RB / 16, BYTES = FT * kBgemmFeat * RB, OPS = BYTES / 1024;
     static_assert(BYTES % 1024 == 0 && (PIECES & (PIECES - 1)) == 0, "staging shape");
 };
 
-template <int WT, bool LN>
+template <int WT, bool LN, int FT>
 __device__ __forceinline__ void stage_weights(const BgemmArgs& p, int n0, int cw0, int c1, char* dst) {
     using C = BChunk<WT>;
-    using SH = WStageShape<WT, LN>;
+    using SH = WStageShape<WT, LN, FT>;
     constexpr int PPC = C::CB / 16;  // pieces per chunk
     const int lane = threadIdx.x & 63;
     const size_t row_bytes = WT == FTTS_W4A16 ? (size_t)p.K / 2 : WT == FTTS_W8A16 ? (size_t)p.K : (size_t)p.K * 2;
@@ -127,9 +127,9 @@ __device__ __forceinline__ void stage_weights(const BgemmArgs& p, int n0, int cw
 }
 
 // This lane's weight operands of local chunk j (row fr, k half h) from the staged rows.
-template <int WT, bool LN>
+template <int WT, bool LN, int FT>
 __device__ __forceinline__ void read_weights(const char* src, int fr, int h, int j, BChunk<WT>& ch) {
-    using SH = WStageShape<WT, LN>;
+    using SH = WStageShape<WT, LN, FT>;
     constexpr int NW = (int)(sizeof(ch.w) / 16), PPC = BChunk<WT>::CB / 16;
 #pragma unroll
     for (int i = 0; i < NW; ++i) {
@@ -192,38 +192,44 @@ __device__ __forceinline__ bgemm_bf16x8 w_operand(const BChunk<WT>& ch, int st) 
 
 // Everything the epilogue reads that does not depend on the products, loaded at
 // the start so that it arrives while the weights stream in.
-constexpr int kBgemmEpt = kBgemmRows * kBgemmFeat / kBgemmThreads;  // tile elements per thread
-template <int WT, int EPI> struct EpiPre {
+template <int EPT> struct EpiPre {
     float bias, scale;
-    float xold[kBgemmEpt];   // EPI_RESID
-    int on[kBgemmEpt];       // EPI_QKV: the row is active (appends its key and value)
-    int slot[kBgemmEpt];     //          at this KV slot
-    int phys[kBgemmEpt];     //          in this physical page
+    float xold[EPT];   // EPI_RESID
+    int on[EPT];       // EPI_QKV: the row is active (appends its key and value)
+    int slot[EPT];     //          at this KV slot
+    int phys[EPT];     //          in this physical page
 };
 
-template <int WT, int EPI, bool LN>
+// FT = 2: the workgroup owns 64 features (each wave two MFMA tiles over its chunks),
+// which halves the input rows staged per weight byte; used for the wide
+// LayerNorm-fused linears.
+template <int WT, int EPI, bool LN, int FT>
 __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p) {
     using C = BChunk<WT>;
-    constexpr int CPW = ChunksPerWave<WT, LN>::value, NT = kBgemmThreads, EPT = kBgemmEpt;
+    constexpr int FEAT = FT * kBgemmFeat, EPT = kBgemmRows * FEAT / kBgemmThreads;
+    constexpr int CPW = ChunksPerWave<WT, LN>::value, NT = kBgemmThreads;
+    constexpr int MAXS = FT == 1 ? kBgemmMaxSplits : 8;
+    static_assert(FT == 1 || (WT != FTTS_W4A16 && EPI != EPI_RESID), "two tiles per wave: 16-bit / int8 only, no stats");
+    static_assert(!LN || XStageShape<WT>::BYTES >= kBgemmRows * FEAT * 4, "wave tile must fit the staged inputs");
     constexpr int SLICE = CPW * kBgemmWaves * C::KC, GBPER = (SLICE + NT - 1) / NT;  // columns of a K slice
     // the wave tiles are added in LDS: in the staged inputs once those are read
-    __shared__ float s_red[LN ? 1 : kBgemmWaves][LN ? 1 : kBgemmRows * kBgemmFeat];
+    __shared__ float s_red[LN ? 1 : kBgemmWaves][LN ? 1 : kBgemmRows * FEAT];
     __shared__ __attribute__((aligned(1024))) char s_xs[LN ? kBgemmWaves : 1][LN ? XStageShape<WT>::BYTES : 16];
     __shared__ int s_last;
     __shared__ __attribute__((aligned(16))) float s_g[LN ? SLICE : 4];
     __shared__ __attribute__((aligned(16))) float s_b[LN ? SLICE : 4];
     __shared__ float2 s_gs[LN ? kLnGroups : 1][kBgemmRows];
     __shared__ float s_mean[kBgemmRows], s_rstd[kBgemmRows];
-    __shared__ __attribute__((aligned(1024))) char s_wt[kBgemmWaves][WStageShape<WT, LN>::BYTES];
+    __shared__ __attribute__((aligned(1024))) char s_wt[kBgemmWaves][WStageShape<WT, LN, FT>::BYTES];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int f = blockIdx.x, s = blockIdx.y, S = gridDim.y;
-    const int n0 = f * kBgemmFeat;
+    const int n0 = f * FEAT;
     const int fr = lane & 31, h = lane >> 5;
     const int nchunks = p.K / C::KC;
     const int c0 = s * nchunks / S, c1 = (s + 1) * nchunks / S;
     // this thread's epilogue elements: feature ne, rows mrow(i)
-    const int ne = min(n0 + (tid & (kBgemmFeat - 1)), p.N - 1);
-    auto mrow = [&](int i) { return (tid >> 5) + (NT / kBgemmFeat) * i; };
+    const int ne = min(n0 + (tid & (FEAT - 1)), p.N - 1);
+    auto mrow = [&](int i) { return tid / FEAT + (NT / FEAT) * i; };
 
     // 1. LayerNorm inputs: this thread's (row, tile group) statistics, the slice's gains/biases.
     const int T = p.K / kStatTile, TP = (T + kLnGroups - 1) / kLnGroups;
@@ -243,7 +249,7 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
         }
     }
     // 2. epilogue operands
-    EpiPre<WT, EPI> pre;
+    EpiPre<EPT> pre;
     pre.bias = bf16_to_f32(reinterpret_cast<const uint16_t*>(p.bias)[ne]);
     pre.scale = WT == FTTS_W8A16 ? bf16_to_f32(p.scale[ne]) : 1.f;
     if constexpr (EPI == EPI_RESID) {
@@ -262,7 +268,7 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
     // 3. every weight and input load of this wave: its chunks are c0 + wave * CPW + j
     // (indices past the slice repeat its last chunk and are not used)
     const int cw0 = c0 + wave * CPW;
-    stage_weights<WT, LN>(p, n0, cw0, c1, s_wt[wave]);
+    stage_weights<WT, LN, FT>(p, n0, cw0, c1, s_wt[wave]);
     if constexpr (LN) stage_x<WT>(p, cw0, c1, s_xs[wave]);
     C ch[CPW];
 #pragma unroll
@@ -365,37 +371,44 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
                 for (int i = 0; i < (int)(sizeof(ch[j].a) / 16); ++i) ch[j].a[i] = make_uint4(0, 0, 0, 0);
         }
     }
-    // 5. products
-    bgemm_f32x16 acc;
+    // 5. products: tile t covers features n0 + 32 t ..
+    bgemm_f32x16 acc[FT];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+    for (int t = 0; t < FT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[t][i] = 0.f;
 #pragma unroll
     for (int j = 0; j < CPW; ++j) {
         if (cw0 + j < c1) {
-            read_weights<WT, LN>(s_wt[wave], fr, h, j, ch[j]);
-            bgemm_f32x16 part;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) part[i] = 0.f;
+            for (int t = 0; t < FT; ++t) {
+                read_weights<WT, LN, FT>(s_wt[wave], fr + kBgemmFeat * t, h, j, ch[j]);
+                bgemm_f32x16 part;
 #pragma unroll
-            for (int st2 = 0; st2 < C::STEPS; ++st2) {
-                const bgemm_bf16x8 av = __builtin_bit_cast(bgemm_bf16x8, ch[j].a[st2]);
-                part = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, w_operand<WT>(ch[j], st2), part, 0, 0, 0);
-            }
-            if constexpr (WT == FTTS_W4A16) {
+                for (int i = 0; i < 16; ++i) part[i] = 0.f;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) acc[i] = fmaf(ch[j].s, part[i], acc[i]);
-            } else {
+                for (int st2 = 0; st2 < C::STEPS; ++st2) {
+                    const bgemm_bf16x8 av = __builtin_bit_cast(bgemm_bf16x8, ch[j].a[st2]);
+                    part = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, w_operand<WT>(ch[j], st2), part, 0, 0, 0);
+                }
+                if constexpr (WT == FTTS_W4A16) {
 #pragma unroll
-                for (int i = 0; i < 16; ++i) acc[i] += part[i];
+                    for (int i = 0; i < 16; ++i) acc[t][i] = fmaf(ch[j].s, part[i], acc[t][i]);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) acc[t][i] += part[i];
+                }
             }
         }
     }
-    // acc[i] holds (sequence m, feature n0 + fr): m = (i / 4) * 8 + h * 4 + i % 4
+    // acc[t][i] holds (sequence m, feature n0 + 32 t + fr): m = (i / 4) * 8 + h * 4 + i % 4
     auto red = [&](int w) { return LN ? reinterpret_cast<float*>(s_xs[w]) : s_red[LN ? 0 : w]; };
     {
         float* r = red(wave);
 #pragma unroll
-        for (int i = 0; i < 16; ++i) r[((i >> 2) * 8 + h * 4 + (i & 3)) * kBgemmFeat + fr] = acc[i];
+        for (int t = 0; t < FT; ++t)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) r[((i >> 2) * 8 + h * 4 + (i & 3)) * FEAT + kBgemmFeat * t + fr] = acc[t][i];
     }
     __syncthreads();
     float v[EPT];
@@ -413,7 +426,7 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
         // any cache flush.
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
-            const int m = mrow(i), n = n0 + (tid & (kBgemmFeat - 1));
+            const int m = mrow(i), n = n0 + (tid & (FEAT - 1));
             if (m < p.B && n < p.N)
                 __hip_atomic_store(p.part + ((size_t)s * p.B + m) * p.N + n, v[i], __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
@@ -427,9 +440,9 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
         if (!s_last) return;
         // Every partial load goes out before the first add; only the S slices that
         // exist are read (uniform branches), the rest stay zero and add nothing.
-        float pv[EPT][kBgemmMaxSplits];
+        float pv[EPT][MAXS];
 #pragma unroll
-        for (int k = 0; k < kBgemmMaxSplits; ++k) {
+        for (int k = 0; k < MAXS; ++k) {
 #pragma unroll
             for (int i = 0; i < EPT; ++i) pv[i][k] = 0.f;
             if (k < S) {
@@ -443,13 +456,13 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
         for (int i = 0; i < EPT; ++i) {
             float t = 0.f;
 #pragma unroll
-            for (int k = 0; k < kBgemmMaxSplits; ++k) t += pv[i][k];
+            for (int k = 0; k < MAXS; ++k) t += pv[i][k];
             v[i] = t;
         }
         if (tid == 0) __hip_atomic_store(p.count + f, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     // 6. epilogue
-    const bool col_ok = n0 + (tid & (kBgemmFeat - 1)) < p.N;
+    const bool col_ok = n0 + (tid & (FEAT - 1)) < p.N;
     float xn[EPT];
 #pragma unroll
     for (int i = 0; i < EPT; ++i) {
@@ -483,22 +496,32 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
 #pragma unroll
             for (int i = 0; i < EPT; ++i) {
                 const float2 ts = tile_stats32(xn[i]);
-                if ((tid & (kBgemmFeat - 1)) == 0 && mrow(i) < p.B) p.stats_out[(size_t)f * p.stats_ld + mrow(i)] = ts;
+                if ((tid & (FEAT - 1)) == 0 && mrow(i) < p.B) p.stats_out[(size_t)f * p.stats_ld + mrow(i)] = ts;
             }
         }
     }
 }
 
 template <int WT, bool LN>
-static hipError_t bgemm_by_epi(int epi, const BgemmArgs& a, dim3 g, hipStream_t st) {
+static hipError_t bgemm_by_epi(int epi, int ft, const BgemmArgs& a, dim3 g, hipStream_t st) {
     const dim3 blk(kBgemmThreads);
+    constexpr bool two = LN && WT != FTTS_W4A16;  // the only instantiations with FT = 2
     switch (epi) {
-        case EPI_STORE: hipLaunchKernelGGL((bgemm_kernel<WT, EPI_STORE, LN>), g, blk, 0, st, a); break;
-        case EPI_QKV: hipLaunchKernelGGL((bgemm_kernel<WT, EPI_QKV, LN>), g, blk, 0, st, a); break;
-        case EPI_GELU: hipLaunchKernelGGL((bgemm_kernel<WT, EPI_GELU, LN>), g, blk, 0, st, a); break;
+        case EPI_STORE:
+            if (two && ft == 2) hipLaunchKernelGGL((bgemm_kernel<WT, EPI_STORE, LN, two ? 2 : 1>), g, blk, 0, st, a);
+            else hipLaunchKernelGGL((bgemm_kernel<WT, EPI_STORE, LN, 1>), g, blk, 0, st, a);
+            break;
+        case EPI_QKV:
+            if (two && ft == 2) hipLaunchKernelGGL((bgemm_kernel<WT, EPI_QKV, LN, two ? 2 : 1>), g, blk, 0, st, a);
+            else hipLaunchKernelGGL((bgemm_kernel<WT, EPI_QKV, LN, 1>), g, blk, 0, st, a);
+            break;
+        case EPI_GELU:
+            if (two && ft == 2) hipLaunchKernelGGL((bgemm_kernel<WT, EPI_GELU, LN, two ? 2 : 1>), g, blk, 0, st, a);
+            else hipLaunchKernelGGL((bgemm_kernel<WT, EPI_GELU, LN, 1>), g, blk, 0, st, a);
+            break;
         case EPI_RESID:
             if constexpr (LN) return hipErrorInvalidValue;  // the residual update never normalises its input
-            else hipLaunchKernelGGL((bgemm_kernel<WT, EPI_RESID, false>), g, blk, 0, st, a);
+            else hipLaunchKernelGGL((bgemm_kernel<WT, EPI_RESID, false, 1>), g, blk, 0, st, a);
             break;
         default: return hipErrorInvalidValue;
     }
@@ -530,7 +553,18 @@ hipError_t launch_bgemm(int wdtype, int epi, const BgemmArgs& in, hipStream_t st
     if (!bgemm_supported(wt, in.K, ln)) return hipErrorInvalidValue;
     if (epi == EPI_RESID && in.stats_out && in.N % kStatTile != 0) return hipErrorInvalidValue;
     const int S = bgemm_splits(wt, in.N, in.K, ln);
-    const dim3 g((in.N + kBgemmFeat - 1) / kBgemmFeat, S);
+    // 64 features per workgroup for a LayerNorm-fused linear whose 32-feature grid
+    // would not be resident at once (three workgroups per CU): fewer, larger groups
+    // beat a second round.
+    static const int n_cu = [] {
+        int dev = 0, n = 0;
+        if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        return n;
+    }();
+    const long tiles32 = (in.N + kBgemmFeat - 1) / kBgemmFeat;
+    const int ft = ln && wt != FTTS_W4A16 && epi != EPI_RESID && S <= 8 && tiles32 * S > 3L * n_cu ? 2 : 1;
+    const dim3 g((in.N + kBgemmFeat * ft - 1) / (kBgemmFeat * ft), S);
     for (int b0 = 0; b0 < in.B; b0 += kBgemmRows) {
         BgemmArgs a = in;
         a.B = in.B - b0 < kBgemmRows ? in.B - b0 : kBgemmRows;
@@ -548,9 +582,9 @@ hipError_t launch_bgemm(int wdtype, int epi, const BgemmArgs& in, hipStream_t st
         }
         hipError_t e;
         switch (wt) {
-            case FTTS_BF16: e = ln ? bgemm_by_epi<FTTS_BF16, true>(epi, a, g, st) : bgemm_by_epi<FTTS_BF16, false>(epi, a, g, st); break;
-            case FTTS_W8A16: e = ln ? bgemm_by_epi<FTTS_W8A16, true>(epi, a, g, st) : bgemm_by_epi<FTTS_W8A16, false>(epi, a, g, st); break;
-            case FTTS_W4A16: e = ln ? bgemm_by_epi<FTTS_W4A16, true>(epi, a, g, st) : bgemm_by_epi<FTTS_W4A16, false>(epi, a, g, st); break;
+            case FTTS_BF16: e = ln ? bgemm_by_epi<FTTS_BF16, true>(epi, ft, a, g, st) : bgemm_by_epi<FTTS_BF16, false>(epi, ft, a, g, st); break;
+            case FTTS_W8A16: e = ln ? bgemm_by_epi<FTTS_W8A16, true>(epi, ft, a, g, st) : bgemm_by_epi<FTTS_W8A16, false>(epi, ft, a, g, st); break;
+            case FTTS_W4A16: e = ln ? bgemm_by_epi<FTTS_W4A16, true>(epi, ft, a, g, st) : bgemm_by_epi<FTTS_W4A16, false>(epi, ft, a, g, st); break;
             default: return hipErrorInvalidValue;
         }
         if (e != hipSuccess) return e;
