@@ -5,11 +5,11 @@
 // and is bound by HBM, but the per-row dot products of the GEMV family would
 // re-stage all activations in every workgroup and run 8-32 FMAs per weight on
 // the VALU.  Here each wave computes a 32 (sequences) x 32 (features) tile with
-// v_mfma_f32_32x32x16_bf16 over a range of K: its weight rows come in through
-// coalesced direct-to-LDS loads (whole row runs per instruction; an operand read
-// in MFMA layout touches 32 rows, which as a global load would cost the address
-// units far more than the bytes), the bf16 activations (a few tens of KB,
-// L2-resident) straight into registers.
+// v_mfma_f32_32x32x16_bf16 over a range of K: its weight rows and its input rows
+// (bf16 activations, or the fp32 residual stream when a LayerNorm is fused) come
+// in through coalesced direct-to-LDS loads (whole row runs per instruction; an
+// operand read in MFMA layout touches 32 rows, which as a global load would cost
+// the address units far more than the bytes) and are read back in MFMA layout.
 //
 // Work split: a workgroup (4 waves) owns 32 features and one of S slices of K;
 // each wave takes a run of consecutive 32-column chunks (128 for W4A16, one
@@ -80,12 +80,8 @@ __device__ __forceinline__ void load_chunk(const BgemmArgs& p, int n, int m, int
     // Every load is unconditional (rows past the batch read the last row and are
     // zeroed afterwards), so the loads of all chunks stay in flight together.
     const int mr = min(m, p.B - 1);
-    if constexpr (!LN) {
-        // bf16 row m: 8 x 16 bytes for W4A16, 2 otherwise
-        const uint4* ar = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.act) + (size_t)mr * p.K + ka);
-#pragma unroll
-        for (int i = 0; i < (int)(sizeof(ch.a) / 16); ++i) ch.a[i] = ar[i];
-    }
+    (void)mr;
+    (void)ka;
     if constexpr (WT == FTTS_W4A16) {
         ch.s = bf16_to_f32(p.scale[(size_t)nn * (p.K / 128) + c]);
         ch.z = bf16_to_f32(p.zero[(size_t)nn * (p.K / 128) + c]);
@@ -162,6 +158,38 @@ __device__ __forceinline__ void stage_x(const BgemmArgs& p, int cw0, int c1, cha
     }
 }
 
+// A 16-bit input is staged the same way: this wave's 32 bf16 rows over its CPW
+// chunks, RBA bytes a row.
+template <int WT> struct AStageShape {
+    static constexpr int RBA = ChunksPerWave<WT, false>::value * BChunk<WT>::KC * 2;
+    static constexpr int PIECES = RBA / 16, BYTES = kBgemmRows * RBA, OPS = BYTES / 1024;
+    static_assert(BYTES % 1024 == 0 && (PIECES & (PIECES - 1)) == 0, "input staging shape");
+};
+
+template <int WT>
+__device__ __forceinline__ void stage_act(const BgemmArgs& p, int cw0, int c1, char* dst) {
+    using SH = AStageShape<WT>;
+    constexpr int KC = BChunk<WT>::KC;
+    const int lane = threadIdx.x & 63;
+    const uint16_t* act = reinterpret_cast<const uint16_t*>(p.act);
+#pragma unroll
+    for (int i = 0; i < SH::OPS; ++i) {
+        const int off = i * 1024 + lane * 16, r = off / SH::RBA, q = (off % SH::RBA) / 16;
+        const int pc = q ^ (r & (SH::PIECES - 1));  // columns pc*8 .. +7
+        const int c = min(cw0 + pc * 8 / KC, c1 - 1);
+        const uint16_t* src = act + (size_t)min(r, p.B - 1) * p.K + (size_t)c * KC + (pc * 8) % KC;
+        lds_dma16(reinterpret_cast<const char*>(src), dst + i * 1024);
+    }
+}
+
+// Eight consecutive bf16 inputs of row fr at column kl of this wave's staged run.
+template <int WT>
+__device__ __forceinline__ uint4 read_a8(const char* src, int fr, int kl) {
+    using SH = AStageShape<WT>;
+    const int q = (kl >> 3) ^ (fr & (SH::PIECES - 1));
+    return *reinterpret_cast<const uint4*>(src + fr * SH::RBA + q * 16);
+}
+
 // Four consecutive fp32 inputs of row fr at column kl of this wave's staged run.
 template <int WT>
 __device__ __forceinline__ float4 read_x4(const char* src, int fr, int kl) {
@@ -210,17 +238,18 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
     constexpr int CPW = ChunksPerWave<WT, LN>::value, NT = kBgemmThreads;
     constexpr int MAXS = FT == 1 ? kBgemmMaxSplits : 8;
     static_assert(FT == 1 || (WT != FTTS_W4A16 && EPI != EPI_RESID), "two tiles per wave: 16-bit / int8 only, no stats");
-    static_assert(!LN || XStageShape<WT>::BYTES >= kBgemmRows * FEAT * 4, "wave tile must fit the staged inputs");
     constexpr int SLICE = CPW * kBgemmWaves * C::KC, GBPER = (SLICE + NT - 1) / NT;  // columns of a K slice
-    // the wave tiles are added in LDS: in the staged inputs once those are read
-    __shared__ float s_red[LN ? 1 : kBgemmWaves][LN ? 1 : kBgemmRows * FEAT];
-    __shared__ __attribute__((aligned(1024))) char s_xs[LN ? kBgemmWaves : 1][LN ? XStageShape<WT>::BYTES : 16];
-    __shared__ int s_last;
-    __shared__ __attribute__((aligned(16))) float s_g[LN ? SLICE : 4];
-    __shared__ __attribute__((aligned(16))) float s_b[LN ? SLICE : 4];
-    __shared__ float2 s_gs[LN ? kLnGroups : 1][kBgemmRows];
-    __shared__ float s_mean[kBgemmRows], s_rstd[kBgemmRows];
+    // staged input rows (fp32 for a LayerNorm input, else bf16); once consumed, the
+    // wave's buffer takes its partial tile for the sum over waves
+    constexpr int IN_BYTES = LN ? XStageShape<WT>::BYTES : AStageShape<WT>::BYTES;
+    static_assert(IN_BYTES >= kBgemmRows * FEAT * 4, "wave tile must fit the staged inputs");
+    __shared__ __attribute__((aligned(1024))) char s_xs[kBgemmWaves][IN_BYTES];
+    __shared__ __attribute__((aligned(16))) float s_g[LN ? SLICE : 1];
+    __shared__ __attribute__((aligned(16))) float s_b[LN ? SLICE : 1];
+    __shared__ float2 s_gs[LN ? kLnGroups : 1][LN ? kBgemmRows : 1];
+    __shared__ float s_mean[LN ? kBgemmRows : 1], s_rstd[LN ? kBgemmRows : 1];
     __shared__ __attribute__((aligned(1024))) char s_wt[kBgemmWaves][WStageShape<WT, LN, FT>::BYTES];
+    int& s_last = *reinterpret_cast<int*>(s_wt[0]);  // used only after every product is formed
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int f = blockIdx.x, s = blockIdx.y, S = gridDim.y;
     const int n0 = f * FEAT;
@@ -270,6 +299,7 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
     const int cw0 = c0 + wave * CPW;
     stage_weights<WT, LN, FT>(p, n0, cw0, c1, s_wt[wave]);
     if constexpr (LN) stage_x<WT>(p, cw0, c1, s_xs[wave]);
+    else stage_act<WT>(p, cw0, c1, s_xs[wave]);
     C ch[CPW];
 #pragma unroll
     for (int j = 0; j < CPW; ++j) load_chunk<WT, LN>(p, n0 + fr, fr, h, min(cw0 + j, c1 - 1), ch[j]);
@@ -364,12 +394,15 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
         }
     }
     if constexpr (!LN) {
-        if (fr >= p.B) {
+        // operand a[i] of chunk j: columns j*KC + h*KC/2 + 8i .. +7 of the staged run
+        const bool live = fr < p.B;
 #pragma unroll
-            for (int j = 0; j < CPW; ++j)
+        for (int j = 0; j < CPW; ++j)
 #pragma unroll
-                for (int i = 0; i < (int)(sizeof(ch[j].a) / 16); ++i) ch[j].a[i] = make_uint4(0, 0, 0, 0);
-        }
+            for (int i = 0; i < (int)(sizeof(ch[j].a) / 16); ++i) {
+                const uint4 a = read_a8<WT>(s_xs[wave], fr, j * C::KC + h * (C::KC / 2) + 8 * i);
+                ch[j].a[i] = live ? a : make_uint4(0, 0, 0, 0);
+            }
     }
     // 5. products: tile t covers features n0 + 32 t ..
     bgemm_f32x16 acc[FT];
@@ -402,7 +435,7 @@ __global__ __launch_bounds__(kBgemmThreads) void bgemm_kernel(const BgemmArgs p)
         }
     }
     // acc[t][i] holds (sequence m, feature n0 + 32 t + fr): m = (i / 4) * 8 + h * 4 + i % 4
-    auto red = [&](int w) { return LN ? reinterpret_cast<float*>(s_xs[w]) : s_red[LN ? 0 : w]; };
+    auto red = [&](int w) { return reinterpret_cast<float*>(s_xs[w]); };
     {
         float* r = red(wave);
 #pragma unroll
