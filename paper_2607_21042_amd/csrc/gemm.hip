@@ -49,14 +49,11 @@ __device__ __forceinline__ RowSlot row_slot(const GemmArgs& a, int m) {
     return RowSlot{phys, t % kPage};
 }
 
-// Epilogue of one output element (rs: the row's KV destination, EPI_QKV only).
+// Store of one biased output element for the non-residual epilogues (rs: the
+// row's KV destination, EPI_QKV only).
 template <bool F32, int EPI>
-__device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, int m, int n, float v, RowSlot rs) {
-    v += ld_act<F32>(a.bias, n);
-    if constexpr (EPI == EPI_RESID) {
-        float* o = reinterpret_cast<float*>(a.out) + (size_t)m * a.N + n;
-        *o += v;
-    } else if constexpr (EPI == EPI_GELU) {
+__device__ __forceinline__ void gemm_store(const GemmArgs& a, int m, int n, float v, RowSlot rs) {
+    if constexpr (EPI == EPI_GELU) {
         st_act<F32>(a.out, (size_t)m * a.N + n, gelu_tanh(v));
     } else {
         st_act<F32>(a.out, (size_t)m * a.N + n, v);
@@ -70,6 +67,18 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, int m, int n, f
                 st_act<F32>(a.kv.base, off, v);
             }
         }
+    }
+}
+
+// Epilogue of one output element.
+template <bool F32, int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, int m, int n, float v, RowSlot rs) {
+    v += ld_act<F32>(a.bias, n);
+    if constexpr (EPI == EPI_RESID) {
+        float* o = reinterpret_cast<float*>(a.out) + (size_t)m * a.N + n;
+        *o += v;
+    } else {
+        gemm_store<F32, EPI>(a, m, n, v, rs);
     }
 }
 
@@ -361,6 +370,264 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmArgs a) {
         }
 }
 
+// Large 16-bit prefill GEMMs (bf16 weights, enough 256 x 256 tiles to fill the
+// chip): a 512-thread block computes a 256 x 256 tile as a 2 x 4 grid of waves,
+// each wave 4 x 2 accumulators of 32x32, over 32-column K steps.  Both operand
+// tiles come in through 1 KB direct-to-LDS loads (16 rows of 64 bytes per
+// instruction, 16-byte pieces XOR-swizzled by row / 4 so that an MFMA operand
+// read touches every bank once) into a ring of four stages, three steps ahead of
+// the products: a step waits for its own stage's loads (the two later steps'
+// stay in flight), passes one barrier, reads the operands of its first 16
+// columns, issues the reads of the second 16 and the refill of the stage the
+// previous step used, and runs the first 8 matrix instructions while those reads
+// return, then the other 8.  The
+// stages are separate LDS objects and the loop is unrolled over them, so the
+// compiler sees that a read of one stage does not wait for loads into another.
+// Twice the tile edge of the 128 x 128 kernel halves the operand bytes per
+// product.  Tiles are ordered for the per-XCD L2s: workgroups are spread over the
+// 8 XCDs round-robin, so block b takes tile t from the contiguous run of tiles
+// given to XCD b % 8, and consecutive tiles form groups of 4 row blocks that
+// walk the columns -- the 32 tiles an XCD runs at once share 4 row blocks of the
+// activations and about 8 column blocks of the weights.  (The mapping is a
+// bijection whatever the placement; only the cache reuse depends on it.)
+constexpr int GB = 256, GBKB = 32, GSTAGE = GB * GBKB * 2;  // tile edge, K step, bytes per operand stage
+__shared__ __attribute__((aligned(1024))) char g_sa0[GSTAGE], g_sa1[GSTAGE], g_sa2[GSTAGE], g_sa3[GSTAGE];
+__shared__ __attribute__((aligned(1024))) char g_sb0[GSTAGE], g_sb1[GSTAGE], g_sb2[GSTAGE], g_sb3[GSTAGE];
+template <int S> __device__ __forceinline__ char* big_a() {
+    return S == 0 ? g_sa0 : S == 1 ? g_sa1 : S == 2 ? g_sa2 : g_sa3;
+}
+template <int S> __device__ __forceinline__ char* big_b() {
+    return S == 0 ? g_sb0 : S == 1 ? g_sb1 : S == 2 ? g_sb2 : g_sb3;
+}
+
+typedef __attribute__((address_space(3))) char gemm_lds_char;
+// Wave w's 16 KB epilogue buffer: one of the eight operand stages.
+__device__ __forceinline__ char* big_epi_buf(int w) {
+    switch (w) {
+        case 0: return g_sa0; case 1: return g_sa1; case 2: return g_sa2; case 3: return g_sa3;
+        case 4: return g_sb0; case 5: return g_sb1; case 6: return g_sb2; default: return g_sb3;
+    }
+}
+
+// The tanh GELU written as u * sigmoid(2 c (u + 0.044715 u^3)) -- the same
+// function, since 0.5 (1 + tanh z) = 1 / (1 + exp(-2 z)) -- on one exponential.
+__device__ __forceinline__ float gelu_sigmoid_form(float u) {
+    const float c2 = 2.0f * 0.7978845608028654f;
+    return u / (1.0f + __expf(-c2 * (u + 0.044715f * u * u * u)));
+}
+__device__ __forceinline__ void gemm_dma16(const void* src, char* dst) {
+    __builtin_amdgcn_global_load_lds(src, (gemm_lds_char*)dst, 16, 0, 0);
+}
+
+// This wave's share (2 of 16 instructions) of one 256 x 32 bf16 operand tile:
+// rows r0 .. r0 + 255 (clamped to rows - 1), columns k0 .. k0 + 31.
+__device__ __forceinline__ int big_slot(int row, int piece) { return piece ^ ((row >> 2) & 3); }
+__device__ __forceinline__ void big_stage(const uint16_t* X, int rows, int K, int r0, int k0, char* dst) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int o = wave * 2 + i, r = o * 16 + (lane >> 2), pc = big_slot(r, lane & 3);
+        gemm_dma16(X + (size_t)min(r0 + r, rows - 1) * K + k0 + pc * 8, dst + o * 1024);
+    }
+}
+
+// Operand reads are issued as ds_read_b128 in inline assembly and waited for by
+// big_wait: the compiler cannot tell which stage a direct-to-LDS load writes, and
+// would otherwise wait for every load in flight before the first read of a step.
+__device__ __forceinline__ bf16x8_t big_read(const char* tile, int row, int piece) {
+    const uint32_t addr = (uint32_t)(uintptr_t)(gemm_lds_char*)(tile + row * 64 + (big_slot(row, piece) << 4));
+    bf16x8_t r;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr) : "memory");
+    return r;
+}
+
+struct BigCtx {
+    const uint16_t *A, *W;
+    int M, N, K, m0, n0, wm, wn, fr, fh, nk;
+};
+
+// One K step on stage S: kt is the step, loads for step kt + 3 go to stage (S + 3) % 4.
+template <int S>
+__device__ __forceinline__ void big_step(const BigCtx& c, int kt, f32x16_t (&acc)[4][2]) {
+    // this step's loads are the oldest in flight: 4 per later step may remain
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + 2 < c.nk) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else if (kt + 1 < c.nk) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // A bare barrier: every wave's share of this stage has landed (the waits above)
+    // and every wave has consumed its reads of the stage refilled below (the
+    // products of the previous step, which used them, precede it).  A fenced
+    // __syncthreads would also wait for the later stages' loads.
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    // K half 0's operands, then (in flight under half 0's products) half 1's
+    bf16x8_t av[4][2], bv[2][2];  // [tile][k step of 16]
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) av[mt][0] = big_read(big_a<S>(), c.wm * 128 + mt * 32 + c.fr, c.fh);
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) bv[nt][0] = big_read(big_b<S>(), c.wn * 64 + nt * 32 + c.fr, c.fh);
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(av[0][0]), "+v"(av[1][0]), "+v"(av[2][0]), "+v"(av[3][0]), "+v"(bv[0][0]), "+v"(bv[1][0])
+                 :
+                 : "memory");
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) av[mt][1] = big_read(big_a<S>(), c.wm * 128 + mt * 32 + c.fr, 2 + c.fh);
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) bv[nt][1] = big_read(big_b<S>(), c.wn * 64 + nt * 32 + c.fr, 2 + c.fh);
+    if (kt + 3 < c.nk) {  // stage (S + 3) % 4 was last read by step kt - 1, before this step's barrier
+        big_stage(c.A, c.M, c.K, c.m0, (kt + 3) * GBKB, big_a<(S + 3) % 4>());
+        big_stage(c.W, c.N, c.K, c.n0, (kt + 3) * GBKB, big_b<(S + 3) % 4>());
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[mt][0], bv[nt][0], acc[mt][nt], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(av[0][1]), "+v"(av[1][1]), "+v"(av[2][1]), "+v"(av[3][1]), "+v"(bv[0][1]), "+v"(bv[1][1])
+                 :
+                 : "memory");
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[mt][1], bv[nt][1], acc[mt][nt], 0, 0, 0);
+}
+
+template <int EPI>
+__global__ __launch_bounds__(512) void gemm_big_kernel(const GemmArgs a) {
+    __shared__ RowSlot s_rows[EPI == EPI_QKV ? GB : 1];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    BigCtx c;
+    c.A = reinterpret_cast<const uint16_t*>(a.a);
+    c.W = reinterpret_cast<const uint16_t*>(a.w);
+    c.M = a.M, c.N = a.N, c.K = a.K;
+    {
+        const int tn = (a.N + GB - 1) / GB, tm = (a.M + GB - 1) / GB, T = tm * tn;
+        const int b = blockIdx.x, x = b & 7, l = b >> 3, q = T >> 3, r = T & 7;
+        const int t = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + l;
+        constexpr int GM = 4;  // row blocks per group
+        const int g = t / (GM * tn), gm = min(GM, tm - g * GM), w = t - g * GM * tn;
+        c.m0 = (g * GM + w % gm) * GB;
+        c.n0 = (w / gm) * GB;
+    }
+    c.wm = wave >> 2, c.wn = wave & 3;  // rows wm*128 .., columns wn*64 ..
+    c.fr = lane & 31, c.fh = lane >> 5;
+    c.nk = a.K / GBKB;
+    const int m0 = c.m0, n0 = c.n0, wm = c.wm, wn = c.wn, fr = c.fr, fh = c.fh;
+    if constexpr (EPI == EPI_QKV) {
+        if (tid < GB) s_rows[tid] = row_slot(a, min(m0 + tid, a.M - 1));  // read after the first barrier
+    }
+    f32x16_t acc[4][2];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[mt][nt][i] = 0.f;
+    // prologue: steps 0, 1, 2 into stages 0, 1, 2
+    big_stage(c.A, c.M, c.K, m0, 0, g_sa0);
+    big_stage(c.W, c.N, c.K, n0, 0, g_sb0);
+    if (c.nk > 1) {
+        big_stage(c.A, c.M, c.K, m0, GBKB, g_sa1);
+        big_stage(c.W, c.N, c.K, n0, GBKB, g_sb1);
+    }
+    if (c.nk > 2) {
+        big_stage(c.A, c.M, c.K, m0, 2 * GBKB, g_sa2);
+        big_stage(c.W, c.N, c.K, n0, 2 * GBKB, g_sb2);
+    }
+    for (int kt = 0; kt < c.nk; kt += 4) {
+        big_step<0>(c, kt, acc);
+        if (kt + 1 < c.nk) big_step<1>(c, kt + 1, acc);
+        if (kt + 2 < c.nk) big_step<2>(c, kt + 2, acc);
+        if (kt + 3 < c.nk) big_step<3>(c, kt + 3, acc);
+    }
+    __syncthreads();  // s_rows written before the loop is read below
+    // Epilogue through LDS (the operand stages are free now: one 16 KB stage per
+    // wave): each wave writes its biased (and activated) 128 x 64 sub-tile in
+    // row-major order, then reads it back as 16-byte row pieces for coalesced
+    // stores -- the output rows, the new keys and values into their KV pages, or
+    // for the residual update x += y in two 64-row halves, all old values of a
+    // half loaded before its stores.  Pieces are XOR-swizzled by row so that the
+    // column-wise writes of the MFMA layout do not collide in banks.
+    char* eb = big_epi_buf(wave);
+    float bias[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) bias[nt] = ld_act<false>(a.bias, min(n0 + wn * 64 + nt * 32 + fr, a.N - 1));
+    const int rw0 = m0 + wm * 128, cw0 = n0 + wn * 64;  // this wave's first row and column
+    if constexpr (EPI != EPI_RESID) {
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int rl = mt * 32 + (i >> 2) * 8 + fh * 4 + (i & 3), cl = nt * 32 + fr;
+                    float y = acc[mt][nt][i] + bias[nt];
+                    if constexpr (EPI == EPI_GELU) y = gelu_sigmoid_form(y);
+                    *reinterpret_cast<uint16_t*>(eb + rl * 128 + (((cl >> 3) ^ (rl & 7)) << 4) + (cl & 7) * 2) =
+                        f32_to_bf16(y);
+                }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        uint16_t* out = reinterpret_cast<uint16_t*>(a.out);
+#pragma unroll
+        for (int it = 0; it < 16; ++it) {
+            const int j = lane + 64 * it, rl = j >> 3, q = j & 7;
+            const uint4 v = *reinterpret_cast<const uint4*>(eb + rl * 128 + ((q ^ (rl & 7)) << 4));
+            const int m = rw0 + rl, n = cw0 + q * 8;
+            if (m < a.M && n < a.N) {
+                *reinterpret_cast<uint4*>(out + (size_t)m * a.N + n) = v;
+                if constexpr (EPI == EPI_QKV) {
+                    const int d = a.kv.d_model;
+                    const RowSlot rs = s_rows[wm * 128 + rl];
+                    if (n >= d && rs.phys >= 0) {
+                        const int kvsel = n >= 2 * d, r = n - d - kvsel * d;
+                        const size_t off = kv_offset(a.kv.layer, a.kv.n_pages, rs.phys, kvsel, a.kv.n_head,
+                                                     r / kHeadDim, rs.slot) + (r % kHeadDim);
+                        *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.kv.base) + off) = v;
+                    }
+                }
+            }
+        }
+    } else {
+        float* x = reinterpret_cast<float*>(a.out);
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+#pragma unroll
+            for (int mh = 0; mh < 2; ++mh)
+#pragma unroll
+                for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const int rl = mh * 32 + (i >> 2) * 8 + fh * 4 + (i & 3), cl = nt * 32 + fr;
+                        const int slot = (cl >> 2) ^ (((rl >> 2) & 1) << 3);
+                        *reinterpret_cast<float*>(eb + rl * 256 + slot * 16 + (cl & 3) * 4) =
+                            acc[half * 2 + mh][nt][i] + bias[nt];
+                    }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            float4 y[16], old[16];
+#pragma unroll
+            for (int it = 0; it < 16; ++it) {
+                const int j = lane + 64 * it, rl = j >> 4, q = j & 15;
+                y[it] = *reinterpret_cast<const float4*>(eb + rl * 256 + ((q ^ (((rl >> 2) & 1) << 3)) << 4));
+                const int m = min(rw0 + half * 64 + rl, a.M - 1), n = min(cw0 + q * 4, a.N - 4);
+                old[it] = *reinterpret_cast<const float4*>(x + (size_t)m * a.N + n);
+            }
+#pragma unroll
+            for (int it = 0; it < 16; ++it) {
+                const int j = lane + 64 * it, rl = j >> 4, q = j & 15;
+                const int m = rw0 + half * 64 + rl, n = cw0 + q * 4;
+                if (m < a.M && n < a.N)
+                    *reinterpret_cast<float4*>(x + (size_t)m * a.N + n) =
+                        make_float4(old[it].x + y[it].x, old[it].y + y[it].y, old[it].z + y[it].z, old[it].w + y[it].w);
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this half's reads done before the next half's writes
+        }
+    }
+}
+
 template <int WT, int MT>
 static hipError_t mfma_by_epi(int epi, const GemmArgs& a, dim3 g, hipStream_t st) {
     switch (epi) {
@@ -407,6 +674,19 @@ hipError_t launch_gemm(int wdtype, int epi, const GemmArgs& a, hipStream_t st) {
         return hipGetLastError();
     }
     if (!gemm_mfma_supported(a.K)) return hipErrorInvalidValue;
+    // bf16 weights with at least 128 tiles of 256 x 256: the large-tile kernel
+    const long big_tiles = (long)((a.M + GB - 1) / GB) * ((a.N + GB - 1) / GB);
+    if (wdtype == FTTS_BF16 && big_tiles >= 128 && a.N % 8 == 0) {
+        const dim3 g((unsigned)big_tiles);
+        switch (epi) {
+            case EPI_STORE: hipLaunchKernelGGL(gemm_big_kernel<EPI_STORE>, g, dim3(512), 0, st, a); break;
+            case EPI_QKV: hipLaunchKernelGGL(gemm_big_kernel<EPI_QKV>, g, dim3(512), 0, st, a); break;
+            case EPI_GELU: hipLaunchKernelGGL(gemm_big_kernel<EPI_GELU>, g, dim3(512), 0, st, a); break;
+            case EPI_RESID: hipLaunchKernelGGL(gemm_big_kernel<EPI_RESID>, g, dim3(512), 0, st, a); break;
+            default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    }
     const GemmPlan p = gemm_plan(a.M, a.N, a.K);
     if (p.splits > 1 && (!a.part || !a.count)) return hipErrorInvalidValue;
     const dim3 g(p.tiles_n, p.tiles_m, p.splits);

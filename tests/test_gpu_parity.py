@@ -504,6 +504,29 @@ def mid_master():
     return workload.master_weights(MID, seed=0)
 
 
+def test_prefill_large_tiles(torch_cuda, mid_master):
+    """A prefill of 20 ragged prefixes (6,713 rows) at d=1280 puts every linear on
+    the 256 x 256-tile kernel (at least 128 tiles each, ragged last row tile):
+    the prefill logits and two batched decode steps over the cache it wrote
+    match the oracle."""
+    from paper_2607_21042_amd import ftts
+    mode = "bf16"
+    inputs = model_inputs(MID, mode, mid_master)
+    lens = [int(x) for x in np.random.default_rng(21).integers(200, 460, size=20)]
+    lens[-1] += 6713 - sum(lens)
+    assert sum(lens) == 6713 and min(lens) > 0
+    flat = workload.prefix_embeddings(lens, MID.d_model, seed=5, bf16=True)
+    prefixes = np.split(flat, np.cumsum(lens)[:-1])
+    fed = workload.random_tokens(2, len(lens), MID.vocab, seed=6)
+    fed[0, :] = MID.start_token
+    om = ogpt.GPT(helpers.oracle_weights(inputs, mode), MID.n_head, MID.d_head, dtype=np.float32)
+    say("prefill large tiles")
+    dm = ftts.DeviceModel(inputs, MID, wd(mode))
+    res = helpers.run_gpu(dm, MID, prefixes, fed)
+    worst, _ = compare_run(res, om, prefixes, fed, mode, check_sampled=False)
+    say(f"  worst err {worst:.3g}")
+
+
 @pytest.mark.parametrize("mode,B", [("bf16", 33), ("w8a16", 9), ("w4a16", 33)])
 def test_batched_decode_model_width(torch_cuda, mid_master, mode, B):
     """The batched linears at d=1280 / FFN 5120 (several K slices per feature tile
