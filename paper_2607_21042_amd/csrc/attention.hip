@@ -5,11 +5,14 @@
 // One workgroup per (head, sequence) whose 8 waves stride over the logical
 // pages (split-K inside the workgroup).  A 64x64 K or V page is read as 8 fully
 // coalesced 1 KB wave loads, lane l holding dims (l%8)*8 .. +7 of tokens
-// i*8 + l/8; the next page's K and V are loaded while the current one is used.
+// i*8 + l/8 (with 16-bit pages the next page's K and V would be loaded while
+// the current one is used; only the fp32 instantiation is launched).
 // Scores are reduced over the 8 lanes of a token, each page's softmax is
 // folded into a running (max, sum, output) triple, and the 8 wave partials
 // are merged in LDS with the log-sum-exp rule.  The walk follows logical
-// pages, so the result does not depend on where pages live in the pool.
+// pages, so the result does not depend on where pages live in the pool.  This
+// is the fp32-KV kernel; the 16-bit KV kernel (attn_decode_bf16_kernel, below)
+// keeps one page per wave in registers so that two groups share a CU.
 //
 // Prefill (causal attention over each prefix).  16-bit activations run on the
 // matrix cores: a workgroup of 4 waves takes 128 queries of one head, each wave

@@ -11,19 +11,21 @@
 // operand read in MFMA layout touches 32 rows, which as a global load would cost
 // the address units far more than the bytes) and are read back in MFMA layout.
 //
-// Work split: a workgroup (4 waves) owns 32 features and one of S slices of K;
-// each wave takes a run of consecutive 32-column chunks (128 for W4A16, one
-// quantisation group) of the slice, issues every load of its share at once (S is
-// chosen so that a share fits), and the waves add their tiles in LDS.  With S > 1 every workgroup
+// Work split: a workgroup (4 waves) owns 32 features (or 64, two MFMA tiles per
+// wave, when the 32-feature grid of a LayerNorm-fused linear would not be
+// resident at once) and one of S slices of K; each wave takes a run of
+// consecutive 32-column chunks (128 for W4A16, one quantisation group) of the
+// slice, issues every load of its share at once (S is chosen so that a share
+// fits), and the waves add their tiles in LDS.  With S > 1 every workgroup
 // stores its partial tile, and the last of the S to arrive (a per-tile counter)
 // adds the S partials in slice order -- the same order whatever the arrival
 // order, so results are reproducible -- and applies the epilogue; it also
 // resets the counter, which is zero between calls.
 //
 // K order inside a chunk: lane (row, h) feeds the MFMA k-slots h*8..h*8+7 of
-// step st from contiguous memory (bf16: k = h*16 + st*8 + i; W4A16: word h*8+st),
-// and the activation operand uses the same map, so each lane's loads are
-// contiguous and the dot product is unchanged.
+// step st from contiguous columns (bf16: k = h*16 + st*8 + i; W4A16: word
+// h*8+st), and the input operand uses the same map, so the dot product is
+// unchanged.
 #include "ftts_internal.hpp"
 
 namespace ftts {

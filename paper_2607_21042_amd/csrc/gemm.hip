@@ -1,7 +1,8 @@
 // Dense contractions of the prefill: C[M][N] = A[M][K] . W[N][K]^T with fused
 // epilogues (bias, q/k/v store + paged KV scatter, GELU, residual add).
 //
-// 16-bit modes: bf16 MFMA (v_mfma_f32_32x32x16_bf16, gfx950).  A 256-thread
+// 16-bit modes: bf16 MFMA (v_mfma_f32_32x32x16_bf16, gfx950).  Large GEMMs with
+// bf16 weights take gemm_big_kernel (256 x 256 tiles, below).  Otherwise a 256-thread
 // block computes a (64*MT) x 128 tile as a 2x2 grid of waves, each wave MT x 2
 // accumulators of 32x32, over 64-column K steps: 16*MT matrix instructions per
 // wave between barriers, while the next step's tiles of A and W are in flight
