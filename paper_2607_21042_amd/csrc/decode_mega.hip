@@ -138,7 +138,9 @@ __device__ __forceinline__ void dma_rows(const void* W, int row_b, int r0, int n
     lds_char* d = (lds_char*)(dst);
     for (int c0 = 0; c0 < n; c0 += 64) {
         const int c = min(c0 + lane, n - 1);
-        __builtin_amdgcn_global_load_lds(s + (size_t)c * 16, d + c0 * 16, 16, 0, 0);
+        // cache policy 2 = nt: weights are read once per step, and streaming them
+        // non-temporally keeps them from evicting the exchange words being polled
+        __builtin_amdgcn_global_load_lds(s + (size_t)c * 16, d + c0 * 16, 16, 0, 2);
     }
 }
 
