@@ -447,54 +447,68 @@ struct BigCtx {
     int M, N, K, m0, n0, wm, wn, fr, fh, nk;
 };
 
-// One K step on stage S: kt is the step, loads for step kt + 3 go to stage (S + 3) % 4.
+// Operand reads of one K half (16 columns) of a stage, and the wait for them.
 template <int S>
-__device__ __forceinline__ void big_step(const BigCtx& c, int kt, f32x16_t (&acc)[4][2]) {
-    // this step's loads are the oldest in flight: 4 per later step may remain
-    __builtin_amdgcn_sched_barrier(0);
-    if (kt + 2 < c.nk) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else if (kt + 1 < c.nk) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    // A bare barrier: every wave's share of this stage has landed (the waits above)
-    // and every wave has consumed its reads of the stage refilled below (the
-    // products of the previous step, which used them, precede it).  A fenced
-    // __syncthreads would also wait for the later stages' loads.
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-    // K half 0's operands, then (in flight under half 0's products) half 1's
-    bf16x8_t av[4][2], bv[2][2];  // [tile][k step of 16]
+__device__ __forceinline__ void big_read_half(const BigCtx& c, int half, bf16x8_t (&av)[4], bf16x8_t (&bv)[2]) {
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) av[mt][0] = big_read(big_a<S>(), c.wm * 128 + mt * 32 + c.fr, c.fh);
+    for (int mt = 0; mt < 4; ++mt) av[mt] = big_read(big_a<S>(), c.wm * 128 + mt * 32 + c.fr, 2 * half + c.fh);
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) bv[nt][0] = big_read(big_b<S>(), c.wn * 64 + nt * 32 + c.fr, c.fh);
+    for (int nt = 0; nt < 2; ++nt) bv[nt] = big_read(big_b<S>(), c.wn * 64 + nt * 32 + c.fr, 2 * half + c.fh);
+}
+__device__ __forceinline__ void big_wait_half(bf16x8_t (&av)[4], bf16x8_t (&bv)[2]) {
     asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(av[0][0]), "+v"(av[1][0]), "+v"(av[2][0]), "+v"(av[3][0]), "+v"(bv[0][0]), "+v"(bv[1][0])
+                 : "+v"(av[0]), "+v"(av[1]), "+v"(av[2]), "+v"(av[3]), "+v"(bv[0]), "+v"(bv[1])
                  :
                  : "memory");
+}
+__device__ __forceinline__ void big_mfma_half(f32x16_t (&acc)[4][2], const bf16x8_t (&av)[4], const bf16x8_t (&bv)[2]) {
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) av[mt][1] = big_read(big_a<S>(), c.wm * 128 + mt * 32 + c.fr, 2 + c.fh);
+    for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) bv[nt][1] = big_read(big_b<S>(), c.wn * 64 + nt * 32 + c.fr, 2 + c.fh);
-    if (kt + 3 < c.nk) {  // stage (S + 3) % 4 was last read by step kt - 1, before this step's barrier
+        for (int nt = 0; nt < 2; ++nt)
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[mt], bv[nt], acc[mt][nt], 0, 0, 0);
+}
+
+// Stage s's loads have landed in every wave: wait until only the later steps'
+// loads (4 per step, steps up to kt + 3 issued) are in flight, then a bare
+// barrier.  A fenced __syncthreads would also wait for those later loads.
+__device__ __forceinline__ void big_stage_ready(const BigCtx& c, int s) {
+    __builtin_amdgcn_sched_barrier(0);
+    const int later = (s + 1 < c.nk) + (s + 2 < c.nk);  // steps after s whose loads are out
+    if (later == 2) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else if (later == 1) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// One K step on stage S, software-pipelined by halves: on entry (a0, b0) hold
+// step kt's first half, read and waited for.  The second half's reads go out
+// with the refill of the stage step kt - 1 used (loads for step kt + 3), then the
+// first half's products; after the next stage is ready its first half is read
+// into (a0, b0) while the second half's products run.
+template <int S>
+__device__ __forceinline__ void big_step(const BigCtx& c, int kt, f32x16_t (&acc)[4][2], bf16x8_t (&a0)[4],
+                                         bf16x8_t (&b0)[2]) {
+    bf16x8_t a1[4], b1[2];
+    big_read_half<S>(c, 1, a1, b1);
+    if (kt + 3 < c.nk) {  // stage (S + 3) % 4: every wave finished reading it before the last barrier
         big_stage(c.A, c.M, c.K, c.m0, (kt + 3) * GBKB, big_a<(S + 3) % 4>());
         big_stage(c.W, c.N, c.K, c.n0, (kt + 3) * GBKB, big_b<(S + 3) % 4>());
     }
     __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[mt][0], bv[nt][0], acc[mt][nt], 0, 0, 0);
+    big_mfma_half(acc, a0, b0);
     __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(av[0][1]), "+v"(av[1][1]), "+v"(av[2][1]), "+v"(av[3][1]), "+v"(bv[0][1]), "+v"(bv[1][1])
-                 :
-                 : "memory");
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[mt][1], bv[nt][1], acc[mt][nt], 0, 0, 0);
+    big_wait_half(a1, b1);
+    if (kt + 1 < c.nk) {
+        // (the step's reads of stage S are complete, so this barrier also frees it)
+        big_stage_ready(c, kt + 1);
+        big_read_half<(S + 1) % 4>(c, 0, a0, b0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    big_mfma_half(acc, a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + 1 < c.nk) big_wait_half(a0, b0);
 }
 
 template <int EPI>
@@ -539,11 +553,15 @@ __global__ __launch_bounds__(512) void gemm_big_kernel(const GemmArgs a) {
         big_stage(c.A, c.M, c.K, m0, 2 * GBKB, g_sa2);
         big_stage(c.W, c.N, c.K, n0, 2 * GBKB, g_sb2);
     }
+    bf16x8_t a0[4], b0[2];
+    big_stage_ready(c, 0);
+    big_read_half<0>(c, 0, a0, b0);
+    big_wait_half(a0, b0);
     for (int kt = 0; kt < c.nk; kt += 4) {
-        big_step<0>(c, kt, acc);
-        if (kt + 1 < c.nk) big_step<1>(c, kt + 1, acc);
-        if (kt + 2 < c.nk) big_step<2>(c, kt + 2, acc);
-        if (kt + 3 < c.nk) big_step<3>(c, kt + 3, acc);
+        big_step<0>(c, kt, acc, a0, b0);
+        if (kt + 1 < c.nk) big_step<1>(c, kt + 1, acc, a0, b0);
+        if (kt + 2 < c.nk) big_step<2>(c, kt + 2, acc, a0, b0);
+        if (kt + 3 < c.nk) big_step<3>(c, kt + 3, acc, a0, b0);
     }
     __syncthreads();  // s_rows written before the loop is read below
     // Epilogue through LDS (the operand stages are free now: one 16 KB stage per
