@@ -411,10 +411,19 @@ __device__ __forceinline__ char* big_epi_buf(int w) {
 }
 
 // The tanh GELU written as u * sigmoid(2 c (u + 0.044715 u^3)) -- the same
-// function, since 0.5 (1 + tanh z) = 1 / (1 + exp(-2 z)) -- on one exponential.
+// function, since 0.5 (1 + tanh z) = 1 / (1 + exp(-2 z)) -- on one exponential
+// and one hardware reciprocal (the result is rounded to bf16).
 __device__ __forceinline__ float gelu_sigmoid_form(float u) {
     const float c2 = 2.0f * 0.7978845608028654f;
-    return u / (1.0f + __expf(-c2 * (u + 0.044715f * u * u * u)));
+    return u * __builtin_amdgcn_rcpf(1.0f + __expf(-c2 * (u + 0.044715f * u * u * u)));
+}
+
+// Two fp32 values to packed bf16 (round to nearest even) in one gfx950 instruction.
+__device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
+    typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+    typedef float f32x2_v __attribute__((ext_vector_type(2)));
+    const f32x2_v v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_v));
 }
 __device__ __forceinline__ void gemm_dma16(const void* src, char* dst) {
     __builtin_amdgcn_global_load_lds(src, (gemm_lds_char*)dst, 16, 0, 0);
@@ -582,12 +591,16 @@ __global__ __launch_bounds__(512) void gemm_big_kernel(const GemmArgs a) {
 #pragma unroll
             for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int rl = mt * 32 + (i >> 2) * 8 + fh * 4 + (i & 3), cl = nt * 32 + fr;
-                    float y = acc[mt][nt][i] + bias[nt];
-                    if constexpr (EPI == EPI_GELU) y = gelu_sigmoid_form(y);
-                    *reinterpret_cast<uint16_t*>(eb + rl * 128 + (((cl >> 3) ^ (rl & 7)) << 4) + (cl & 7) * 2) =
-                        f32_to_bf16(y);
+                for (int i = 0; i < 16; i += 2) {
+                    float2 y = make_float2(acc[mt][nt][i] + bias[nt], acc[mt][nt][i + 1] + bias[nt]);
+                    if constexpr (EPI == EPI_GELU) y = make_float2(gelu_sigmoid_form(y.x), gelu_sigmoid_form(y.y));
+                    const uint32_t pk = bf16x2_rne(y.x, y.y);  // rows i and i + 1 of the same column
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const int rl = mt * 32 + ((i + e) >> 2) * 8 + fh * 4 + ((i + e) & 3), cl = nt * 32 + fr;
+                        *reinterpret_cast<uint16_t*>(eb + rl * 128 + (((cl >> 3) ^ (rl & 7)) << 4) + (cl & 7) * 2) =
+                            (uint16_t)(pk >> (16 * e));
+                    }
                 }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         uint16_t* out = reinterpret_cast<uint16_t*>(a.out);
