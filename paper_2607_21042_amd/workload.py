@@ -221,3 +221,71 @@ def quantisable_weights(master: dict, threads: int = 8) -> dict:
         for k in LINEAR_KEYS:
             lw_out[k] = lw[k]
     return out
+
+
+# ---- Semantic-to-Mel flow-matching DiT (synthetic shape) ---------------------------------
+@dataclass(frozen=True)
+class DitShape:
+    n_layer: int
+    d_model: int
+    n_head: int
+    d_head: int
+    d_ff: int
+    n_mel: int      # mel bins of the state being integrated
+    d_cond: int     # width of the per-frame conditioning rows (GPT hidden states)
+    t_dim: int = 256  # sinusoidal timestep features
+
+    def matrices(self):
+        d, f = self.d_model, self.d_ff
+        return [("qkv", 3 * d, d), ("out", d, d), ("fc1", f, d), ("fc2", d, f)]
+
+    def n_params(self) -> int:
+        d = self.d_model
+        per_layer = sum(N * K + N for _, N, K in self.matrices()) + 4 * d
+        return (d * (self.n_mel + self.d_cond) + d + d * self.t_dim + d + d * d + d
+                + self.n_layer * per_layer + 2 * d + self.n_mel * d + self.n_mel)
+
+
+# Tiny DiT for parity: 2 blocks of width 256.  The 96M-parameter shape: 13 pre-LN
+# blocks of width 768 (12 heads of 64, FFN 3072), 128 mel bins, conditioned on the
+# GPT's 1280-wide hidden states.
+DIT_TINY = DitShape(n_layer=2, d_model=256, n_head=4, d_head=64, d_ff=1024, n_mel=128, d_cond=256)
+DIT_96M = DitShape(n_layer=13, d_model=768, n_head=12, d_head=64, d_ff=3072, n_mel=128, d_cond=1280)
+
+
+def dit_master_weights(shape: DitShape, seed: int = 20) -> dict:
+    """fp32 DiT weights ~N(0, 0.02) (LayerNorm gains 1 + N(0, 0.02)), one stream per tensor.
+
+    ``{"w_in" [d][n_mel + d_cond], "b_in", "w_t1" [d][t_dim], "b_t1", "w_t2" [d][d], "b_t2",
+    "layers": [ {ln1_g, ln1_b, w_qkv, b_qkv, w_out, b_out, ln2_g, ln2_b, w_fc1, b_fc1, w_fc2,
+    b_fc2} ], "lnf_g", "lnf_b", "w_out_mel" [n_mel][d], "b_out_mel"}``.
+    """
+    d = shape.d_model
+    specs = [("w_in", None, (d, shape.n_mel + shape.d_cond), 0.0), ("b_in", None, (d,), 0.0),
+             ("w_t1", None, (d, shape.t_dim), 0.0), ("b_t1", None, (d,), 0.0),
+             ("w_t2", None, (d, d), 0.0), ("b_t2", None, (d,), 0.0)]
+    for l in range(shape.n_layer):
+        specs += [("ln1_g", l, (d,), 1.0), ("ln1_b", l, (d,), 0.0)]
+        for name, N, K in shape.matrices():
+            if name == "fc1":
+                specs += [("ln2_g", l, (d,), 1.0), ("ln2_b", l, (d,), 0.0)]
+            specs += [("w_" + name, l, (N, K), 0.0), ("b_" + name, l, (N,), 0.0)]
+    specs += [("lnf_g", None, (d,), 1.0), ("lnf_b", None, (d,), 0.0),
+              ("w_out_mel", None, (shape.n_mel, d), 0.0), ("b_out_mel", None, (shape.n_mel,), 0.0)]
+    out: dict = {"layers": [dict() for _ in range(shape.n_layer)]}
+    for i, (key, layer, shp, mean) in enumerate(specs):
+        a = _normal(seed, i, shp, INIT_STD, mean)
+        if layer is None:
+            out[key] = a
+        else:
+            out["layers"][layer][key] = a
+    return out
+
+
+def dit_inputs(shape: DitShape, T: int, seed: int = 21):
+    """The state x [T][n_mel] ~N(0, 1) (fp32) and conditioning rows cond [T][d_cond] ~N(0, 1)
+    rounded to bf16 (the GPU takes them as bf16)."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((T, shape.n_mel), dtype=np.float32)
+    cond = bf16_round(rng.standard_normal((T, shape.d_cond), dtype=np.float32))
+    return x, cond
