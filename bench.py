@@ -57,6 +57,11 @@ def parse():
                    help="continuous batching instead: --requests utterances (default 64) with the --paged length "
                         "mix through --batch decode slots (default 32), chunks of 16 steps, top-k 30 sampling")
     p.add_argument("--requests", type=int, default=64)
+    p.add_argument("--dit", action="store_true",
+                   help="flow-matching DiT (96M shape): guided Euler steps over --frames mel frames")
+    p.add_argument("--frames", type=int, default=500)
+    p.add_argument("--euler", type=int, default=25, help="Euler steps per DiT job")
+    p.add_argument("--graph", action="store_true", help="DiT: replay each job's steps from one HIP graph")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain device copy of known size (scales the rocprofv3 byte counters)")
     return p.parse_args()
@@ -329,6 +334,100 @@ def serve_run(args, torch, ftts, workload, shape, dm, mode):
     }
 
 
+def dit_flops(shape, T):
+    """Algorithmic flops of one guided Euler step over T frames (both branches):
+    2 M N K per linear at M = 2T rows, 4 T^2 d per block and branch for the
+    attention (Q K^T and P V), and the M-independent time MLP."""
+    M, d = 2 * T, shape.d_model
+    lin = sum(N * K for _, N, K in shape.matrices()) * shape.n_layer + d * (shape.n_mel + shape.d_cond) \
+        + shape.n_mel * d
+    return 2.0 * M * lin + shape.n_layer * 2 * 4.0 * T * T * d + 2.0 * (d * shape.t_dim + d * d)
+
+
+def dit_run(args, torch, ftts, workload):
+    """One job = --euler guided Euler steps of the 96M DiT over --frames frames
+    (t from 0 to 1 in equal steps), state and conditioning resident in HBM."""
+    shape = workload.DIT_96M
+    T, K = args.frames, args.euler
+    w = workload.bf16_weights(workload.dit_master_weights(shape, seed=20))
+    dm = ftts.DitDeviceModel(w, shape)
+    x0_np, cond_np = workload.dit_inputs(shape, T, seed=21)
+    x0 = torch.from_numpy(x0_np).cuda()
+    x = torch.empty_like(x0)
+    cond = torch.from_numpy(cond_np).cuda().to(torch.bfloat16)
+    ws = torch.empty(ftts.dit_workspace_bytes(dm.cfg, T), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    cfg_w, dt = 1.7, 1.0 / K
+
+    def solve(evs=None):
+        x.copy_(x0)
+        for k in range(K):
+            if evs is not None:
+                evs[k][0].record(stream)
+            ftts.dit_step(dm, x, cond, k * dt, dt, cfg_w, x, None, ws)
+            if evs is not None:
+                evs[k][1].record(stream)
+
+    graph = None
+    if args.graph:
+        solve()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            solve()
+    for _ in range(args.warmup):
+        graph.replay() if graph else solve()
+    torch.cuda.synchronize()
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+           for _ in range(args.steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    stream = torch.cuda.current_stream()
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for j in range(args.steps):
+        if graph:
+            graph.replay()
+        else:
+            solve(evs[j])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    job_ms = t0.elapsed_time(t1) / args.steps
+    step_ms = job_ms / K if graph else float(np.mean([[a.elapsed_time(b) for a, b in r] for r in evs]))
+    fl = dit_flops(shape, T)
+    achieved = fl / (step_ms / 1e3) / 1e12
+    peak = 2500.0
+    out = {
+        "metric": "DiT guided Euler steps/s on 1 MI355X (96M flow-matching DiT); achieved TFLOP/s vs bf16 MFMA peak",
+        "value": round(1e3 / step_ms, 2), "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(job_ms, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: seeded random-init 96M DiT (13x768, 12 heads, FFN 3072, 128 mel, cond 1280)",
+        "config": {"workload": f"dit-96m bf16 frames={T} euler={K} cfg both branches in one batch",
+                   "frames": T, "euler_steps": K, "graph": bool(graph)},
+        "ms_per_euler_step": round(step_ms, 4),
+        "frames_per_s": round(T * 1e3 / step_ms, 1),
+        "wall_s": round(wall, 3),
+        "roofline": {"bound": "mfma", "kernel": "whole guided Euler step (GEMMs, attention, LayerNorms)",
+                     "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "flops_per_step": fl, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        import threadpoolctl
+        from oracle import dit as odit
+        cores = len(os.sched_getaffinity(0))
+        with threadpoolctl.threadpool_limits(cores):
+            ora = odit.DiT(w, shape.n_head, shape.d_head, dtype=np.float64)
+            c0 = time.perf_counter()
+            ora.step(x0_np, cond_np, 0.0, dt, cfg_w)
+            cpu_s = time.perf_counter() - c0
+            used = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
+        out["cpu_baseline"] = {"value": round(1.0 / cpu_s, 4), "unit": "steps/s", "cores": int(min(used, cores)),
+                               "kind": "oracle", "sample": f"one guided Euler step over {T} frames, numpy fp64 "
+                                                           f"oracle on the same bf16 weights"}
+    return out
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -344,6 +443,9 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
+    if args.dit:
+        print(json.dumps(dit_run(args, torch, ftts, workload)), flush=True)
+        return
     shape = workload.INDEXTTS2
     mode = args.mode
     wdtype = {"f32": ftts.F32, "bf16": ftts.BF16, "w8a16": ftts.W8A16, "w4a16": ftts.W4A16}[mode]

@@ -322,6 +322,58 @@ int ftts_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t
 int ftts_sample(const float* logits, int32_t B, int32_t V, const ftts_sampling* samp,
                 const float* uniforms, int32_t* sampled_out, void* stream);
 
+/* ---- Semantic-to-Mel flow-matching DiT: one guided Euler step ------------------------
+ *
+ * Sec. II-A: the Semantic-to-Mel module is conditional flow matching with a
+ * Diffusion Transformer conditioned on the GPT's hidden states; inference runs an
+ * Euler ODE solver with classifier-free guidance over several steps.  Sec. III-A:
+ * the DiT has 96M parameters.  The paper gives no block layout; this step reads
+ * it as (all weights bf16, biases and LayerNorm parameters bf16, fp32 residual):
+ *   e(t) = W_t2 silu(W_t1 s(t) + b_t1) + b_t2, s(t) = [cos(1000 t f_i), sin(1000 t f_i)],
+ *          f_i = 10000^(-i / (t_dim/2))
+ *   h    = [x | c] W_in^T + b_in + e(t)                  (one row per frame)
+ *   h   += Attn(LN1(h)) W_out^T + b_out ; h += gelu(LN2(h) W_fc1^T + b_fc1) W_fc2^T + b_fc2
+ *          (ftts_layer blocks; attention over all frames, no mask, no positions)
+ *   v(c) = LN_f(h) W_mel^T + b_mel
+ *   v    = v(0) + cfg_w (v(c) - v(0)) ;  x' = x + dt v
+ */
+typedef struct {
+    int32_t n_layer, d_model, n_head, d_head, d_ff;
+    int32_t n_mel;   /* state width (mel bins) */
+    int32_t d_cond;  /* conditioning row width */
+    int32_t t_dim;   /* sinusoidal time features (even) */
+    float ln_eps;
+} ftts_dit_config;
+
+/* in.w [d_model][n_mel + d_cond]; t1.w [d_model][t_dim]; t2.w [d_model][d_model];
+ * layers: [host] array of n_layer blocks as in ftts_layer; lnf_g / lnf_b [d_model];
+ * mel.w [n_mel][d_model].  Every tensor bf16 (scale / zero unused), 16-byte aligned. */
+typedef struct {
+    ftts_dit_config cfg;
+    ftts_linear in;
+    ftts_linear t1;
+    ftts_linear t2;
+    const ftts_layer* layers;
+    const void* lnf_g;
+    const void* lnf_b;
+    ftts_linear mel;
+} ftts_dit_weights;
+
+/* Workspace bytes for ftts_dit_step with up to max_frames frames. */
+size_t ftts_dit_workspace_bytes(const ftts_dit_config* cfg, int32_t max_frames);
+
+/* One guided Euler step over T frames (both guidance branches in one batch).
+ *   x       [T][n_mel] fp32, the state at time t
+ *   cond    [T][d_cond] bf16, conditioning rows (zeroed for the unguided branch)
+ *   t, dt, cfg_w   time, step, guidance strength (host floats; t, dt finite)
+ *   x_out   [T][n_mel] fp32, x + dt v (may alias x)
+ *   v_out   [T][n_mel] fp32, the guided velocity, or NULL
+ * Requires d_head == 64, d_model, d_ff and n_mel multiples of 64, n_mel + d_cond a
+ * multiple of 64, t_dim even and <= 1024, 1 <= T (FTTS_E_SHAPE otherwise).
+ * FTTS_E_WORKSPACE if ws_bytes < ftts_dit_workspace_bytes(cfg, T). */
+int ftts_dit_step(const ftts_dit_weights* w, const float* x, const void* cond, int32_t T, float t, float dt,
+                  float cfg_w, float* x_out, float* v_out, void* ws, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

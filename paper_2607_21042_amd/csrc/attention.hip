@@ -22,7 +22,9 @@
 // straight from its score registers: the MFMA k order is a permutation shared by
 // both operands, so P needs no reshuffle.  V is transposed through LDS (double
 // buffered, one barrier per tile).  fp32 activations keep a VALU kernel: one
-// thread per query row streams 64-key tiles of K and V through LDS.
+// thread per query row streams 64-key tiles of K and V through LDS.  The same
+// matrix-core kernel without the causal mask serves the flow-matching DiT, whose
+// frames all see each other.
 #include "kv_page.hpp"
 
 namespace ftts {
@@ -409,6 +411,8 @@ constexpr int kVtStride = kPfK + 8;                // bf16 per transposed-V row 
 
 __device__ __forceinline__ pf_bf16x8 pf_op(uint4 v) { return __builtin_bit_cast(pf_bf16x8, v); }
 
+// CAUSAL: query i sees keys 0..i of its sequence; otherwise every key of it.
+template <bool CAUSAL>
 __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const AttnPrefillArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t vt[2][kHeadDim][kVtStride];
     const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -451,7 +455,7 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const 
 #pragma unroll
     for (int i = 0; i < 16; ++i) o0[i] = o1[i] = 0.f;
     float m = -INFINITY, l = 0.f;
-    const int kend = min(len, tile * kPfQ + kPfQ);  // keys any query of this workgroup sees
+    const int kend = CAUSAL ? min(len, tile * kPfQ + kPfQ) : len;  // keys any query of this workgroup sees
     const int ntiles = (kend + kPfK - 1) / kPfK;
     store_v(load_v(0), 0);
     __syncthreads();
@@ -459,7 +463,7 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const 
         const int buf = t & 1, k0 = t * kPfK;
         uint4 vnext = make_uint4(0, 0, 0, 0);
         if (t + 1 < ntiles) vnext = load_v(t + 1);
-        if (k0 <= qw + 31 && qw < len) {  // some query of this wave sees a key of this tile
+        if ((!CAUSAL || k0 <= qw + 31) && qw < len) {  // some query of this wave sees a key of this tile
             // K as the A operand: lane (key k0 + ql, hh) holds dims kk*16 + hh*8 .. +7
             const uint16_t* krow = qkv + (size_t)(row0 + min(k0 + ql, len - 1)) * ld + a.d_model + h * kHeadDim;
             uint4 kr[4];
@@ -475,7 +479,7 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const 
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const int key = k0 + (i >> 2) * 8 + hh * 4 + (i & 3);
-                s[i] = key <= qi && key < len ? s[i] * kScale : -INFINITY;
+                s[i] = (!CAUSAL || key <= qi) && key < len ? s[i] * kScale : -INFINITY;
                 tmax = fmaxf(tmax, s[i]);
             }
             {
@@ -542,7 +546,12 @@ int prefill_tile_rows(int wdtype) { return wdtype == FTTS_F32 ? 64 : kPfQ; }
 hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_tiles, hipStream_t st) {
     const dim3 g(total_tiles, a.n_head);
     if (wdtype == FTTS_F32) hipLaunchKernelGGL(attn_prefill_kernel<true>, g, dim3(64), 0, st, a);
-    else hipLaunchKernelGGL(attn_prefill_mfma_kernel, g, dim3(kPfWaves * 64), 0, st, a);
+    else hipLaunchKernelGGL(attn_prefill_mfma_kernel<true>, g, dim3(kPfWaves * 64), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_full_bf16(const AttnPrefillArgs& a, int total_tiles, hipStream_t st) {
+    hipLaunchKernelGGL(attn_prefill_mfma_kernel<false>, dim3(total_tiles, a.n_head), dim3(kPfWaves * 64), 0, st, a);
     return hipGetLastError();
 }
 

@@ -843,3 +843,215 @@ int ftts_prefill_ids(const ftts_weights* w, const void* cond_emb, const int32_t*
 }
 
 }  // extern "C"
+
+// ---- flow-matching DiT step -------------------------------------------------------------
+
+namespace {
+
+struct DitWs {
+    float* h;        // [M][D] fp32 residual stream
+    void* a;         // [M][max(D, Kin)] bf16: input rows, LayerNorm outputs, attention outputs
+    void* qkv;       // [M][3D] bf16
+    void* f;         // [M][F] bf16 GELU activations
+    float* vel;      // [M][n_mel] fp32 velocities of both branches
+    float* u;        // [D] time MLP hidden
+    float* e;        // [D] time embedding
+    float* part;     // split-K partial tiles
+    uint32_t* count; // split-K arrival counters
+    size_t n_count;
+};
+
+int check_dit_config(const ftts_dit_config* c) {
+    if (!c) return fail(FTTS_E_INVALID_ARG, "config is NULL");
+    if (c->n_layer < 1) return fail(FTTS_E_SHAPE, "n_layer must be >= 1");
+    if (c->d_head != kHeadDim) return fail(FTTS_E_UNSUPPORTED, "d_head must be 64 (got %d)", c->d_head);
+    if (c->n_head < 1 || c->n_head * kHeadDim != c->d_model)
+        return fail(FTTS_E_SHAPE, "n_head * d_head must equal d_model");
+    if (c->d_model % 64 || c->d_model > 2048) return fail(FTTS_E_SHAPE, "d_model must be a multiple of 64, <= 2048");
+    if (c->d_ff < 64 || c->d_ff % 64 || c->d_ff > 16384) return fail(FTTS_E_SHAPE, "d_ff must be a multiple of 64");
+    if (c->n_mel < 64 || c->n_mel % 64) return fail(FTTS_E_SHAPE, "n_mel must be a positive multiple of 64");
+    if (c->d_cond < 0 || (c->n_mel + c->d_cond) % 64)
+        return fail(FTTS_E_SHAPE, "n_mel + d_cond must be a multiple of 64");
+    if (c->t_dim < 2 || c->t_dim > 1024 || c->t_dim % 2) return fail(FTTS_E_SHAPE, "t_dim must be even, <= 1024");
+    if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return fail(FTTS_E_RANGE, "ln_eps must be finite and > 0");
+    return FTTS_OK;
+}
+
+// Split-K scratch of the step's six GEMM shapes at M = 2T rows, maximised over every
+// row count up to M (a smaller call may split where a larger one does not).
+void dit_gemm_scratch(const ftts_dit_config& c, int M, size_t* part_floats, size_t* counters) {
+    const int d = c.d_model, F = c.d_ff, Kin = c.n_mel + c.d_cond;
+    const int NK[6][2] = {{d, Kin}, {3 * d, d}, {d, d}, {F, d}, {d, F}, {c.n_mel, d}};
+    size_t pf = 0, cn = 0;
+    for (int r = 64;; r += 64) {
+        const int rows = std::min(r, M);
+        for (const auto& t : NK) {
+            const GemmPlan p = gemm_plan(rows, t[0], t[1]);
+            if (p.splits > 1) {
+                pf = std::max(pf, (size_t)p.splits * rows * t[0]);
+                cn = std::max(cn, (size_t)p.tiles_m * p.tiles_n);
+            }
+        }
+        if (rows >= M) break;
+    }
+    *part_floats = pf;
+    *counters = cn;
+}
+
+size_t dit_bytes(const ftts_dit_config& c, int T, DitWs* out, char* base) {
+    const size_t M = 2 * (size_t)T, d = c.d_model, Kin = (size_t)c.n_mel + c.d_cond;
+    size_t off = 0;
+    auto take = [&](size_t n) { size_t o = off; off += round256(n); return base ? base + o : nullptr; };
+    char* h = take(M * d * 4);
+    char* a = take(M * std::max(d, Kin) * 2);
+    char* qkv = take(M * 3 * d * 2);
+    char* f = take(M * (size_t)c.d_ff * 2);
+    char* vel = take(M * (size_t)c.n_mel * 4);
+    char* u = take(d * 4);
+    char* e = take(d * 4);
+    size_t pf, cn;
+    dit_gemm_scratch(c, (int)M, &pf, &cn);
+    char* part = pf ? take(pf * 4) : nullptr;
+    char* count = cn ? take(cn * 4) : nullptr;
+    if (out) *out = DitWs{(float*)h, a, qkv, f, (float*)vel, (float*)u, (float*)e, (float*)part, (uint32_t*)count, cn};
+    return off;
+}
+
+int check_bf16_linear(const ftts_linear& l, const char* name) {
+    char buf[64];
+    snprintf(buf, sizeof(buf), "%s.w", name);
+    TRY(check_ptr(l.w, buf));
+    snprintf(buf, sizeof(buf), "%s.bias", name);
+    TRY(check_ptr(l.bias, buf));
+    return FTTS_OK;
+}
+
+int check_dit_weights(const ftts_dit_weights* w) {
+    if (!w) return fail(FTTS_E_INVALID_ARG, "weights is NULL");
+    TRY(check_dit_config(&w->cfg));
+    TRY(check_bf16_linear(w->in, "in"));
+    TRY(check_bf16_linear(w->t1, "t1"));
+    TRY(check_bf16_linear(w->t2, "t2"));
+    TRY(check_bf16_linear(w->mel, "mel"));
+    TRY(check_ptr(w->lnf_g, "lnf_g"));
+    TRY(check_ptr(w->lnf_b, "lnf_b"));
+    if (!w->layers) return fail(FTTS_E_INVALID_ARG, "layers is NULL");
+    for (int l = 0; l < w->cfg.n_layer; ++l) {
+        const ftts_layer& L = w->layers[l];
+        TRY(check_ptr(L.ln1_g, "ln1_g"));
+        TRY(check_ptr(L.ln1_b, "ln1_b"));
+        TRY(check_ptr(L.ln2_g, "ln2_g"));
+        TRY(check_ptr(L.ln2_b, "ln2_b"));
+        TRY(check_bf16_linear(L.qkv, "qkv"));
+        TRY(check_bf16_linear(L.out, "out"));
+        TRY(check_bf16_linear(L.fc1, "fc1"));
+        TRY(check_bf16_linear(L.fc2, "fc2"));
+    }
+    return FTTS_OK;
+}
+
+GemmArgs dit_gemm(const ftts_linear& l, const void* a, int M, int N, int K, void* out, const DitWs& W) {
+    GemmArgs g{};
+    g.a = a;
+    g.w = l.w;
+    g.bias = l.bias;
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.out = out;
+    g.part = W.part;
+    g.count = W.count;
+    return g;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ftts_dit_workspace_bytes(const ftts_dit_config* cfg, int32_t max_frames) {
+    if (check_dit_config(cfg) != FTTS_OK || max_frames < 1 || max_frames > (1 << 20)) return 0;
+    return dit_bytes(*cfg, max_frames, nullptr, nullptr);
+}
+
+int ftts_dit_step(const ftts_dit_weights* w, const float* x, const void* cond, int32_t T, float t, float dt,
+                  float cfg_w, float* x_out, float* v_out, void* ws, size_t ws_bytes, void* stream) {
+    TRY(check_dit_weights(w));
+    const ftts_dit_config& c = w->cfg;
+    if (T < 1 || T > (1 << 20)) return fail(FTTS_E_SHAPE, "T must be in [1, 2^20] (got %d)", T);
+    if (!std::isfinite(t) || !std::isfinite(dt) || !std::isfinite(cfg_w))
+        return fail(FTTS_E_RANGE, "t, dt and cfg_w must be finite");
+    TRY(check_ptr(x, "x"));
+    TRY(check_ptr(x_out, "x_out"));
+    if (c.d_cond > 0) TRY(check_ptr(cond, "cond"));
+    if (v_out) TRY(check_ptr(v_out, "v_out"));
+    TRY(check_ptr(ws, "workspace"));
+    const size_t need = dit_bytes(c, T, nullptr, nullptr);
+    if (ws_bytes < need) return fail(FTTS_E_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
+
+    hipStream_t st = (hipStream_t)stream;
+    DitWs W;
+    dit_bytes(c, T, &W, reinterpret_cast<char*>(ws));
+    const int d = c.d_model, F = c.d_ff, M = 2 * T, Kin = c.n_mel + c.d_cond;
+
+    (void)hipGetLastError();
+    hipError_t e;
+    if ((e = launch_dit_time(t, w->t1.w, w->t1.bias, w->t2.w, w->t2.bias, d, c.t_dim, W.u, W.e, st)) != hipSuccess)
+        return hip_fail(e, "time embedding");
+    DitPrepareArgs pa{};
+    pa.T = T;
+    pa.n_mel = c.n_mel;
+    pa.d_cond = c.d_cond;
+    pa.d_model = d;
+    pa.x = x;
+    pa.cond = cond;
+    pa.e = W.e;
+    pa.inp = W.a;
+    pa.h = W.h;
+    pa.vel = W.vel;
+    pa.count = W.count;
+    pa.n_count = W.n_count;
+    if ((e = launch_dit_prepare(pa, st)) != hipSuccess) return hip_fail(e, "step inputs");
+    // h = [x | c] W_in^T + b_in + e(t)
+    if ((e = launch_gemm(FTTS_BF16, EPI_RESID, dit_gemm(w->in, W.a, M, d, Kin, W.h, W), st)) != hipSuccess)
+        return hip_fail(e, "input projection");
+
+    AttnPrefillArgs ap{};
+    ap.qkv = W.qkv;
+    ap.o = W.a;
+    ap.d_model = d;
+    ap.n_head = c.n_head;
+    ap.seqs.n = 2;
+    ap.seqs.cu[0] = 0;
+    ap.seqs.cu[1] = T;
+    ap.seqs.cu[2] = M;
+    const int qt = (T + prefill_tile_rows(FTTS_BF16) - 1) / prefill_tile_rows(FTTS_BF16);
+    ap.tiles_cu[0] = 0;
+    ap.tiles_cu[1] = qt;
+    ap.tiles_cu[2] = 2 * qt;
+
+    for (int l = 0; l < c.n_layer; ++l) {
+        const ftts_layer& L = w->layers[l];
+        if ((e = launch_ln_rows(FTTS_BF16, W.h, L.ln1_g, L.ln1_b, c.ln_eps, M, d, W.a, st)) != hipSuccess)
+            return hip_fail(e, "ln1");
+        if ((e = launch_gemm(FTTS_BF16, EPI_STORE, dit_gemm(L.qkv, W.a, M, 3 * d, d, W.qkv, W), st)) != hipSuccess)
+            return hip_fail(e, "qkv gemm");
+        if ((e = launch_attn_full_bf16(ap, ap.tiles_cu[2], st)) != hipSuccess) return hip_fail(e, "attention");
+        if ((e = launch_gemm(FTTS_BF16, EPI_RESID, dit_gemm(L.out, W.a, M, d, d, W.h, W), st)) != hipSuccess)
+            return hip_fail(e, "out gemm");
+        if ((e = launch_ln_rows(FTTS_BF16, W.h, L.ln2_g, L.ln2_b, c.ln_eps, M, d, W.a, st)) != hipSuccess)
+            return hip_fail(e, "ln2");
+        if ((e = launch_gemm(FTTS_BF16, EPI_GELU, dit_gemm(L.fc1, W.a, M, F, d, W.f, W), st)) != hipSuccess)
+            return hip_fail(e, "fc1 gemm");
+        if ((e = launch_gemm(FTTS_BF16, EPI_RESID, dit_gemm(L.fc2, W.f, M, d, F, W.h, W), st)) != hipSuccess)
+            return hip_fail(e, "fc2 gemm");
+    }
+    if ((e = launch_ln_rows(FTTS_BF16, W.h, w->lnf_g, w->lnf_b, c.ln_eps, M, d, W.a, st)) != hipSuccess)
+        return hip_fail(e, "final layer norm");
+    if ((e = launch_gemm(FTTS_BF16, EPI_RESID, dit_gemm(w->mel, W.a, M, c.n_mel, d, W.vel, W), st)) != hipSuccess)
+        return hip_fail(e, "mel projection");
+    if ((e = launch_dit_guide(W.vel, T, c.n_mel, cfg_w, dt, x, x_out, v_out, st)) != hipSuccess)
+        return hip_fail(e, "guidance");
+    return FTTS_OK;
+}
+
+}  // extern "C"

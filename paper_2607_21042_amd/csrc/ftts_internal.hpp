@@ -281,6 +281,9 @@ hipError_t launch_ln_rows(int wdtype, const float* x, const void* g, const void*
 hipError_t launch_gemm(int wdtype, int epi, const GemmArgs& a, hipStream_t st);
 hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_tiles, hipStream_t st);
 int prefill_tile_rows(int wdtype);  // queries per prefill-attention workgroup
+// Attention without a mask (every query sees every key of its sequence), bf16 rows of
+// prefill_tile_rows(FTTS_BF16) queries per workgroup.
+hipError_t launch_attn_full_bf16(const AttnPrefillArgs& a, int total_tiles, hipStream_t st);
 hipError_t launch_gather_rows(const float* x, int d, const SeqTable& seqs, float* out, hipStream_t st);
 hipError_t launch_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled,
                           int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,
@@ -291,6 +294,24 @@ int bgemm_splits(int wdtype, int N, int K, bool ln);
 bool bgemm_supported(int wdtype, int K, bool ln);
 hipError_t launch_act_to_f32(int wdtype, const void* src, int rows, int d, float* dst, hipStream_t st);
 hipError_t launch_assemble_prefix(int wdtype, const AssembleArgs& a, int rows, hipStream_t st);
+
+// Flow-matching DiT step (bf16): time embedding, input rows and guidance.
+struct DitPrepareArgs {
+    int T, n_mel, d_cond, d_model;
+    const float* x;          // [T][n_mel] state
+    const void* cond;        // [T][d_cond] bf16
+    const float* e;          // [d_model] time embedding
+    void* inp;               // [2T][n_mel + d_cond] bf16 out
+    float* h;                // [2T][d_model] out: every row = e
+    float* vel;              // [2T][n_mel] out: zeros
+    uint32_t* count;         // [n_count] out: zeros
+    size_t n_count;
+};
+hipError_t launch_dit_time(float t, const void* w1, const void* b1, const void* w2, const void* b2, int D, int t_dim,
+                           float* u, float* e, hipStream_t st);
+hipError_t launch_dit_prepare(const DitPrepareArgs& a, hipStream_t st);
+hipError_t launch_dit_guide(const float* vel, int T, int n_mel, float w, float dt, const float* x, float* x_out,
+                            float* v_out, hipStream_t st);
 
 namespace mega {
 constexpr int D = 1280, FF = 5120, NH = 20;

@@ -55,6 +55,16 @@ class Weights(_c.Structure):
                 ("lnf_g", vp), ("lnf_b", vp), ("head", Linear)]
 
 
+class DitConfig(_c.Structure):
+    _fields_ = [("n_layer", i32), ("d_model", i32), ("n_head", i32), ("d_head", i32), ("d_ff", i32),
+                ("n_mel", i32), ("d_cond", i32), ("t_dim", i32), ("ln_eps", f32)]
+
+
+class DitWeights(_c.Structure):
+    _fields_ = [("cfg", DitConfig), ("in_", Linear), ("t1", Linear), ("t2", Linear), ("layers", _c.POINTER(Layer)),
+                ("lnf_g", vp), ("lnf_b", vp), ("mel", Linear)]
+
+
 class KvPool(_c.Structure):
     _fields_ = [("base", vp), ("n_pages", i32)]
 
@@ -105,6 +115,10 @@ def lib():
         L.ftts_advance.argtypes = [vp, vp, vp, vp, vp, i32, vp, vp, i32, i32, vp]
         L.ftts_sample.restype = _c.c_int
         L.ftts_sample.argtypes = [vp, i32, i32, P(Sampling), vp, vp, vp]
+        L.ftts_dit_workspace_bytes.restype = _c.c_size_t
+        L.ftts_dit_workspace_bytes.argtypes = [P(DitConfig), i32]
+        L.ftts_dit_step.restype = _c.c_int
+        L.ftts_dit_step.argtypes = [P(DitWeights), vp, vp, i32, f32, f32, f32, vp, vp, vp, _c.c_size_t, vp]
         _lib = L
     return _lib
 
@@ -368,3 +382,68 @@ class PageTableView:
         self.block_table = block_table.to(torch.int32).contiguous()
         self.seq_lens = seq_lens.to(torch.int32).contiguous()
         self.c = PageTable(self.block_table.data_ptr(), self.seq_lens.data_ptr(), self.block_table.shape[1])
+
+
+# ---- flow-matching DiT step ---------------------------------------------------------------
+
+def make_dit_config(shape, eps: float = 1e-5) -> DitConfig:
+    return DitConfig(shape.n_layer, shape.d_model, shape.n_head, shape.d_head, shape.d_ff, shape.n_mel,
+                     shape.d_cond, shape.t_dim, eps)
+
+
+def dit_workspace_bytes(cfg: DitConfig, max_frames: int) -> int:
+    n = lib().ftts_dit_workspace_bytes(_c.byref(cfg), max_frames)
+    if n == 0:
+        raise FTTSError(-2, "invalid DiT config or frame count")
+    return n
+
+
+def dit_step(model, x, cond, t: float, dt: float, cfg_w: float, x_out, v_out, ws, stream=None):
+    """One guided Euler step over the T frames of x (ftts_dit_step)."""
+    T = x.shape[0]
+    _check(lib().ftts_dit_step(_c.byref(model.c), _ptr(x), _ptr(cond), T, t, dt, cfg_w, _ptr(x_out), _ptr(v_out),
+                               _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+class DitDeviceModel:
+    """DiT weights resident in HBM (bf16) plus the ftts_dit_weights struct pointing at them.
+
+    `weights` is the dict of ``workload.dit_master_weights``; its values must be
+    bf16-representable (``workload.bf16_round``) so that the oracle can take the
+    very same numbers.
+    """
+
+    GLOBAL = ("w_in", "b_in", "w_t1", "b_t1", "w_t2", "b_t2", "lnf_g", "lnf_b", "w_out_mel", "b_out_mel")
+    LAYER = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_out", "b_out", "ln2_g", "ln2_b", "w_fc1", "b_fc1", "w_fc2",
+             "b_fc2")
+
+    def __init__(self, weights: dict, shape, device="cuda"):
+        self.shape = shape
+        self.cfg = make_dit_config(shape)
+
+        def up(a):
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device).to(torch.bfloat16)
+
+        self.tensors = {k: up(weights[k]) for k in self.GLOBAL}
+        for k in self.LAYER:
+            self.tensors[k] = up(np.stack([lw[k] for lw in weights["layers"]]))
+        T = self.tensors
+        self.layers = (Layer * shape.n_layer)()
+        for l in range(shape.n_layer):
+            Ly = self.layers[l]
+            Ly.ln1_g, Ly.ln1_b = T["ln1_g"][l].data_ptr(), T["ln1_b"][l].data_ptr()
+            Ly.ln2_g, Ly.ln2_b = T["ln2_g"][l].data_ptr(), T["ln2_b"][l].data_ptr()
+            for name in ("qkv", "out", "fc1", "fc2"):
+                setattr(Ly, name, Linear(T["w_" + name][l].data_ptr(), None, None, T["b_" + name][l].data_ptr()))
+        c = DitWeights()
+        c.cfg = self.cfg
+        c.in_ = Linear(T["w_in"].data_ptr(), None, None, T["b_in"].data_ptr())
+        c.t1 = Linear(T["w_t1"].data_ptr(), None, None, T["b_t1"].data_ptr())
+        c.t2 = Linear(T["w_t2"].data_ptr(), None, None, T["b_t2"].data_ptr())
+        c.layers = self.layers
+        c.lnf_g, c.lnf_b = T["lnf_g"].data_ptr(), T["lnf_b"].data_ptr()
+        c.mel = Linear(T["w_out_mel"].data_ptr(), None, None, T["b_out_mel"].data_ptr())
+        self.c = c
+
+    def weight_bytes(self) -> int:
+        return sum(t.numel() * t.element_size() for t in self.tensors.values())

@@ -185,3 +185,57 @@ def test_decode_path_query():
         assert L.ftts_decode_path(ctypes.byref(w), 1) == 1
     finally:
         ftts.set_decode_path(ftts.PATH_AUTO)
+
+
+def _fake_dit(shape):
+    cfg = ftts.make_dit_config(shape)
+    layers = (ftts.Layer * shape.n_layer)()
+    for L in layers:
+        L.ln1_g = L.ln1_b = L.ln2_g = L.ln2_b = FAKE
+        for lin in (L.qkv, L.out, L.fc1, L.fc2):
+            lin.w = lin.bias = FAKE
+    w = ftts.DitWeights()
+    w.cfg = cfg
+    for lin in (w.in_, w.t1, w.t2, w.mel):
+        lin.w = lin.bias = FAKE
+    w.lnf_g = w.lnf_b = FAKE
+    w.layers = layers
+    w._layers = layers
+    return w
+
+
+def _dit_step(w, T=8, t=0.5, ws_bytes=1 << 30, x=FAKE, x_out=FAKE, cond=FAKE):
+    return ftts.lib().ftts_dit_step(ctypes.byref(w), x, cond, T, t, 0.1, 1.0, x_out, None, FAKE, ws_bytes, None)
+
+
+def test_dit_workspace_bytes():
+    """Grows with the frame count, covers the split-K scratch of every smaller
+    call, and is 0 for a config the step rejects."""
+    cfg = ftts.make_dit_config(workload.DIT_96M)
+    sizes = [ftts.dit_workspace_bytes(cfg, T) for T in (1, 2, 37, 64, 500, 4096)]
+    assert all(a < b for a, b in zip(sizes, sizes[1:]))
+    assert sizes[0] % 256 == 0
+    L = ftts.lib()
+    assert L.ftts_dit_workspace_bytes(ctypes.byref(cfg), 0) == 0
+    for field, value in [("d_head", 32), ("n_head", 5), ("n_mel", 100), ("d_cond", 33), ("t_dim", 3),
+                         ("t_dim", 2048), ("d_ff", 96), ("n_layer", 0), ("ln_eps", 0.0)]:
+        bad = ftts.make_dit_config(workload.DIT_96M)
+        setattr(bad, field, value)
+        assert L.ftts_dit_workspace_bytes(ctypes.byref(bad), 16) == 0, field
+
+
+def test_dit_step_argument_errors():
+    w = _fake_dit(workload.DIT_TINY)
+    L = ftts.lib()
+    assert _dit_step(w, T=0) == -2
+    assert _dit_step(w, t=float("inf")) == -5
+    assert _dit_step(w, x=None) == -1
+    assert _dit_step(w, x_out=FAKE + 8) == -4
+    assert _dit_step(w, cond=None) == -1
+    need = ftts.dit_workspace_bytes(w.cfg, 8)
+    assert _dit_step(w, ws_bytes=need - 1) == -8
+    assert b"workspace" in L.ftts_last_error()
+    w.layers[1].fc2.bias = None
+    assert _dit_step(w) == -1
+    w.cfg.d_head = 32
+    assert _dit_step(w) == -7
