@@ -59,7 +59,8 @@ def parse():
     p.add_argument("--requests", type=int, default=64)
     p.add_argument("--dit", action="store_true",
                    help="flow-matching DiT (96M shape): guided Euler steps over --frames mel frames")
-    p.add_argument("--frames", type=int, default=500)
+    p.add_argument("--frames", type=int, default=500, help="DiT: mel frames per utterance")
+    p.add_argument("--dit-batch", type=int, default=1, help="DiT: utterances per step")
     p.add_argument("--euler", type=int, default=25, help="Euler steps per DiT job")
     p.add_argument("--graph", action="store_true", help="DiT: replay each job's steps from one HIP graph")
     p.add_argument("--copy-calibration", action="store_true",
@@ -334,28 +335,32 @@ def serve_run(args, torch, ftts, workload, shape, dm, mode):
     }
 
 
-def dit_flops(shape, T):
-    """Algorithmic flops of one guided Euler step over T frames (both branches):
-    2 M N K per linear at M = 2T rows, 4 T^2 d per block and branch for the
-    attention (Q K^T and P V), and the M-independent time MLP."""
-    M, d = 2 * T, shape.d_model
+def dit_flops(shape, lens):
+    """Algorithmic flops of one guided Euler step over utterances of `lens` frames
+    (both branches): 2 M N K per linear at M = 2 sum(lens) rows, 4 T^2 d per
+    block, branch and utterance of T frames for the attention (Q K^T and P V),
+    and the M-independent time MLP."""
+    M, d = 2 * sum(lens), shape.d_model
     lin = sum(N * K for _, N, K in shape.matrices()) * shape.n_layer + d * (shape.n_mel + shape.d_cond) \
         + shape.n_mel * d
-    return 2.0 * M * lin + shape.n_layer * 2 * 4.0 * T * T * d + 2.0 * (d * shape.t_dim + d * d)
+    att = sum(4.0 * T * T * d for T in lens)
+    return 2.0 * M * lin + shape.n_layer * 2 * att + 2.0 * (d * shape.t_dim + d * d)
 
 
 def dit_run(args, torch, ftts, workload):
-    """One job = --euler guided Euler steps of the 96M DiT over --frames frames
-    (t from 0 to 1 in equal steps), state and conditioning resident in HBM."""
+    """One job = --euler guided Euler steps of the 96M DiT for --dit-batch
+    utterances of --frames frames each (t from 0 to 1 in equal steps), state and
+    conditioning resident in HBM."""
     shape = workload.DIT_96M
-    T, K = args.frames, args.euler
+    T, K, B = args.frames, args.euler, args.dit_batch
+    lens = [T] * B
     w = workload.bf16_weights(workload.dit_master_weights(shape, seed=20))
     dm = ftts.DitDeviceModel(w, shape)
-    x0_np, cond_np = workload.dit_inputs(shape, T, seed=21)
+    x0_np, cond_np = workload.dit_inputs(shape, T * B, seed=21)
     x0 = torch.from_numpy(x0_np).cuda()
     x = torch.empty_like(x0)
     cond = torch.from_numpy(cond_np).cuda().to(torch.bfloat16)
-    ws = torch.empty(ftts.dit_workspace_bytes(dm.cfg, T), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(ftts.dit_workspace_bytes(dm.cfg, T * B), dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
     cfg_w, dt = 1.7, 1.0 / K
 
@@ -364,7 +369,7 @@ def dit_run(args, torch, ftts, workload):
         for k in range(K):
             if evs is not None:
                 evs[k][0].record(stream)
-            ftts.dit_step(dm, x, cond, k * dt, dt, cfg_w, x, None, ws)
+            ftts.dit_step(dm, x, cond, k * dt, dt, cfg_w, x, None, ws, lens=lens)
             if evs is not None:
                 evs[k][1].record(stream)
 
@@ -394,7 +399,7 @@ def dit_run(args, torch, ftts, workload):
     wall = time.perf_counter() - wall0
     job_ms = t0.elapsed_time(t1) / args.steps
     step_ms = job_ms / K if graph else float(np.mean([[a.elapsed_time(b) for a, b in r] for r in evs]))
-    fl = dit_flops(shape, T)
+    fl = dit_flops(shape, lens)
     achieved = fl / (step_ms / 1e3) / 1e12
     peak = 2500.0
     out = {
@@ -403,10 +408,10 @@ def dit_run(args, torch, ftts, workload):
         "warmup": args.warmup, "ms_per_step": round(job_ms, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic: seeded random-init 96M DiT (13x768, 12 heads, FFN 3072, 128 mel, cond 1280)",
-        "config": {"workload": f"dit-96m bf16 frames={T} euler={K} cfg both branches in one batch",
-                   "frames": T, "euler_steps": K, "graph": bool(graph)},
+        "config": {"workload": f"dit-96m bf16 batch={B} frames={T} euler={K} cfg both branches in one batch",
+                   "batch": B, "frames": T, "euler_steps": K, "graph": bool(graph)},
         "ms_per_euler_step": round(step_ms, 4),
-        "frames_per_s": round(T * 1e3 / step_ms, 1),
+        "frames_per_s": round(B * T * 1e3 / step_ms, 1),
         "wall_s": round(wall, 3),
         "roofline": {"bound": "mfma", "kernel": "whole guided Euler step (GEMMs, attention, LayerNorms)",
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
@@ -419,12 +424,13 @@ def dit_run(args, torch, ftts, workload):
         with threadpoolctl.threadpool_limits(cores):
             ora = odit.DiT(w, shape.n_head, shape.d_head, dtype=np.float64)
             c0 = time.perf_counter()
-            ora.step(x0_np, cond_np, 0.0, dt, cfg_w)
-            cpu_s = time.perf_counter() - c0
+            ora.step(x0_np[:T], cond_np[:T], 0.0, dt, cfg_w)  # one utterance; the rate below scales by B
+            cpu_s = (time.perf_counter() - c0) * B
             used = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
         out["cpu_baseline"] = {"value": round(1.0 / cpu_s, 4), "unit": "steps/s", "cores": int(min(used, cores)),
-                               "kind": "oracle", "sample": f"one guided Euler step over {T} frames, numpy fp64 "
-                                                           f"oracle on the same bf16 weights"}
+                               "kind": "oracle", "sample": f"one guided Euler step of one {T}-frame utterance, "
+                                                           f"numpy fp64 oracle on the same bf16 weights, "
+                                                           f"scaled to the batch of {B}"}
     return out
 
 

@@ -359,20 +359,28 @@ typedef struct {
     ftts_linear mel;
 } ftts_dit_weights;
 
-/* Workspace bytes for ftts_dit_step with up to max_frames frames. */
+#define FTTS_DIT_MAX_BATCH 32
+
+/* Workspace bytes for ftts_dit_step over up to max_frames frames in total. */
 size_t ftts_dit_workspace_bytes(const ftts_dit_config* cfg, int32_t max_frames);
 
-/* One guided Euler step over T frames (both guidance branches in one batch).
- *   x       [T][n_mel] fp32, the state at time t
- *   cond    [T][d_cond] bf16, conditioning rows (zeroed for the unguided branch)
- *   t, dt, cfg_w   time, step, guidance strength (host floats; t, dt finite)
- *   x_out   [T][n_mel] fp32, x + dt v (may alias x)
- *   v_out   [T][n_mel] fp32, the guided velocity, or NULL
+/* One guided Euler step for a batch of B utterances (Sec. II-B: every stage runs
+ * batched over utterances of different lengths), their frames packed one after
+ * another instead of padded: utterance b owns frames
+ * [sum_{i<b} lens[i], sum_{i<=b} lens[i]) and attends only to its own frames.
+ * All utterances share t, dt and cfg_w; both guidance branches run in one pass.
+ *   x       [S][n_mel] fp32, the state at time t (S = sum of lens)
+ *   cond    [S][d_cond] bf16, conditioning rows (zeroed for the unguided branch)
+ *   lens    [host][B] frames per utterance, each >= 1; 1 <= B <= FTTS_DIT_MAX_BATCH
+ *   t, dt, cfg_w   time, step, guidance strength (finite host floats)
+ *   x_out   [S][n_mel] fp32, x + dt v (may alias x)
+ *   v_out   [S][n_mel] fp32, the guided velocity, or NULL
  * Requires d_head == 64, d_model, d_ff and n_mel multiples of 64, n_mel + d_cond a
- * multiple of 64, t_dim even and <= 1024, 1 <= T (FTTS_E_SHAPE otherwise).
- * FTTS_E_WORKSPACE if ws_bytes < ftts_dit_workspace_bytes(cfg, T). */
-int ftts_dit_step(const ftts_dit_weights* w, const float* x, const void* cond, int32_t T, float t, float dt,
-                  float cfg_w, float* x_out, float* v_out, void* ws, size_t ws_bytes, void* stream);
+ * multiple of 64, t_dim even and <= 1024 (FTTS_E_SHAPE / FTTS_E_UNSUPPORTED otherwise).
+ * FTTS_E_WORKSPACE if ws_bytes < ftts_dit_workspace_bytes(cfg, S). */
+int ftts_dit_step(const ftts_dit_weights* w, const float* x, const void* cond, const int32_t* lens, int32_t B,
+                  float t, float dt, float cfg_w, float* x_out, float* v_out, void* ws, size_t ws_bytes,
+                  void* stream);
 
 #ifdef __cplusplus
 }

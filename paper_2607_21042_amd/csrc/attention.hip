@@ -22,9 +22,11 @@
 // straight from its score registers: the MFMA k order is a permutation shared by
 // both operands, so P needs no reshuffle.  V is transposed through LDS (double
 // buffered, one barrier per tile).  fp32 activations keep a VALU kernel: one
-// thread per query row streams 64-key tiles of K and V through LDS.  The same
-// matrix-core kernel without the causal mask serves the flow-matching DiT, whose
-// frames all see each other.
+// thread per query row streams 64-key tiles of K and V through LDS.
+//
+// Full attention (no mask: the flow-matching DiT's frames all see each other)
+// has its own matrix-core kernel, attn_full_mfma_kernel, which splits the keys
+// of a query tile over the waves of a workgroup.
 #include "kv_page.hpp"
 
 namespace ftts {
@@ -411,8 +413,6 @@ constexpr int kVtStride = kPfK + 8;                // bf16 per transposed-V row 
 
 __device__ __forceinline__ pf_bf16x8 pf_op(uint4 v) { return __builtin_bit_cast(pf_bf16x8, v); }
 
-// CAUSAL: query i sees keys 0..i of its sequence; otherwise every key of it.
-template <bool CAUSAL>
 __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const AttnPrefillArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t vt[2][kHeadDim][kVtStride];
     const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -455,7 +455,7 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const 
 #pragma unroll
     for (int i = 0; i < 16; ++i) o0[i] = o1[i] = 0.f;
     float m = -INFINITY, l = 0.f;
-    const int kend = CAUSAL ? min(len, tile * kPfQ + kPfQ) : len;  // keys any query of this workgroup sees
+    const int kend = min(len, tile * kPfQ + kPfQ);  // keys any query of this workgroup sees
     const int ntiles = (kend + kPfK - 1) / kPfK;
     store_v(load_v(0), 0);
     __syncthreads();
@@ -463,7 +463,7 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const 
         const int buf = t & 1, k0 = t * kPfK;
         uint4 vnext = make_uint4(0, 0, 0, 0);
         if (t + 1 < ntiles) vnext = load_v(t + 1);
-        if ((!CAUSAL || k0 <= qw + 31) && qw < len) {  // some query of this wave sees a key of this tile
+        if (k0 <= qw + 31 && qw < len) {  // some query of this wave sees a key of this tile
             // K as the A operand: lane (key k0 + ql, hh) holds dims kk*16 + hh*8 .. +7
             const uint16_t* krow = qkv + (size_t)(row0 + min(k0 + ql, len - 1)) * ld + a.d_model + h * kHeadDim;
             uint4 kr[4];
@@ -479,7 +479,7 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const 
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const int key = k0 + (i >> 2) * 8 + hh * 4 + (i & 3);
-                s[i] = (!CAUSAL || key <= qi) && key < len ? s[i] * kScale : -INFINITY;
+                s[i] = key <= qi && key < len ? s[i] * kScale : -INFINITY;
                 tmax = fmaxf(tmax, s[i]);
             }
             {
@@ -541,17 +541,205 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const 
     }
 }
 
+// Attention without a mask (every query sees every key of its sequence), bf16.
+// A workgroup takes 32 queries of one head; its 4 waves split the 32-key tiles
+// round-robin (wave w takes tiles w, w + 4, ...), so a sequence of L keys keeps
+// ceil(L / 32) * 4 waves busy per head and each wave's dependent chain is a
+// quarter of the keys.  Every wave forms S^T = K Q^T and O^T = V^T P^T as in the
+// prefill kernel, transposes its own V tile through a private LDS slice (no
+// workgroup barrier in the loop) and prefetches the next tile's K and V rows
+// into registers.  The four (max, sum, output) partials are merged by the
+// log-sum-exp rule through LDS at the end.
+constexpr int kFaWaves = 4, kFaQ = 32, kFaK = 32;
+
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__global__ __launch_bounds__(kFaWaves * 64) void attn_full_mfma_kernel(const AttnPrefillArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t vt[kFaWaves][kHeadDim][kVtStride];
+    __shared__ float mrg[kFaWaves - 1][34][64];  // waves 1..3: 32 output values, max, sum per lane
+    const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int gt = blockIdx.x, sq = 0;
+    while (sq + 1 < a.seqs.n && a.tiles_cu[sq + 1] <= gt) ++sq;
+    const int tile = gt - a.tiles_cu[sq];
+    const int row0 = a.seqs.cu[sq], len = a.seqs.cu[sq + 1] - row0;
+    if (len <= 0) return;  // uniform over the workgroup
+    const size_t ld = 3 * (size_t)a.d_model;
+    const uint16_t* qkv = reinterpret_cast<const uint16_t*>(a.qkv);
+    const int ql = lane & 31, hh = lane >> 5;
+    const int qi = tile * kFaQ + ql;
+    const float kScale = 0.125f * 1.44269504088896340736f;  // 1/sqrt(64) * log2(e)
+
+    uint4 qr[4];
+    {
+        const uint16_t* qrow = qkv + (size_t)(row0 + min(qi, len - 1)) * ld + h * kHeadDim;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qr[kk] = *reinterpret_cast<const uint4*>(qrow + kk * 16 + hh * 8);
+    }
+    // V staging: lane l carries keys 2p, 2p + 1 (p = l % 16) of the tile, dims g*16 .. +15 (g = l / 16)
+    const int vp = lane & 15, vg = lane >> 4;
+    auto load_k = [&](int t, uint4 (&kr)[4]) {
+        const uint16_t* krow = qkv + (size_t)(row0 + min(t * kFaK + ql, len - 1)) * ld + a.d_model + h * kHeadDim;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) kr[kk] = *reinterpret_cast<const uint4*>(krow + kk * 16 + hh * 8);
+    };
+    auto load_v = [&](int t, uint4 (&vr)[4]) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int key = min(t * kFaK + 2 * vp + e, len - 1);
+            const uint16_t* vrow = qkv + (size_t)(row0 + key) * ld + 2 * a.d_model + h * kHeadDim + vg * 16;
+            vr[2 * e] = *reinterpret_cast<const uint4*>(vrow);
+            vr[2 * e + 1] = *reinterpret_cast<const uint4*>(vrow + 8);
+        }
+    };
+    const int nt = (len + kFaK - 1) / kFaK;
+    const int t0 = wave;
+
+    pf_f32x16 o0, o1;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o0[i] = o1[i] = 0.f;
+    float m = -INFINITY, l = 0.f;
+    uint4 kr[4], vr[4];
+    if (t0 < nt) {
+        load_k(t0, kr);
+        load_v(t0, vr);
+    }
+    for (int t = t0; t < nt; t += kFaWaves) {
+        // V^T of this tile into the wave's LDS slice: one 32-bit word = two keys of one dim
+        const uint32_t w0[8] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w, vr[1].x, vr[1].y, vr[1].z, vr[1].w};
+        const uint32_t w1[8] = {vr[2].x, vr[2].y, vr[2].z, vr[2].w, vr[3].x, vr[3].y, vr[3].z, vr[3].w};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const uint32_t lo = (j & 1) ? (w0[j >> 1] >> 16) : (w0[j >> 1] & 0xFFFFu);
+            const uint32_t hi = (j & 1) ? (w1[j >> 1] >> 16) : (w1[j >> 1] & 0xFFFFu);
+            *reinterpret_cast<uint32_t*>(&vt[wave][vg * 16 + j][2 * vp]) = lo | (hi << 16);
+        }
+        uint4 kc[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) kc[kk] = kr[kk];
+        if (t + kFaWaves < nt) {  // next tile's rows, in flight during this one
+            load_k(t + kFaWaves, kr);
+            load_v(t + kFaWaves, vr);
+        }
+        const int k0 = t * kFaK;
+        pf_f32x16 s;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s[i] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(kc[kk]), pf_op(qr[kk]), s, 0, 0, 0);
+        float tmax = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int key = k0 + (i >> 2) * 8 + hh * 4 + (i & 3);
+            s[i] = key < len ? s[i] * kScale : -INFINITY;
+            tmax = fmaxf(tmax, s[i]);
+        }
+        {
+            const RowPair pr = swap32(tmax);
+            tmax = fmaxf(pr.a, pr.b);
+        }
+        const float mn = fmaxf(m, tmax);  // finite: key k0 < len is in this tile
+        const float alpha = exp2f(m - mn);
+        m = mn;
+        uint32_t pw[8];
+        float rs = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; i += 2) {
+            const uint16_t lo = f32_to_bf16(exp2f(s[i] - mn)), hi = f32_to_bf16(exp2f(s[i + 1] - mn));
+            rs += bf16_to_f32(lo) + bf16_to_f32(hi);
+            pw[i / 2] = (uint32_t)lo | ((uint32_t)hi << 16);
+        }
+        {
+            const RowPair pr = swap32(rs);
+            rs = pr.a + pr.b;
+        }
+        l = l * alpha + rs;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            o0[i] *= alpha;
+            o1[i] *= alpha;
+        }
+        wave_lds_sync();  // the V^T words of every lane are in LDS
+#pragma unroll
+        for (int st2 = 0; st2 < 2; ++st2) {
+            const pf_bf16x8 pb = pf_op(make_uint4(pw[4 * st2], pw[4 * st2 + 1], pw[4 * st2 + 2], pw[4 * st2 + 3]));
+            const int c = st2 * 16 + hh * 4;
+            const uint2 a0 = *reinterpret_cast<const uint2*>(&vt[wave][ql][c]);
+            const uint2 a1 = *reinterpret_cast<const uint2*>(&vt[wave][ql][c + 8]);
+            const uint2 b0 = *reinterpret_cast<const uint2*>(&vt[wave][32 + ql][c]);
+            const uint2 b1 = *reinterpret_cast<const uint2*>(&vt[wave][32 + ql][c + 8]);
+            o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(make_uint4(a0.x, a0.y, a1.x, a1.y)), pb, o0, 0, 0, 0);
+            o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(make_uint4(b0.x, b0.y, b1.x, b1.y)), pb, o1, 0, 0, 0);
+        }
+        wave_lds_sync();  // every lane has read the slice before the next tile overwrites it
+    }
+    // merge: waves 1..3 hand (o, m, l) to wave 0 lane for lane
+    if (wave > 0) {
+        float* mw = &mrg[wave - 1][0][0];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            mw[i * 64 + lane] = o0[i];
+            mw[(16 + i) * 64 + lane] = o1[i];
+        }
+        mw[32 * 64 + lane] = m;
+        mw[33 * 64 + lane] = l;
+    }
+    __syncthreads();
+    if (wave > 0 || qi >= len) return;
+    // wave 0 always holds tile 0, so m is finite; an idle wave has m = -inf, l = 0, o = 0
+    float mm = m;
+#pragma unroll
+    for (int w = 0; w < kFaWaves - 1; ++w) mm = fmaxf(mm, mrg[w][32][lane]);
+    float sc = exp2f(m - mm);
+    l *= sc;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        o0[i] *= sc;
+        o1[i] *= sc;
+    }
+#pragma unroll
+    for (int w = 0; w < kFaWaves - 1; ++w) {
+        const float f = exp2f(mrg[w][32][lane] - mm);
+        l += mrg[w][33][lane] * f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            o0[i] += mrg[w][i][lane] * f;
+            o1[i] += mrg[w][16 + i][lane] * f;
+        }
+    }
+    const float inv = 1.0f / l;
+    uint16_t* orow = reinterpret_cast<uint16_t*>(a.o) + (size_t)(row0 + qi) * a.d_model + h * kHeadDim;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const int dd = g * 8 + hh * 4;
+        *reinterpret_cast<uint2*>(orow + dd) =
+            make_uint2((uint32_t)f32_to_bf16(o0[4 * g] * inv) | ((uint32_t)f32_to_bf16(o0[4 * g + 1] * inv) << 16),
+                       (uint32_t)f32_to_bf16(o0[4 * g + 2] * inv) | ((uint32_t)f32_to_bf16(o0[4 * g + 3] * inv) << 16));
+        *reinterpret_cast<uint2*>(orow + 32 + dd) =
+            make_uint2((uint32_t)f32_to_bf16(o1[4 * g] * inv) | ((uint32_t)f32_to_bf16(o1[4 * g + 1] * inv) << 16),
+                       (uint32_t)f32_to_bf16(o1[4 * g + 2] * inv) | ((uint32_t)f32_to_bf16(o1[4 * g + 3] * inv) << 16));
+    }
+}
+
 int prefill_tile_rows(int wdtype) { return wdtype == FTTS_F32 ? 64 : kPfQ; }
 
 hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_tiles, hipStream_t st) {
     const dim3 g(total_tiles, a.n_head);
     if (wdtype == FTTS_F32) hipLaunchKernelGGL(attn_prefill_kernel<true>, g, dim3(64), 0, st, a);
-    else hipLaunchKernelGGL(attn_prefill_mfma_kernel<true>, g, dim3(kPfWaves * 64), 0, st, a);
+    else hipLaunchKernelGGL(attn_prefill_mfma_kernel, g, dim3(kPfWaves * 64), 0, st, a);
     return hipGetLastError();
 }
 
-hipError_t launch_attn_full_bf16(const AttnPrefillArgs& a, int total_tiles, hipStream_t st) {
-    hipLaunchKernelGGL(attn_prefill_mfma_kernel<false>, dim3(total_tiles, a.n_head), dim3(kPfWaves * 64), 0, st, a);
+hipError_t launch_attn_full_bf16(const AttnPrefillArgs& a, hipStream_t st) {
+    AttnPrefillArgs b = a;  // query tiles of this kernel's size
+    b.tiles_cu[0] = 0;
+    for (int i = 0; i < a.seqs.n; ++i)
+        b.tiles_cu[i + 1] = b.tiles_cu[i] + (a.seqs.cu[i + 1] - a.seqs.cu[i] + kFaQ - 1) / kFaQ;
+    if (b.tiles_cu[a.seqs.n] == 0) return hipSuccess;
+    hipLaunchKernelGGL(attn_full_mfma_kernel, dim3(b.tiles_cu[a.seqs.n], a.n_head), dim3(kFaWaves * 64), 0, st, b);
     return hipGetLastError();
 }
 

@@ -846,6 +846,8 @@ int ftts_prefill_ids(const ftts_weights* w, const void* cond_emb, const int32_t*
 
 // ---- flow-matching DiT step -------------------------------------------------------------
 
+static_assert(2 * FTTS_DIT_MAX_BATCH <= kMaxPrefillSeqs, "both guidance branches of every utterance need a sequence");
+
 namespace {
 
 struct DitWs {
@@ -973,11 +975,20 @@ size_t ftts_dit_workspace_bytes(const ftts_dit_config* cfg, int32_t max_frames) 
     return dit_bytes(*cfg, max_frames, nullptr, nullptr);
 }
 
-int ftts_dit_step(const ftts_dit_weights* w, const float* x, const void* cond, int32_t T, float t, float dt,
-                  float cfg_w, float* x_out, float* v_out, void* ws, size_t ws_bytes, void* stream) {
+int ftts_dit_step(const ftts_dit_weights* w, const float* x, const void* cond, const int32_t* lens, int32_t B,
+                  float t, float dt, float cfg_w, float* x_out, float* v_out, void* ws, size_t ws_bytes,
+                  void* stream) {
     TRY(check_dit_weights(w));
     const ftts_dit_config& c = w->cfg;
-    if (T < 1 || T > (1 << 20)) return fail(FTTS_E_SHAPE, "T must be in [1, 2^20] (got %d)", T);
+    if (B < 1 || B > FTTS_DIT_MAX_BATCH) return fail(FTTS_E_SHAPE, "B must be in [1, %d]", FTTS_DIT_MAX_BATCH);
+    if (!lens) return fail(FTTS_E_INVALID_ARG, "lens is NULL");
+    int64_t total = 0;
+    for (int b = 0; b < B; ++b) {
+        if (lens[b] < 1) return fail(FTTS_E_SHAPE, "lens[%d] = %d must be >= 1", b, lens[b]);
+        total += lens[b];
+        if (total > (1 << 20)) return fail(FTTS_E_SHAPE, "more than 2^20 frames in one step");
+    }
+    const int T = (int)total;  // frames of the whole batch
     if (!std::isfinite(t) || !std::isfinite(dt) || !std::isfinite(cfg_w))
         return fail(FTTS_E_RANGE, "t, dt and cfg_w must be finite");
     TRY(check_ptr(x, "x"));
@@ -1020,14 +1031,13 @@ int ftts_dit_step(const ftts_dit_weights* w, const float* x, const void* cond, i
     ap.o = W.a;
     ap.d_model = d;
     ap.n_head = c.n_head;
-    ap.seqs.n = 2;
+    // 2B sequences: the conditional rows of every utterance, then the unconditional ones
+    ap.seqs.n = 2 * B;
     ap.seqs.cu[0] = 0;
-    ap.seqs.cu[1] = T;
-    ap.seqs.cu[2] = M;
-    const int qt = (T + prefill_tile_rows(FTTS_BF16) - 1) / prefill_tile_rows(FTTS_BF16);
-    ap.tiles_cu[0] = 0;
-    ap.tiles_cu[1] = qt;
-    ap.tiles_cu[2] = 2 * qt;
+    for (int b = 0; b < B; ++b) {
+        ap.seqs.cu[b + 1] = ap.seqs.cu[b] + lens[b];
+        ap.seqs.cu[B + b + 1] = T + ap.seqs.cu[b + 1];
+    }
 
     for (int l = 0; l < c.n_layer; ++l) {
         const ftts_layer& L = w->layers[l];
@@ -1035,7 +1045,7 @@ int ftts_dit_step(const ftts_dit_weights* w, const float* x, const void* cond, i
             return hip_fail(e, "ln1");
         if ((e = launch_gemm(FTTS_BF16, EPI_STORE, dit_gemm(L.qkv, W.a, M, 3 * d, d, W.qkv, W), st)) != hipSuccess)
             return hip_fail(e, "qkv gemm");
-        if ((e = launch_attn_full_bf16(ap, ap.tiles_cu[2], st)) != hipSuccess) return hip_fail(e, "attention");
+        if ((e = launch_attn_full_bf16(ap, st)) != hipSuccess) return hip_fail(e, "attention");
         if ((e = launch_gemm(FTTS_BF16, EPI_RESID, dit_gemm(L.out, W.a, M, d, d, W.h, W), st)) != hipSuccess)
             return hip_fail(e, "out gemm");
         if ((e = launch_ln_rows(FTTS_BF16, W.h, L.ln2_g, L.ln2_b, c.ln_eps, M, d, W.a, st)) != hipSuccess)

@@ -281,9 +281,9 @@ hipError_t launch_ln_rows(int wdtype, const float* x, const void* g, const void*
 hipError_t launch_gemm(int wdtype, int epi, const GemmArgs& a, hipStream_t st);
 hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_tiles, hipStream_t st);
 int prefill_tile_rows(int wdtype);  // queries per prefill-attention workgroup
-// Attention without a mask (every query sees every key of its sequence), bf16 rows of
-// prefill_tile_rows(FTTS_BF16) queries per workgroup.
-hipError_t launch_attn_full_bf16(const AttnPrefillArgs& a, int total_tiles, hipStream_t st);
+// Attention without a mask (every query sees every key of its sequence), bf16; the
+// launcher sets its own query tiling (tiles_cu of `a` is ignored).
+hipError_t launch_attn_full_bf16(const AttnPrefillArgs& a, hipStream_t st);
 hipError_t launch_gather_rows(const float* x, int d, const SeqTable& seqs, float* out, hipStream_t st);
 hipError_t launch_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled,
                           int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,

@@ -118,7 +118,8 @@ def lib():
         L.ftts_dit_workspace_bytes.restype = _c.c_size_t
         L.ftts_dit_workspace_bytes.argtypes = [P(DitConfig), i32]
         L.ftts_dit_step.restype = _c.c_int
-        L.ftts_dit_step.argtypes = [P(DitWeights), vp, vp, i32, f32, f32, f32, vp, vp, vp, _c.c_size_t, vp]
+        L.ftts_dit_step.argtypes = [P(DitWeights), vp, vp, P(i32), i32, f32, f32, f32, vp, vp, vp, _c.c_size_t,
+                                    vp]
         _lib = L
     return _lib
 
@@ -398,11 +399,13 @@ def dit_workspace_bytes(cfg: DitConfig, max_frames: int) -> int:
     return n
 
 
-def dit_step(model, x, cond, t: float, dt: float, cfg_w: float, x_out, v_out, ws, stream=None):
-    """One guided Euler step over the T frames of x (ftts_dit_step)."""
-    T = x.shape[0]
-    _check(lib().ftts_dit_step(_c.byref(model.c), _ptr(x), _ptr(cond), T, t, dt, cfg_w, _ptr(x_out), _ptr(v_out),
-                               _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+def dit_step(model, x, cond, t: float, dt: float, cfg_w: float, x_out, v_out, ws, lens=None, stream=None):
+    """One guided Euler step (ftts_dit_step) over the utterances packed in x, of
+    `lens` frames each (default: one utterance of all of x's rows)."""
+    lens = [x.shape[0]] if lens is None else list(lens)
+    arr = (i32 * max(len(lens), 1))(*lens)
+    _check(lib().ftts_dit_step(_c.byref(model.c), _ptr(x), _ptr(cond), arr, len(lens), t, dt, cfg_w, _ptr(x_out),
+                               _ptr(v_out), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 class DitDeviceModel:

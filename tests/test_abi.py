@@ -204,8 +204,11 @@ def _fake_dit(shape):
     return w
 
 
-def _dit_step(w, T=8, t=0.5, ws_bytes=1 << 30, x=FAKE, x_out=FAKE, cond=FAKE):
-    return ftts.lib().ftts_dit_step(ctypes.byref(w), x, cond, T, t, 0.1, 1.0, x_out, None, FAKE, ws_bytes, None)
+def _dit_step(w, T=8, t=0.5, ws_bytes=1 << 30, x=FAKE, x_out=FAKE, cond=FAKE, lens=None):
+    lens = [T] if lens is None else lens
+    arr = (ctypes.c_int32 * max(len(lens), 1))(*lens)
+    return ftts.lib().ftts_dit_step(ctypes.byref(w), x, cond, arr, len(lens), t, 0.1, 1.0, x_out, None, FAKE,
+                                    ws_bytes, None)
 
 
 def test_dit_workspace_bytes():
@@ -228,6 +231,11 @@ def test_dit_step_argument_errors():
     w = _fake_dit(workload.DIT_TINY)
     L = ftts.lib()
     assert _dit_step(w, T=0) == -2
+    assert _dit_step(w, lens=[]) == -2
+    assert _dit_step(w, lens=[4] * 33) == -2
+    assert _dit_step(w, lens=[4, 0, 4]) == -2
+    need = ftts.dit_workspace_bytes(w.cfg, 4 + 9 + 30)
+    assert _dit_step(w, lens=[4, 9, 30], ws_bytes=need - 1) == -8
     assert _dit_step(w, t=float("inf")) == -5
     assert _dit_step(w, x=None) == -1
     assert _dit_step(w, x_out=FAKE + 8) == -4

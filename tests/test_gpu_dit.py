@@ -65,10 +65,11 @@ def check(v, v_ref, label):
     assert ok, (label, rel, err)
 
 
-@pytest.mark.parametrize("T", [1, 37, 300])
+@pytest.mark.parametrize("T", [1, 37, 97, 300])
 def test_dit_step_tiny(torch_cuda, T):
-    """Two blocks of width 256: one frame, a ragged single tile and three
-    attention tiles (128 queries each) with a ragged tail."""
+    """Two blocks of width 256.  Attention works in 32-key tiles split over 4
+    waves: one frame (3 waves idle), two tiles, four tiles with a single key in
+    the last, and ten tiles with a ragged tail (waves with 2 and 3 tiles)."""
     xo, vo, x_ref, v_ref, x = run_step(torch_cuda, workload.DIT_TINY, T, 0.3, 0.04, 1.7, seed=21 + T)
     check(vo, v_ref, f"v T={T}")
     # x' - x = dt v: compare the update itself through the velocity's bar
@@ -102,6 +103,39 @@ def test_dit_step_96m(torch_cuda):
     xo, vo, x_ref, v_ref, x = run_step(torch_cuda, workload.DIT_96M, 500, 0.64, 0.04, 2.0, seed=31)
     check(vo, v_ref, "v 96M T=500")
     check((xo.astype(np.float64) - x) / 0.04, (x_ref - x) / 0.04, "(x'-x)/dt 96M")
+
+
+def run_batch(torch, shape, lens, t, dt, cfg_w, seed):
+    """One call over several packed utterances; each checked against its own oracle step."""
+    from paper_2607_21042_amd import ftts
+    dm, ora = device_model(torch, shape)
+    parts = [workload.dit_inputs(shape, n, seed=seed + i) for i, n in enumerate(lens)]
+    x = np.concatenate([p[0] for p in parts])
+    cond = np.concatenate([p[1] for p in parts])
+    xg = torch.from_numpy(x).cuda()
+    cg = torch.from_numpy(cond).cuda().to(torch.bfloat16)
+    xo, vo = torch.empty_like(xg), torch.empty_like(xg)
+    ws = torch.empty(ftts.dit_workspace_bytes(dm.cfg, int(sum(lens))), dtype=torch.uint8, device="cuda")
+    say(f"dit batch: lens={lens} d={shape.d_model} layers={shape.n_layer} t={t} dt={dt} w={cfg_w}")
+    ftts.dit_step(dm, xg, cg, t, dt, cfg_w, xo, vo, ws, lens=lens)
+    torch.cuda.synchronize()
+    vo = vo.cpu().numpy()
+    off = 0
+    for i, (n, (xi, ci)) in enumerate(zip(lens, parts)):
+        _, v_ref = ora.step(xi, ci, t, dt, cfg_w)
+        check(vo[off:off + n], v_ref, f"utterance {i} ({n} frames)")
+        off += n
+
+
+def test_dit_step_batch_tiny(torch_cuda):
+    """Utterances attend only to their own frames: a batch of four lengths (one
+    of a single frame) matches four separate oracle steps."""
+    run_batch(torch_cuda, workload.DIT_TINY, [37, 1, 130, 64], 0.45, 0.05, 1.6, seed=40)
+
+
+def test_dit_step_batch_96m(torch_cuda):
+    """Two utterances of the 96M shape in one step."""
+    run_batch(torch_cuda, workload.DIT_96M, [431, 257], 0.2, 0.04, 1.7, seed=50)
 
 
 def test_dit_step_rejects_bad_calls(torch_cuda):
