@@ -551,6 +551,13 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const 
 // into registers.  The four (max, sum, output) partials are merged by the
 // log-sum-exp rule through LDS at the end.
 constexpr int kFaWaves = 4, kFaQ = 32, kFaK = 32;
+typedef __bf16 fa_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float fa_f32x2 __attribute__((ext_vector_type(2)));
+
+// Two floats to packed bf16 (round to nearest even, one instruction).
+__device__ __forceinline__ uint32_t fa_pack_bf16(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((fa_f32x2){lo, hi}, fa_bf16x2));
+}
 
 __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -558,7 +565,7 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__global__ __launch_bounds__(kFaWaves * 64) void attn_full_mfma_kernel(const AttnPrefillArgs a) {
+__global__ __launch_bounds__(kFaWaves * 64, 3) void attn_full_mfma_kernel(const AttnPrefillArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t vt[kFaWaves][kHeadDim][kVtStride];
     __shared__ float mrg[kFaWaves - 1][34][64];  // waves 1..3: 32 output values, max, sum per lane
     const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -642,26 +649,31 @@ __global__ __launch_bounds__(kFaWaves * 64) void attn_full_mfma_kernel(const Att
             tmax = fmaxf(pr.a, pr.b);
         }
         const float mn = fmaxf(m, tmax);  // finite: key k0 < len is in this tile
-        const float alpha = exp2f(m - mn);
-        m = mn;
+        // probabilities (arguments <= 0; the hardware exp2 flushes results below 2^-126 to 0),
+        // rounded to bf16 once: the same values feed P V and the row sum
         uint32_t pw[8];
         float rs = 0.f;
 #pragma unroll
         for (int i = 0; i < 16; i += 2) {
-            const uint16_t lo = f32_to_bf16(exp2f(s[i] - mn)), hi = f32_to_bf16(exp2f(s[i + 1] - mn));
-            rs += bf16_to_f32(lo) + bf16_to_f32(hi);
-            pw[i / 2] = (uint32_t)lo | ((uint32_t)hi << 16);
+            pw[i / 2] = fa_pack_bf16(__builtin_amdgcn_exp2f(s[i] - mn), __builtin_amdgcn_exp2f(s[i + 1] - mn));
+            rs += __uint_as_float(pw[i / 2] << 16) + __uint_as_float(pw[i / 2] & 0xFFFF0000u);
         }
         {
             const RowPair pr = swap32(rs);
             rs = pr.a + pr.b;
         }
-        l = l * alpha + rs;
+        // rescale the running sums only when some lane's maximum grew (alpha = 1 elsewhere)
+        if (__any(mn > m)) {
+            const float alpha = __builtin_amdgcn_exp2f(m - mn);  // m = -inf on the first tile: 0
+            l *= alpha;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            o0[i] *= alpha;
-            o1[i] *= alpha;
+            for (int i = 0; i < 16; ++i) {
+                o0[i] *= alpha;
+                o1[i] *= alpha;
+            }
         }
+        m = mn;
+        l += rs;
         wave_lds_sync();  // the V^T words of every lane are in LDS
 #pragma unroll
         for (int st2 = 0; st2 < 2; ++st2) {

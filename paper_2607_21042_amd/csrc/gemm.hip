@@ -678,7 +678,7 @@ static hipError_t mfma_by_epi(int epi, const GemmArgs& a, dim3 g, hipStream_t st
 GemmPlan gemm_plan(int M, int N, int K) {
     GemmPlan p{};
     const int tn = (N + G2N - 1) / G2N;
-    p.mt = (M + 127) / 128 * tn >= 512 ? 2 : 1;
+    p.mt = (M + 127) / 128 * tn >= 256 ? 2 : 1;
     const int bm = 64 * p.mt;
     p.tiles_m = (M + bm - 1) / bm;
     p.tiles_n = tn;
