@@ -154,3 +154,42 @@ def test_dit_step_rejects_bad_calls(torch_cuda):
         ftts.dit_step(dm, x[:0], c[:0], 0.1, 0.1, 1.0, x[:0], None, ws)
     with pytest.raises(ftts.FTTSError):
         ftts.dit_step(dm, x, c, float("nan"), 0.1, 1.0, x, None, ws)
+
+
+def test_dit_steps_replay_from_a_graph(torch_cuda):
+    """Three Euler steps captured into one HIP graph: every replay (with eager
+    work and synchronisations between them) equals the eager steps bit for bit
+    (fixed split-K summation order; the step clears its scratch with kernels)."""
+    import torch
+    from paper_2607_21042_amd import ftts
+    sh = workload.DIT_TINY
+    dm, _ = device_model(torch, sh)
+    lens = [70, 33]
+    x0_np, cond_np = workload.dit_inputs(sh, sum(lens), seed=60)
+    x0 = torch.from_numpy(x0_np).cuda()
+    cond = torch.from_numpy(cond_np).cuda().to(torch.bfloat16)
+    ws = torch.empty(ftts.dit_workspace_bytes(dm.cfg, sum(lens)), dtype=torch.uint8, device="cuda")
+    x = torch.empty_like(x0)
+
+    def solve():
+        x.copy_(x0)
+        for k in range(3):
+            ftts.dit_step(dm, x, cond, 0.1 + 0.2 * k, 0.2, 1.5, x, None, ws, lens=lens)
+
+    say("dit graph: eager reference")
+    solve()
+    torch.cuda.synchronize()
+    ref = x.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        solve()
+    for r in range(3):
+        x.fill_(float("nan"))
+        torch.cuda.synchronize()
+        say(f"dit graph: replay {r}")
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(x, ref), r
+        solve()  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(x, ref)
