@@ -637,25 +637,29 @@ __global__ __launch_bounds__(kFaWaves * 64, 3) void attn_full_mfma_kernel(const 
         for (int i = 0; i < 16; ++i) s[i] = 0.f;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(kc[kk]), pf_op(qr[kk]), s, 0, 0, 0);
-        float tmax = -INFINITY;
+        // raw scores; keys past the end exist only in a sequence's last tile
+        if (k0 + kFaK > len) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int key = k0 + (i >> 2) * 8 + hh * 4 + (i & 3);
-            s[i] = key < len ? s[i] * kScale : -INFINITY;
-            tmax = fmaxf(tmax, s[i]);
+            for (int i = 0; i < 16; ++i)
+                if (k0 + (i >> 2) * 8 + hh * 4 + (i & 3) >= len) s[i] = -INFINITY;
         }
+        float tmax = s[0];
+#pragma unroll
+        for (int i = 1; i < 16; ++i) tmax = fmaxf(tmax, s[i]);
         {
             const RowPair pr = swap32(tmax);
             tmax = fmaxf(pr.a, pr.b);
         }
-        const float mn = fmaxf(m, tmax);  // finite: key k0 < len is in this tile
-        // probabilities (arguments <= 0; the hardware exp2 flushes results below 2^-126 to 0),
-        // rounded to bf16 once: the same values feed P V and the row sum
+        const float mn = fmaxf(m, tmax * kScale);  // finite: key k0 < len is in this tile
+        // probabilities exp2(s * scale - max) (arguments <= 0; the hardware exp2 flushes
+        // results below 2^-126 to 0), rounded to bf16 once: the same values feed P V
+        // and the row sum
         uint32_t pw[8];
         float rs = 0.f;
 #pragma unroll
         for (int i = 0; i < 16; i += 2) {
-            pw[i / 2] = fa_pack_bf16(__builtin_amdgcn_exp2f(s[i] - mn), __builtin_amdgcn_exp2f(s[i + 1] - mn));
+            pw[i / 2] = fa_pack_bf16(__builtin_amdgcn_exp2f(fmaf(s[i], kScale, -mn)),
+                                     __builtin_amdgcn_exp2f(fmaf(s[i + 1], kScale, -mn)));
             rs += __uint_as_float(pw[i / 2] << 16) + __uint_as_float(pw[i / 2] & 0xFFFF0000u);
         }
         {
