@@ -25,8 +25,9 @@
 // thread per query row streams 64-key tiles of K and V through LDS.
 //
 // Full attention (no mask: the flow-matching DiT's frames all see each other)
-// has its own matrix-core kernel, attn_full_mfma_kernel, which splits the keys
-// of a query tile over the waves of a workgroup.
+// has two matrix-core kernels: attn_full_mfma_kernel splits the keys of a
+// 32-query tile over the waves of a workgroup (short grids), and
+// attn_full_shared_kernel shares each K and V tile among 128 queries (wide grids).
 #include "kv_page.hpp"
 
 namespace ftts {
@@ -541,15 +542,15 @@ __global__ __launch_bounds__(kPfWaves * 64) void attn_prefill_mfma_kernel(const 
     }
 }
 
-// Attention without a mask (every query sees every key of its sequence), bf16.
-// A workgroup takes 32 queries of one head; its 4 waves split the 32-key tiles
-// round-robin (wave w takes tiles w, w + 4, ...), so a sequence of L keys keeps
-// ceil(L / 32) * 4 waves busy per head and each wave's dependent chain is a
-// quarter of the keys.  Every wave forms S^T = K Q^T and O^T = V^T P^T as in the
-// prefill kernel, transposes its own V tile through a private LDS slice (no
-// workgroup barrier in the loop) and prefetches the next tile's K and V rows
-// into registers.  The four (max, sum, output) partials are merged by the
-// log-sum-exp rule through LDS at the end.
+// Attention without a mask (every query sees every key of its sequence), bf16,
+// for short grids.  A workgroup takes 32 queries of one head; its 4 waves split
+// the 32-key tiles round-robin (wave w takes tiles w, w + 4, ...), so a
+// sequence of L keys keeps ceil(L / 32) * 4 waves busy per head and each wave's
+// dependent chain is a quarter of the keys.  Every wave forms S^T = K Q^T and
+// O^T = V^T P^T as in the prefill kernel, transposes its own V tile through a
+// private LDS slice (no workgroup barrier in the loop) and prefetches the next
+// tile's K and V rows into registers.  The four (max, sum, output) partials are
+// merged by the log-sum-exp rule through LDS at the end.
 constexpr int kFaWaves = 4, kFaQ = 32, kFaK = 32;
 typedef __bf16 fa_bf16x2 __attribute__((ext_vector_type(2)));
 typedef float fa_f32x2 __attribute__((ext_vector_type(2)));
@@ -740,6 +741,136 @@ __global__ __launch_bounds__(kFaWaves * 64, 3) void attn_full_mfma_kernel(const 
     }
 }
 
+// The same attention for wide grids: the 4 waves of a workgroup take 128
+// consecutive queries (32 each) and share every 32-key tile, which all 256
+// threads stage once into double-buffered LDS (K as rows, V transposed), one
+// workgroup barrier per tile.  Each K and V row is read from L2 once per 128
+// queries instead of once per 32, the bound of the per-wave kernel above.
+constexpr int kFsK = kHeadDim + 8;  // bf16 per K row in LDS (16-byte aligned, staggered banks)
+
+__global__ __launch_bounds__(kFaWaves * 64, 2) void attn_full_shared_kernel(const AttnPrefillArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t ks[2][kFaK][kFsK];
+    __shared__ __attribute__((aligned(16))) uint16_t vs[2][kHeadDim][kVtStride];
+    const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int gt = blockIdx.x, sq = 0;
+    while (sq + 1 < a.seqs.n && a.tiles_cu[sq + 1] <= gt) ++sq;
+    const int tile = gt - a.tiles_cu[sq];
+    const int row0 = a.seqs.cu[sq], len = a.seqs.cu[sq + 1] - row0;
+    if (len <= 0) return;  // uniform over the workgroup
+    const size_t ld = 3 * (size_t)a.d_model;
+    const uint16_t* qkv = reinterpret_cast<const uint16_t*>(a.qkv);
+    const int ql = lane & 31, hh = lane >> 5;
+    const int qi = tile * (kFaWaves * kFaQ) + wave * kFaQ + ql;  // past len: computed, not stored
+    const float kScale = 0.125f * 1.44269504088896340736f;
+
+    uint4 qr[4];
+    {
+        const uint16_t* qrow = qkv + (size_t)(row0 + min(qi, len - 1)) * ld + h * kHeadDim;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qr[kk] = *reinterpret_cast<const uint4*>(qrow + kk * 16 + hh * 8);
+    }
+    // staging: thread t carries key t / 8, dims (t % 8) * 8 .. +7 of both K and V
+    const int skey = tid >> 3, sd0 = (tid & 7) * 8;
+    auto load_kv = [&](int t, uint4& kv, uint4& vv) {
+        const uint16_t* r = qkv + (size_t)(row0 + min(t * kFaK + skey, len - 1)) * ld + h * kHeadDim + sd0;
+        kv = *reinterpret_cast<const uint4*>(r + a.d_model);
+        vv = *reinterpret_cast<const uint4*>(r + 2 * a.d_model);
+    };
+    auto store_kv = [&](const uint4& kv, const uint4& vv, int buf) {
+        *reinterpret_cast<uint4*>(&ks[buf][skey][sd0]) = kv;
+        const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            vs[buf][sd0 + 2 * i][skey] = (uint16_t)(w[i] & 0xFFFFu);
+            vs[buf][sd0 + 2 * i + 1][skey] = (uint16_t)(w[i] >> 16);
+        }
+    };
+    const int nt = (len + kFaK - 1) / kFaK;
+    pf_f32x16 o0, o1;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o0[i] = o1[i] = 0.f;
+    float m = -INFINITY, l = 0.f;
+    {
+        uint4 kv, vv;
+        load_kv(0, kv, vv);
+        store_kv(kv, vv, 0);
+    }
+    __syncthreads();
+    for (int t = 0; t < nt; ++t) {
+        const int buf = t & 1, k0 = t * kFaK;
+        uint4 kn = make_uint4(0, 0, 0, 0), vn = make_uint4(0, 0, 0, 0);
+        if (t + 1 < nt) load_kv(t + 1, kn, vn);  // in flight during this tile
+        uint4 kc[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) kc[kk] = *reinterpret_cast<const uint4*>(&ks[buf][ql][kk * 16 + hh * 8]);
+        pf_f32x16 s;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s[i] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(kc[kk]), pf_op(qr[kk]), s, 0, 0, 0);
+        if (k0 + kFaK > len) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+                if (k0 + (i >> 2) * 8 + hh * 4 + (i & 3) >= len) s[i] = -INFINITY;
+        }
+        float tmax = s[0];
+#pragma unroll
+        for (int i = 1; i < 16; ++i) tmax = fmaxf(tmax, s[i]);
+        {
+            const RowPair pr = swap32(tmax);
+            tmax = fmaxf(pr.a, pr.b);
+        }
+        const float mn = fmaxf(m, tmax * kScale);
+        uint32_t pw[8];
+        float rs = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; i += 2) {
+            pw[i / 2] = fa_pack_bf16(__builtin_amdgcn_exp2f(fmaf(s[i], kScale, -mn)),
+                                     __builtin_amdgcn_exp2f(fmaf(s[i + 1], kScale, -mn)));
+            rs += __uint_as_float(pw[i / 2] << 16) + __uint_as_float(pw[i / 2] & 0xFFFF0000u);
+        }
+        {
+            const RowPair pr = swap32(rs);
+            rs = pr.a + pr.b;
+        }
+        if (__any(mn > m)) {
+            const float alpha = __builtin_amdgcn_exp2f(m - mn);
+            l *= alpha;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                o0[i] *= alpha;
+                o1[i] *= alpha;
+            }
+        }
+        m = mn;
+        l += rs;
+#pragma unroll
+        for (int st2 = 0; st2 < 2; ++st2) {
+            const pf_bf16x8 pb = pf_op(make_uint4(pw[4 * st2], pw[4 * st2 + 1], pw[4 * st2 + 2], pw[4 * st2 + 3]));
+            const int c = st2 * 16 + hh * 4;
+            const uint2 a0 = *reinterpret_cast<const uint2*>(&vs[buf][ql][c]);
+            const uint2 a1 = *reinterpret_cast<const uint2*>(&vs[buf][ql][c + 8]);
+            const uint2 b0 = *reinterpret_cast<const uint2*>(&vs[buf][32 + ql][c]);
+            const uint2 b1 = *reinterpret_cast<const uint2*>(&vs[buf][32 + ql][c + 8]);
+            o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(make_uint4(a0.x, a0.y, a1.x, a1.y)), pb, o0, 0, 0, 0);
+            o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(make_uint4(b0.x, b0.y, b1.x, b1.y)), pb, o1, 0, 0, 0);
+        }
+        if (t + 1 < nt) store_kv(kn, vn, buf ^ 1);  // that buffer was last read before the previous barrier
+        __syncthreads();
+    }
+    if (qi >= len) return;
+    const float inv = 1.0f / l;
+    uint16_t* orow = reinterpret_cast<uint16_t*>(a.o) + (size_t)(row0 + qi) * a.d_model + h * kHeadDim;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const int dd = g * 8 + hh * 4;
+        *reinterpret_cast<uint2*>(orow + dd) = make_uint2(fa_pack_bf16(o0[4 * g] * inv, o0[4 * g + 1] * inv),
+                                                          fa_pack_bf16(o0[4 * g + 2] * inv, o0[4 * g + 3] * inv));
+        *reinterpret_cast<uint2*>(orow + 32 + dd) = make_uint2(fa_pack_bf16(o1[4 * g] * inv, o1[4 * g + 1] * inv),
+                                                               fa_pack_bf16(o1[4 * g + 2] * inv, o1[4 * g + 3] * inv));
+    }
+}
+
 int prefill_tile_rows(int wdtype) { return wdtype == FTTS_F32 ? 64 : kPfQ; }
 
 hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_tiles, hipStream_t st) {
@@ -750,12 +881,24 @@ hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_t
 }
 
 hipError_t launch_attn_full_bf16(const AttnPrefillArgs& a, hipStream_t st) {
-    AttnPrefillArgs b = a;  // query tiles of this kernel's size
-    b.tiles_cu[0] = 0;
-    for (int i = 0; i < a.seqs.n; ++i)
-        b.tiles_cu[i + 1] = b.tiles_cu[i] + (a.seqs.cu[i + 1] - a.seqs.cu[i] + kFaQ - 1) / kFaQ;
-    if (b.tiles_cu[a.seqs.n] == 0) return hipSuccess;
-    hipLaunchKernelGGL(attn_full_mfma_kernel, dim3(b.tiles_cu[a.seqs.n], a.n_head), dim3(kFaWaves * 64), 0, st, b);
+    // 128-query tiles sharing K and V once they give at least one workgroup per
+    // compute unit, else 32-query tiles with the keys split over the waves
+    constexpr int kFillGroups = 256;
+    AttnPrefillArgs b = a;
+    auto tiles = [&](int q) {
+        b.tiles_cu[0] = 0;
+        for (int i = 0; i < a.seqs.n; ++i)
+            b.tiles_cu[i + 1] = b.tiles_cu[i] + (a.seqs.cu[i + 1] - a.seqs.cu[i] + q - 1) / q;
+        return b.tiles_cu[a.seqs.n];
+    };
+    const int t128 = tiles(kFaWaves * kFaQ);
+    if (t128 == 0) return hipSuccess;
+    if ((long)t128 * a.n_head >= kFillGroups) {
+        hipLaunchKernelGGL(attn_full_shared_kernel, dim3(t128, a.n_head), dim3(kFaWaves * 64), 0, st, b);
+    } else {
+        const int t32 = tiles(kFaQ);
+        hipLaunchKernelGGL(attn_full_mfma_kernel, dim3(t32, a.n_head), dim3(kFaWaves * 64), 0, st, b);
+    }
     return hipGetLastError();
 }
 

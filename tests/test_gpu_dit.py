@@ -133,6 +133,14 @@ def test_dit_step_batch_tiny(torch_cuda):
     run_batch(torch_cuda, workload.DIT_TINY, [37, 1, 130, 64], 0.45, 0.05, 1.6, seed=40)
 
 
+def test_dit_step_batch_wide_grid(torch_cuda):
+    """32 utterances of 257-400 frames: enough 128-query tiles (>= 256 with the
+    heads) that the attention shares each K and V tile among 128 queries instead
+    of splitting the keys over waves; ragged lengths in every tile position."""
+    lens = [257 + (37 * i) % 144 for i in range(32)]
+    run_batch(torch_cuda, workload.DIT_TINY, lens, 0.7, 0.03, 1.3, seed=70)
+
+
 def test_dit_step_batch_96m(torch_cuda):
     """Two utterances of the 96M shape in one step."""
     run_batch(torch_cuda, workload.DIT_96M, [431, 257], 0.2, 0.04, 1.7, seed=50)
