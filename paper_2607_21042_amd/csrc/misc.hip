@@ -118,10 +118,27 @@ __global__ __launch_bounds__(256) void ln_rows_wave_kernel(const float* x, const
         const int j = lane + 64 * i;
         if (j < n4) {
             const float xs[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+            if constexpr (F32) {
 #pragma unroll
-            for (int k = 0; k < 4; ++k)
-                st_act<F32>(out, (size_t)r * d + 4 * j + k,
-                            (xs[k] - mean) * rstd * ld_act<F32>(g, 4 * j + k) + ld_act<F32>(bb, 4 * j + k));
+                for (int k = 0; k < 4; ++k)
+                    st_act<F32>(out, (size_t)r * d + 4 * j + k,
+                                (xs[k] - mean) * rstd * ld_act<F32>(g, 4 * j + k) + ld_act<F32>(bb, 4 * j + k));
+            } else {
+                // four bf16 gains, biases and outputs per 8-byte access (rows of d % 4 == 0)
+                const uint2 gw = reinterpret_cast<const uint2*>(g)[j];
+                const uint2 bw = reinterpret_cast<const uint2*>(bb)[j];
+                const uint32_t gs[2] = {gw.x, gw.y}, bs[2] = {bw.x, bw.y};
+                uint32_t o[2];
+#pragma unroll
+                for (int k = 0; k < 2; ++k) {
+                    const float y0 = (xs[2 * k] - mean) * rstd * __uint_as_float(gs[k] << 16) +
+                                     __uint_as_float(bs[k] << 16);
+                    const float y1 = (xs[2 * k + 1] - mean) * rstd * __uint_as_float(gs[k] & 0xFFFF0000u) +
+                                     __uint_as_float(bs[k] & 0xFFFF0000u);
+                    o[k] = (uint32_t)f32_to_bf16(y0) | ((uint32_t)f32_to_bf16(y1) << 16);
+                }
+                reinterpret_cast<uint2*>(out)[((size_t)r * d) / 4 + j] = make_uint2(o[0], o[1]);
+            }
         }
     }
 }
