@@ -63,33 +63,30 @@ __global__ __launch_bounds__(256) void dit_time_out_kernel(const void* w2, const
     if (lane == 0) e[r] = y;
 }
 
-// One flat index space over the four things the step starts from:
-//   [0, M*Kin)          input row m: x[m mod T] (bf16), then cond[m] or zeros
-//   [.., + M*D)         h[m][j] = e[j]
-//   [.., + M*n_mel)     velocity accumulator <- 0
-//   [.., + n_count)     split-K arrival counters <- 0
+// The four things the step starts from, one row of each per loop iteration
+// (rows m of the 2T-row batch; columns strided over the workgroup):
+//   input row m: x[m mod T] (bf16), then cond[m] or zeros
+//   h[m][j] = e[j]
+//   velocity accumulator row m <- 0
+// and the split-K arrival counters <- 0 (first workgroup).
 __global__ __launch_bounds__(256) void dit_prepare_kernel(const DitPrepareArgs a) {
     const int M = 2 * a.T, Kin = a.n_mel + a.d_cond;
-    const size_t n_in = (size_t)M * Kin, n_h = (size_t)M * a.d_model, n_v = (size_t)M * a.n_mel;
-    const size_t total = n_in + n_h + n_v + a.n_count;
     uint16_t* inp = reinterpret_cast<uint16_t*>(a.inp);
     const uint16_t* cond = reinterpret_cast<const uint16_t*>(a.cond);
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
-        if (i < n_in) {
-            const int m = (int)(i / Kin), c = (int)(i % Kin);
-            const int f = m < a.T ? m : m - a.T;  // frame of this row
-            uint16_t v;
-            if (c < a.n_mel) v = f32_to_bf16(a.x[(size_t)f * a.n_mel + c]);
-            else v = m < a.T ? cond[(size_t)f * a.d_cond + (c - a.n_mel)] : (uint16_t)0;
-            inp[i] = v;
-        } else if (i < n_in + n_h) {
-            const size_t k = i - n_in;
-            a.h[k] = a.e[k % a.d_model];
-        } else if (i < n_in + n_h + n_v) {
-            a.vel[i - n_in - n_h] = 0.f;
-        } else {
-            a.count[i - n_in - n_h - n_v] = 0u;
-        }
+    if (blockIdx.x == 0)
+        for (size_t i = threadIdx.x; i < a.n_count; i += blockDim.x) a.count[i] = 0u;
+    for (int m = blockIdx.x; m < M; m += gridDim.x) {
+        const bool guided = m < a.T;
+        const int f = guided ? m : m - a.T;  // frame of this row
+        const float* xr = a.x + (size_t)f * a.n_mel;
+        const uint16_t* cr = cond + (size_t)f * a.d_cond;
+        uint16_t* ir = inp + (size_t)m * Kin;
+        for (int c = threadIdx.x; c < a.n_mel; c += blockDim.x) ir[c] = f32_to_bf16(xr[c]);
+        for (int c = threadIdx.x; c < a.d_cond; c += blockDim.x) ir[a.n_mel + c] = guided ? cr[c] : (uint16_t)0;
+        float* hr = a.h + (size_t)m * a.d_model;
+        for (int c = threadIdx.x; c < a.d_model; c += blockDim.x) hr[c] = a.e[c];
+        float* vr = a.vel + (size_t)m * a.n_mel;
+        for (int c = threadIdx.x; c < a.n_mel; c += blockDim.x) vr[c] = 0.f;
     }
 }
 
@@ -122,9 +119,8 @@ hipError_t launch_dit_time(float t, const void* w1, const void* b1, const void* 
 }
 
 hipError_t launch_dit_prepare(const DitPrepareArgs& a, hipStream_t st) {
-    const size_t M = 2 * (size_t)a.T;
-    const size_t total = M * (a.n_mel + a.d_cond + a.d_model + a.n_mel) + a.n_count;
-    hipLaunchKernelGGL(dit_prepare_kernel, dim3(flat_grid(total)), dim3(256), 0, st, a);
+    const unsigned rows = 2u * (unsigned)a.T;
+    hipLaunchKernelGGL(dit_prepare_kernel, dim3(std::min(rows, 8192u)), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
