@@ -684,7 +684,9 @@ GemmPlan gemm_plan(int M, int N, int K) {
     p.tiles_n = tn;
     const int tiles = p.tiles_m * p.tiles_n;
     p.splits = 1;
-    if (p.mt == 1 && K % 128 == 0 && tiles > 0 && tiles < 256) {
+    // split K only where each slice keeps enough K steps: below K = 1024 the
+    // partial-tile round trip costs more than the shorter K loop saves
+    if (p.mt == 1 && K % 128 == 0 && K >= 1024 && tiles > 0 && tiles < 256) {
         const int want = (320 + tiles - 1) / tiles, most = K / 256;
         p.splits = std::max(1, std::min(std::min(want, most), kGemmMaxSplits));
     }
