@@ -146,6 +146,32 @@ def test_dit_step_batch_96m(torch_cuda):
     run_batch(torch_cuda, workload.DIT_96M, [431, 257], 0.2, 0.04, 1.7, seed=50)
 
 
+def test_dit_step_without_conditioning(torch_cuda):
+    """d_cond = 0 (cond may be NULL): both guidance branches are the same
+    computation, so the velocity does not depend on the guidance strength.  Also
+    the smallest state width (64 mel bins) and the largest time-feature width
+    (1024)."""
+    import torch
+    from paper_2607_21042_amd import ftts
+    sh = workload.DitShape(n_layer=1, d_model=128, n_head=2, d_head=64, d_ff=256, n_mel=64, d_cond=0, t_dim=1024)
+    w = workload.bf16_weights(workload.dit_master_weights(sh, seed=20))
+    dm = ftts.DitDeviceModel(w, sh)
+    ora = odit.DiT(w, sh.n_head, sh.d_head, dtype=np.float64)
+    x, cond = workload.dit_inputs(sh, 45, seed=3)
+    xg = torch.from_numpy(x).cuda()
+    ws = torch.empty(ftts.dit_workspace_bytes(dm.cfg, 45), dtype=torch.uint8, device="cuda")
+    vs = []
+    for cfg_w in (0.0, 3.0):
+        xo, vo = torch.empty_like(xg), torch.empty_like(xg)
+        say(f"dit step without conditioning: T=45 w={cfg_w}")
+        ftts.dit_step(dm, xg, None, 0.4, 0.1, cfg_w, xo, vo, ws)
+        torch.cuda.synchronize()
+        _, v_ref = ora.step(x, cond, 0.4, 0.1, cfg_w)
+        check(vo.cpu().numpy(), v_ref, f"d_cond=0 w={cfg_w}")
+        vs.append(vo.cpu().numpy())
+    np.testing.assert_allclose(vs[0], vs[1], rtol=0, atol=1e-6)
+
+
 def test_dit_step_rejects_bad_calls(torch_cuda):
     """A workspace too small, no frames or a non-finite time fail before any launch."""
     import torch
