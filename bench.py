@@ -381,12 +381,14 @@ def dit_run(args, torch, ftts, workload):
         with torch.cuda.graph(graph):
             solve()
     for _ in range(args.warmup):
-        graph.replay() if graph else solve()
+        if graph:
+            graph.replay()
+        else:
+            solve()
     torch.cuda.synchronize()
     evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
            for _ in range(args.steps)]
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    stream = torch.cuda.current_stream()
     wall0 = time.perf_counter()
     t0.record(stream)
     for j in range(args.steps):

@@ -1,5 +1,5 @@
 /*
- * ftts.h -- C ABI of the MI355X (gfx950) GPT decode library.
+ * ftts.h -- C ABI of the MI355X (gfx950) IndexTTS-2 inference library.
  *
  * The library runs the autoregressive Text-to-Semantic GPT of IndexTTS-2, a
  * decoder-only GPT-2 style network (Sec. II-A of "Faster IndexTTS-2"), one
@@ -8,7 +8,9 @@
  * token ids and the decoded tokens carry their own position ids, as in the
  * paper's first and third adaptations of the serving engine (Sec. II-C).
  * Linear weights may be bf16 or fp32, or weight-only quantised to W8A16 /
- * W4A16 (Table I caption; Sec. III-B).
+ * W4A16 (Table I caption; Sec. III-B).  It also runs one guided Euler step of
+ * the Semantic-to-Mel flow-matching DiT for a batch of utterances
+ * (ftts_dit_step, at the end of this file).
  *
  * Conventions for every entry point
  * ---------------------------------

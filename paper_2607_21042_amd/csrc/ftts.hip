@@ -1,6 +1,7 @@
 // C ABI entry points of libftts: argument validation, workspace carving and the
-// order of kernel launches for prefill and for one decode step.  Every check
-// happens before the first enqueue, so a rejected call has no side effects.
+// order of kernel launches for prefill, for one decode step and for one guided
+// Euler step of the flow-matching DiT.  Every check happens before the first
+// enqueue, so a rejected call has no side effects.
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
