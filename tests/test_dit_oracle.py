@@ -111,3 +111,13 @@ def test_block_is_the_gpt_block_without_mask():
     mu = ref.mean(axis=1, keepdims=True)
     var = ((ref - mu) ** 2).mean(axis=1, keepdims=True)
     np.testing.assert_allclose(hid, (ref - mu) / np.sqrt(var + 1e-5), rtol=1e-10, atol=1e-12)
+
+
+def test_silu_known_values():
+    """silu(u) = u * sigmoid(u): sigmoid(1) = e / (1 + e) = 0.7310585786300049,
+    silu(-1) = -(1 - sigmoid(1)), silu(0) = 0, and the two tails (u and 0)."""
+    u = np.array([1.0, -1.0, 0.0, 40.0, -40.0])
+    s = odit.silu(u)
+    np.testing.assert_allclose(s[:2], [0.7310585786300049, -0.2689414213699951], rtol=0, atol=1e-15)
+    assert s[2] == 0.0
+    assert abs(s[3] - 40.0) < 1e-12 and abs(s[4]) < 1e-15
