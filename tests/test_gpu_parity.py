@@ -310,12 +310,13 @@ def test_prefill_from_ids(torch_cuda, mode):
         np.testing.assert_array_equal(res["logits"], ref_run["logits"])
 
 
-@pytest.mark.parametrize("mode,B", [("bf16", 33), ("w8a16", 8), ("w4a16", 33)])
+@pytest.mark.parametrize("mode,B", [("bf16", 33), ("w8a16", 8), ("w4a16", 33), ("bf16", 64), ("w4a16", 64)])
 def test_batched_decode_matrix_core_linears(torch_cuda, mode, B):
     """Batches of 8 or more take the MFMA linears (33 = a full group of 32 plus a
-    ragged one): ragged prefixes, sequences retiring at different steps, every
-    logit against the oracle, and bit-identical logits with the pages permuted
-    and from run to run (the split-K sums have a fixed order)."""
+    ragged one; 64, the largest batch, two full groups): ragged prefixes,
+    sequences retiring at different steps, every logit against the oracle, and
+    bit-identical logits with the pages permuted and from run to run (the
+    split-K sums have a fixed order)."""
     shape = workload.TINY
     batched_case(shape, workload.master_weights(shape, seed=0), mode, B)
 
