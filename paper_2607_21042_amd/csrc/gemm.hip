@@ -532,7 +532,7 @@ __global__ __launch_bounds__(512) void gemm_big_kernel(const GemmArgs a) {
         const int tn = (a.N + GB - 1) / GB, tm = (a.M + GB - 1) / GB, T = tm * tn;
         const int b = blockIdx.x, x = b & 7, l = b >> 3, q = T >> 3, r = T & 7;
         const int t = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + l;
-        constexpr int GM = 4;  // row blocks per group
+        constexpr int GM = 8;  // row blocks per group
         const int g = t / (GM * tn), gm = min(GM, tm - g * GM), w = t - g * GM * tn;
         c.m0 = (g * GM + w % gm) * GB;
         c.n0 = (w / gm) * GB;
