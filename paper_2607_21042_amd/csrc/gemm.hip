@@ -169,7 +169,18 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const GemmArgs a) {
     __shared__ RowSlot s_rows[EPI == EPI_QKV ? BM : 1];  // KV destination of each row of the tile
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * G2N;
+    // Workgroups are dealt to the 8 XCDs round-robin by linear id: give each XCD a
+    // contiguous run of tiles in row-major order, so the column tiles of one row
+    // block share an XCD's L2 and the activation block is fetched there once.
+    // Every K slice of a tile maps alike, so the split-K pairing is unchanged.
+    int m0, n0;
+    {
+        const int T = gridDim.x * gridDim.y, b = blockIdx.y * gridDim.x + blockIdx.x;
+        const int x = b & 7, l = b >> 3, q = T >> 3, r = T & 7;
+        const int t = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + l;
+        m0 = (t / gridDim.x) * BM;
+        n0 = (t % gridDim.x) * G2N;
+    }
     if constexpr (EPI == EPI_QKV) {
         if (tid < BM) s_rows[tid] = row_slot(a, min(m0 + tid, a.M - 1));  // read after the first barrier
     }
