@@ -566,6 +566,19 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Workgroups are dealt to the 8 XCDs round-robin by linear id.  Give each XCD a
+// contiguous run of (head, query tile) pairs, query tiles fastest, so the query
+// tiles of one (sequence, head) share an XCD and its K and V rows are fetched
+// into one L2 (used by the wide-grid kernel; measured neutral-to-worse for the
+// key-split one, whose query tiles each read all keys anyway).
+struct FaTile { int tile, head; };
+__device__ __forceinline__ FaTile fa_tile() {
+    const int T = gridDim.x * gridDim.y, b = blockIdx.y * gridDim.x + blockIdx.x;
+    const int x = b & 7, l = b >> 3, q = T >> 3, r = T & 7;
+    const int t = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + l;
+    return FaTile{(int)(t % gridDim.x), (int)(t / gridDim.x)};
+}
+
 __global__ __launch_bounds__(kFaWaves * 64, 3) void attn_full_mfma_kernel(const AttnPrefillArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t vt[kFaWaves][kHeadDim][kVtStride];
     __shared__ float mrg[kFaWaves - 1][34][64];  // waves 1..3: 32 output values, max, sum per lane
@@ -751,8 +764,10 @@ constexpr int kFsK = kHeadDim + 8;  // bf16 per K row in LDS (16-byte aligned, s
 __global__ __launch_bounds__(kFaWaves * 64, 2) void attn_full_shared_kernel(const AttnPrefillArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t ks[2][kFaK][kFsK];
     __shared__ __attribute__((aligned(16))) uint16_t vs[2][kHeadDim][kVtStride];
-    const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    int gt = blockIdx.x, sq = 0;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const FaTile ft = fa_tile();
+    const int h = ft.head;
+    int gt = ft.tile, sq = 0;
     while (sq + 1 < a.seqs.n && a.tiles_cu[sq + 1] <= gt) ++sq;
     const int tile = gt - a.tiles_cu[sq];
     const int row0 = a.seqs.cu[sq], len = a.seqs.cu[sq + 1] - row0;
