@@ -35,7 +35,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "GPT decode tokens/s on 1 MI355X at batch 1 & 32; achieved HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0
-COUNTERS = os.path.join(ROOT, "profiles", "decode_mega_counters.json")
+COUNTERS = os.path.join(ROOT, "profiles", "decode_counters.json")
 
 
 def parse():
@@ -47,9 +47,13 @@ def parse():
     p.add_argument("--batch", type=int, default=1)
     p.add_argument("--prefix", type=int, default=256)
     p.add_argument("--decode", type=int, default=512)
-    p.add_argument("--cpu-steps", type=int, default=16, help="decode steps timed for the CPU oracle baseline")
+    p.add_argument("--cpu-steps", type=int, default=512,
+                   help="decode steps timed for the CPU oracle baseline (default: the whole 512-step run)")
     p.add_argument("--graph-steps", type=int, default=32, help="decode steps per HIP graph (kernel-per-phase path)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-legs", action="store_true",
+                   help="headline workload only (by default the bf16 batch-1 run is followed by the W8A16 and "
+                        "W4A16 batch-1, W8A16 batch-8 and batched paged batch-32 legs in the same JSON line)")
     p.add_argument("--paged", action="store_true",
                    help="the batched paged workload instead: --batch sequences (default 32) with prefix lengths "
                         "~U[128,512], targets ~U[256,768] then STOP, top-k 30 / top-p 0.8 / T 0.8 sampling")
@@ -81,11 +85,15 @@ def copy_calibration():
     print(json.dumps({"copy_calibration": {"bytes_read_per_copy": n, "bytes_written_per_copy": n, "copies": 4}}))
 
 
-def kernel_sources_sha() -> str:
-    """Hash of the sources the persistent decode kernel is built from."""
+MEGA_SOURCES = ("decode_mega.hip", "ftts_internal.hpp", "gemv_impl.hpp", "kv_page.hpp")
+BATCHED_SOURCES = ("bgemm.hip", "attention.hip", "misc.hip", "ftts.hip", "ftts_internal.hpp", "kv_page.hpp")
+
+
+def kernel_sources_sha(files=MEGA_SOURCES) -> str:
+    """Hash of the sources a decode path's kernels are built from."""
     csrc = os.path.join(ROOT, "paper_2607_21042_amd", "csrc")
     h = hashlib.sha256()
-    for f in ("decode_mega.hip", "ftts_internal.hpp", "gemv_impl.hpp", "kv_page.hpp"):
+    for f in files:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(fh.read())
     with open(os.path.join(ROOT, "include", "ftts.h"), "rb") as fh:
@@ -93,16 +101,18 @@ def kernel_sources_sha() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch from the committed counter runs, if they apply."""
+def measured_traffic(workload: str, sha: str):
+    """HBM bytes per timed unit from the committed counter runs, if one was taken
+    on this workload and the kernel sources are unchanged since."""
     try:
         with open(COUNTERS) as fh:
-            c = json.load(fh)
-    except (OSError, ValueError):
+            entries = json.load(fh)["entries"]
+    except (OSError, ValueError, KeyError):
         return None
-    if c.get("workload") != workload or c.get("source_sha256") != kernel_sources_sha():
-        return None
-    return c.get("hbm_bytes_per_launch")
+    for c in entries:
+        if c.get("workload") == workload and c.get("source_sha256") == sha:
+            return c.get("hbm_bytes_per_unit")
+    return None
 
 
 def algorithmic_step_bytes(shape, dm, B, ctx_lens, kv_elem):
@@ -118,27 +128,43 @@ def algorithmic_step_bytes(shape, dm, B, ctx_lens, kv_elem):
     return dm.weight_bytes() - embed_tables + kv_read + kv_write + emb + logits
 
 
-def cpu_baseline(inputs, shape, mode, prefix, n_steps):
+def cpu_baseline(inputs, shape, mode, prefixes, n_steps, sampling=None, batch=None):
+    """The numpy fp32 oracle, as it stands, on the host cores: an untimed prefill
+    of each prefix, then n_steps decode steps per sequence, one sequence after
+    another (greedy, or the oracle sampler with `sampling` = (T, k, p) and
+    seeded uniforms), timed.  `batch` names the GPU batch the sample stands for."""
     import threadpoolctl
     from oracle import gpt as ogpt
     from oracle import quant as oquant
+    from oracle import sample as osample
 
     cores = len(os.sched_getaffinity(0))
     with threadpoolctl.threadpool_limits(cores):
         w = inputs if mode in ("f32", "bf16") else oquant.dequantized_model(
             inputs, "w8" if mode == "w8a16" else "w4")
         om = ogpt.GPT(w, shape.n_head, shape.d_head, dtype=np.float32)
-        cache, _ = om.prefill(prefix)
-        tok = shape.start_token
+        caches = [om.prefill(p)[0] for p in prefixes]
+        uni = np.random.default_rng(2).random((n_steps, len(prefixes)), dtype=np.float32)
         t0 = time.perf_counter()
-        for t in range(n_steps):
-            logits, _ = om.decode_step(cache, tok, t)
-            tok = int(np.argmax(logits))
+        for b, cache in enumerate(caches):
+            tok = shape.start_token
+            for t in range(n_steps):
+                logits, _ = om.decode_step(cache, tok, t)
+                if sampling is None:
+                    tok = int(np.argmax(logits))
+                else:
+                    tok = osample.sample(logits.astype(np.float32), *sampling, uni[t, b])[0]
         dt = time.perf_counter() - t0
         used = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
-    return {"value": round(n_steps / dt, 3), "unit": "tokens/s", "cores": int(min(used, cores)), "kind": "oracle",
-            "sample": f"{n_steps} greedy decode steps (batch 1) after an untimed {prefix.shape[0]}-row prefill, "
-                      f"numpy fp32 oracle on the same {mode} weights"}
+    n_tok = n_steps * len(prefixes)
+    how = "greedy" if sampling is None else "top-k {1} / top-p {2} / T {0} sampled".format(*sampling)
+    lens = sorted({p.shape[0] for p in prefixes})
+    sample = (f"{n_steps} {how} decode steps of {len(prefixes)} sequence(s) after an untimed prefill of "
+              f"{'/'.join(str(x) for x in lens)} rows, numpy fp32 oracle on the same {mode} weights")
+    if batch is not None and batch != len(prefixes):
+        sample += f" (the oracle runs sequences one at a time: its rate for the batch of {batch} is the same)"
+    return {"value": round(n_tok / dt, 3), "unit": "tokens/s", "cores": int(min(used, cores)), "kind": "oracle",
+            "sample": sample}
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
@@ -218,9 +244,10 @@ def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
     reset_and_prefill()
     step(0)
     torch.cuda.synchronize()
-    # One graph per 32 steps (each step reads its own row of uniforms): a graph of
-    # every step would be a single dependency chain of ~100k kernel nodes.
-    S = 32
+    # One graph per --graph-steps steps (each step reads its own row of uniforms):
+    # a graph of every step would be a single chain of ~94k kernel nodes, beyond
+    # the cap on steps per graph.
+    S = ftts.graph_steps(args.graph_steps)
     graphs = []
     for g0 in range(0, T_max, S):
         g = torch.cuda.CUDAGraph()
@@ -268,25 +295,32 @@ def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
         total_bytes += weights + int(((P + t + 1) * act).sum()) * per_tok_kv + int(act.sum()) * (
             per_tok_kv + 2 * shape.d_model * kv_elem + shape.vocab * 4)
     achieved = total_bytes / (decode_ms / 1e3) / 1e9
-    return {
+    workload_name = (f"indextts2-gpt {mode} paged batch={B} prefix~U[128,512] target~U[256,768]+STOP "
+                     f"top-k 30 top-p 0.8 T 0.8")
+    out = {
         "metric": METRIC, "value": round(n_tok / (job_ms / 1e3), 2), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(job_ms, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": {"f32": "f32", "bf16": "bf16", "w8a16": "int8-w/bf16",
                                                           "w4a16": "int4-w/bf16"}[mode],
         "data": "synthetic: seeded random-init IndexTTS-2-shaped GPT; paged KV from a shared pool",
-        "config": {"workload": f"indextts2-gpt {mode} paged batch={B} prefix~U[128,512] target~U[256,768]+STOP "
-                               f"top-k 30 top-p 0.8 T 0.8", "batch": B, "tokens": n_tok, "decode_steps": T_max,
+        "config": {"workload": workload_name, "batch": B, "tokens": n_tok, "decode_steps": T_max,
                    "decode_path": "kernel-per-phase" if ftts.decode_path(dm, B) == 1 else "persistent"},
         "decode_tokens_per_s": round(n_tok / (decode_ms / 1e3), 2),
         "decode_ms_per_step": round(decode_ms / T_max, 4),
         "prefill_ms": round(job_ms - decode_ms, 3),
         "prefill": prefill_report(shape, P, float(np.mean([a.elapsed_time(b) for a, b in pevs]))),
         "wall_s": round(wall, 3),
-        "roofline": {"bound": "hbm", "kernel": f"decode step, kernel per phase ({T_max} steps, 32 per HIP graph)",
+        "roofline": {"bound": "hbm", "kernel": f"decode step, kernel per phase ({T_max} steps, {S} per HIP graph)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "algorithmic_bytes_per_step": int(total_bytes / T_max), "traffic": None},
+                     "algorithmic_bytes_per_step": int(total_bytes / T_max),
+                     "traffic": measured_traffic(workload_name, kernel_sources_sha(BATCHED_SOURCES))},
     }
+    if not args.no_cpu_baseline:
+        flat = workload.prefix_embeddings(P[:2].tolist(), shape.d_model, seed=1, bf16=(mode != "f32"))
+        seqs = np.split(flat, [int(P[0])])
+        out["cpu_baseline"] = cpu_baseline(inputs, shape, mode, seqs, 64, sampling=(0.8, 30, 0.8), batch=B)
+    return out
 
 
 def serve_run(args, torch, ftts, workload, shape, dm, mode):
@@ -436,46 +470,25 @@ def dit_run(args, torch, ftts, workload):
     return out
 
 
-def main():
-    args = parse()
-    if args.copy_calibration:
-        copy_calibration()
-        return
-    if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1",
-                          "n_gpus": args.gpus}))
-        sys.exit(2)
-    import torch
-    from paper_2607_21042_amd import ftts, workload
+DTYPE_NAMES = {"f32": "f32", "bf16": "bf16", "w8a16": "int8-w/bf16", "w4a16": "int4-w/bf16"}
 
-    if not torch.cuda.is_available():
-        print(json.dumps({"error": "no GPU visible"}))
-        sys.exit(1)
-    if args.dit:
-        print(json.dumps(dit_run(args, torch, ftts, workload)), flush=True)
-        return
-    shape = workload.INDEXTTS2
-    mode = args.mode
-    wdtype = {"f32": ftts.F32, "bf16": ftts.BF16, "w8a16": ftts.W8A16, "w4a16": ftts.W4A16}[mode]
-    B, P, T = args.batch, args.prefix, args.decode
-    master = workload.master_weights(shape, seed=0)
+
+def model_inputs(workload, master, mode):
     if mode == "f32":
-        inputs = master
-    elif mode == "bf16":
-        inputs = workload.bf16_weights(master)
-    else:
-        inputs = workload.quantisable_weights(master)
+        return master
+    if mode == "bf16":
+        return workload.bf16_weights(master)
+    return workload.quantisable_weights(master)
+
+
+def fixed_batch(torch, ftts, workload, shape, inputs, mode, B, P, T, steps, warmup, graph_steps=32,
+                cpu_steps=0, cpu_seqs=1):
+    """B sequences with the same prefix length P, T greedy steps each; one job =
+    prefill + T steps with the sampled ids fed back on the device.  The
+    persistent step is timed per launch; the kernel-per-phase step per graph
+    replay of `graph_steps` steps."""
+    wdtype = {"f32": ftts.F32, "bf16": ftts.BF16, "w8a16": ftts.W8A16, "w4a16": ftts.W4A16}[mode]
     dm = ftts.DeviceModel(inputs, shape, wdtype)
-    if args.paged:
-        if args.batch == 1:
-            args.batch = 32
-        print(json.dumps(paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs)), flush=True)
-        return
-    if args.serve:
-        if args.batch == 1:
-            args.batch = 32
-        print(json.dumps(serve_run(args, torch, ftts, workload, shape, dm, mode)), flush=True)
-        return
     adt = ftts.act_dtype(wdtype)
     prefix_np = workload.prefix_embeddings([P] * B, shape.d_model, seed=1, bf16=(mode != "f32"))
     prefix = torch.from_numpy(prefix_np).cuda().to(adt)
@@ -523,7 +536,7 @@ def main():
     torch.cuda.synchronize()
     if not persistent:
         # several kernels per step: capture S steps into one graph
-        S = args.graph_steps if T % args.graph_steps == 0 else 1
+        S = ftts.graph_steps(graph_steps) if T % graph_steps == 0 else 1
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
             for _ in range(S):
@@ -554,19 +567,19 @@ def main():
                 if evs is not None:
                     evs[r][1].record(stream)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         job()
     torch.cuda.synchronize()
     n_units = T if persistent else T // S
     evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_units)]
-           for _ in range(args.steps)]
-    pevs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+           for _ in range(steps)]
+    pevs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t_start.record(stream)
-    for k in range(args.steps):
+    for k in range(steps):
         job(evs[k], pevs[k])
     t_end.record(stream)
     torch.cuda.synchronize()
@@ -574,7 +587,7 @@ def main():
     if persistent:
         ftts.check_workspace(ws)
     total_ms = t_start.elapsed_time(t_end)
-    job_ms = total_ms / args.steps
+    job_ms = total_ms / steps
     value = B * T / (job_ms / 1e3)
 
     kv_elem = 4 if mode == "f32" else 2
@@ -583,20 +596,23 @@ def main():
     if persistent:
         unit_bytes = step_bytes
         kernel = "decode_mega_kernel (persistent single-launch decode step)"
+        sha = kernel_sources_sha(MEGA_SOURCES)
     else:
         unit_bytes = step_bytes.reshape(T // S, S).sum(axis=1)
         kernel = f"decode step, kernel per phase ({S} steps per graph replay)"
+        sha = kernel_sources_sha(BATCHED_SOURCES)
     launch_us = float(unit_ms.mean() * 1e3)
-    achieved = float(unit_bytes.sum() * args.steps / (unit_ms.sum() / 1e3) / 1e9)
+    achieved = float(unit_bytes.sum() * steps / (unit_ms.sum() / 1e3) / 1e9)
     decode_ms = float(unit_ms.sum(axis=1).mean())
     workload_name = f"indextts2-gpt {mode} batch={B} prefix={P} greedy decode={T}"
     out = {
-        "metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(job_ms, 3), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": {"f32": "f32", "bf16": "bf16", "w8a16": "int8-w/bf16", "w4a16": "int4-w/bf16"}[mode],
+        "metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
+        "warmup": warmup, "ms_per_step": round(job_ms, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": DTYPE_NAMES[mode],
         "data": "synthetic: seeded random-init IndexTTS-2-shaped GPT (24x1280, 20 heads, FFN 5120, vocab 8194)",
         "config": {"workload": workload_name, "batch": B, "prefix": P, "decode_tokens": T, "weights": mode,
                    "decode_path": "persistent" if persistent else "kernel-per-phase"},
+        "decode_tokens_per_s": round(B * T / (decode_ms / 1e3), 2),
         "decode_ms_per_token_step": round(decode_ms / T, 4),
         "prefill_ms": round(job_ms - decode_ms, 3),
         "prefill": prefill_report(shape, [P] * B, float(np.mean([a.elapsed_time(b) for a, b in pevs]))),
@@ -605,10 +621,95 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "launch_us": round(launch_us, 2),
                      "algorithmic_bytes_per_launch": int(unit_bytes.mean()),
-                     "traffic": measured_traffic(workload_name) if persistent else None},
+                     "traffic": measured_traffic(workload_name, sha)},
     }
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(inputs, shape, mode, prefix_np[:P], args.cpu_steps)
+    del dm, kv, ws
+    torch.cuda.empty_cache()
+    if cpu_steps > 0:
+        seqs = [prefix_np[b * P:(b + 1) * P] for b in range(min(cpu_seqs, B))]
+        out["cpu_baseline"] = cpu_baseline(inputs, shape, mode, seqs, cpu_steps, batch=B)
+    return out
+
+
+LEG_KEYS = ("config", "dtype", "value", "unit", "ms_per_step", "decode_tokens_per_s", "decode_ms_per_token_step",
+            "decode_ms_per_step", "prefill_ms", "prefill", "roofline", "cpu_baseline", "steps", "warmup")
+
+
+def legs(args, torch, ftts, workload, shape, master):
+    """The rest of the metric, measured in the same run after the headline:
+    W8A16 and W4A16 at batch 1, W8A16 at batch 8, and the batched paged
+    workload at batch 32.  Each leg is a few whole jobs (prefill + all decode
+    steps) after one untimed job."""
+    out = {}
+    for name, mode, B, P in (("w8a16_b1", "w8a16", 1, 256), ("w4a16_b1", "w4a16", 1, 384),
+                             ("w8a16_b8", "w8a16", 8, 256)):
+        t0 = time.perf_counter()
+        inputs = model_inputs(workload, master, mode)
+        r = fixed_batch(torch, ftts, workload, shape, inputs, mode, B, P, 512, steps=3, warmup=1,
+                        cpu_steps=0 if args.no_cpu_baseline else 64, cpu_seqs=1 if B == 1 else 2)
+        r["leg_wall_s"] = round(time.perf_counter() - t0, 1)
+        out[name] = {k: r[k] for k in LEG_KEYS + ("leg_wall_s",) if k in r}
+        print(f"leg {name}: {r['value']} tokens/s, {r['decode_ms_per_token_step']} ms per step",
+              file=sys.stderr, flush=True)
+        del inputs
+    t0 = time.perf_counter()
+    inputs = workload.bf16_weights(master)
+    dm = ftts.DeviceModel(inputs, shape, ftts.BF16)
+    pa = argparse.Namespace(**vars(args))
+    pa.batch, pa.steps, pa.warmup = 32, 2, 1
+    r = paged_batch(pa, torch, ftts, workload, shape, dm, "bf16", ftts.BF16, inputs)
+    del dm
+    torch.cuda.empty_cache()
+    r["leg_wall_s"] = round(time.perf_counter() - t0, 1)
+    out["bf16_b32_paged"] = {k: r[k] for k in LEG_KEYS + ("leg_wall_s",) if k in r}
+    print(f"leg bf16_b32_paged: {r['value']} tokens/s", file=sys.stderr, flush=True)
+    return out
+
+
+def main():
+    args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    from paper_2607_21042_amd import ftts, workload
+
+    try:
+        ftts.graph_steps(args.graph_steps)
+    except ValueError as e:
+        print(json.dumps({"error": str(e)}))
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    if args.dit:
+        print(json.dumps(dit_run(args, torch, ftts, workload)), flush=True)
+        return
+    shape = workload.INDEXTTS2
+    mode = args.mode
+    wdtype = {"f32": ftts.F32, "bf16": ftts.BF16, "w8a16": ftts.W8A16, "w4a16": ftts.W4A16}[mode]
+    master = workload.master_weights(shape, seed=0)
+    inputs = model_inputs(workload, master, mode)
+    if args.paged or args.serve:
+        dm = ftts.DeviceModel(inputs, shape, wdtype)
+        if args.batch == 1:
+            args.batch = 32
+        if args.paged:
+            r = paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs)
+        else:
+            r = serve_run(args, torch, ftts, workload, shape, dm, mode)
+        print(json.dumps(r), flush=True)
+        return
+    out = fixed_batch(torch, ftts, workload, shape, inputs, mode, args.batch, args.prefix, args.decode, args.steps,
+                      args.warmup, graph_steps=args.graph_steps,
+                      cpu_steps=0 if args.no_cpu_baseline else args.cpu_steps)
+    headline = mode == "bf16" and args.batch == 1 and args.prefix == 256 and args.decode == 512
+    if headline and not args.no_legs:
+        out["legs"] = legs(args, torch, ftts, workload, shape, master)
     print(json.dumps(out), flush=True)
 
 

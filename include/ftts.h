@@ -173,7 +173,11 @@ const char* ftts_version(void);
  * qualify -- d_model 1280, 20 heads, d_ff 5120, 256 <= vocab <= 10240, at most
  * 50 layers, 16-bit or quantised weights, batch <= 2, per-layer tensors of each
  * kind at a fixed stride, weight matrices and LayerNorm vectors 16-byte aligned,
- * a 256-CU device -- otherwise one kernel per phase), 1 always one kernel per
+ * a 256-CU device on which the occupancy query admits one of its workgroups per
+ * CU -- otherwise one kernel per phase).  The persistent step needs its 256
+ * workgroups resident together: work launched concurrently on other streams of
+ * the same device can delay that until its bounded wait gives up (see
+ * ftts_check_workspace).  1 always one kernel per
  * phase, 2 always the persistent step (calls that do not qualify return
  * FTTS_E_UNSUPPORTED). */
 int ftts_set_decode_path(int32_t path);
@@ -186,7 +190,12 @@ int ftts_decode_path(const ftts_weights* w, int32_t batch);
 
 /* Synchronises `stream`, then reports FTTS_E_HIP if a persistent decode step on
  * this workspace gave up waiting for one of its inputs (its bounded wait ran
- * out), FTTS_OK otherwise.  ftts_prefill clears the condition. */
+ * out, about a second), FTTS_OK otherwise.  The step that gives up, and every
+ * later step on this workspace, writes sampled_out[b] = -1 for every row (so a
+ * loop driven by ftts_advance retires every slot) and leaves logits_out
+ * unspecified; ftts_prefill clears the condition.  The device-side flag can
+ * also be read without a synchronisation: it is the 32-bit word at byte offset
+ * 4 of the workspace (0 = no failure). */
 int ftts_check_workspace(const void* ws, size_t ws_bytes, void* stream);
 
 /*

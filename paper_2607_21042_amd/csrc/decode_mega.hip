@@ -145,10 +145,24 @@ __device__ __forceinline__ void dma_rows(const void* W, int row_b, int r0, int n
 }
 
 // Workgroup agreement on a failed wait: a flag in LDS, set by any wave that
-// gave up, read by every wave after the barrier that ends each gather.
+// gave up, read by every wave after the barrier that ends each gather.  A wave
+// that gives up also raises the device-wide abort word and marks every row of
+// the step as failed (sampled id -1, row inactive, so the sampler that may
+// follow writes -1 too): a generation loop stops instead of reusing stale ids.
 struct Sync {
     int* fail;
+    int32_t* sampled;
+    int32_t* active_out;
+    int B;
 };
+__device__ __forceinline__ void give_up(const Sync& sy, uint32_t* ctl) {
+    *sy.fail = 1;
+    __hip_atomic_store(ctl + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int b = 0; b < sy.B; ++b) {
+        sy.sampled[b] = -1;
+        sy.active_out[b] = 0;
+    }
+}
 
 // Compute waves: wait until the n exchange words all carry `epoch` and leave their
 // values in dst (LDS); idx(j) maps value j to its word.  Each wave polls its own
@@ -193,10 +207,7 @@ __device__ __forceinline__ bool gather(const uint64_t* src, int n, Idx idx, uint
                 a0 = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (__all((uint32_t)(a1 >> 32) == epoch)) break;
             }
-            if (failed && tid == 0) {
-                *sy.fail = 1;
-                st_agent(ctl + 1, 1u);
-            }
+            if (failed && tid == 0) give_up(sy, ctl);
         }
         bar();
         failed = *sy.fail != 0;
@@ -243,10 +254,7 @@ __device__ __forceinline__ bool gather(const uint64_t* src, int n, Idx idx, uint
         }
     }
     if (mark >= 0) MEGA_MARK(mark + 1);
-    if (failed && (tid & 63) == 0) {
-        *sy.fail = 1;
-        st_agent(ctl + 1, 1u);
-    }
+    if (failed && (tid & 63) == 0) give_up(sy, ctl);
     bar();
     return *sy.fail == 0;
 }
@@ -552,8 +560,11 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
     const int B = a.B;
     const uint32_t step = ld_agent(a.ctl);
     auto E = [&](int ev) { return (step << 8) | (uint32_t)ev; };
-    if (tid == 0) s_abort = ld_agent(a.ctl + 1) != 0;
-    if (tid == 0) s_fail = 0;
+    if (tid == 0) {
+        s_abort = ld_agent(a.ctl + 1) != 0;
+        s_fail = 0;
+    }
+    __syncthreads();
     if (tid < B) {  // the sequence's token, position and KV slot; inactive rows produce nothing
         const int b = tid;
         const int t = a.tokens[b], p = a.positions[b], s = a.seq_lens[b];
@@ -563,16 +574,22 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
             phys = a.block_table[(size_t)b * a.max_pages + s / kPage];
             act = phys >= 0 && phys < a.n_pages;
         }
+        // after an earlier step gave up, every step fails at once: no row is
+        // active and every sampled id is -1 until a prefill clears the abort word
+        if (s_abort) act = false;
         s_active[b] = act;
         s_tok[b] = t;
         s_pos[b] = p;
         s_slot[b] = s;
         s_phys[b] = phys;
-        if (wg == 0) a.active_out[b] = act;
+        if (wg == 0) {
+            a.active_out[b] = act;
+            if (s_abort) a.sampled[b] = -1;
+        }
     }
     __syncthreads();
     if (s_abort) return;
-    Sync sy{&s_fail};
+    Sync sy{&s_fail, a.sampled, a.active_out, B};
     MEGA_MARK(0);
     if (wave == DW) {
         copy_wave<WT, BMAX>(a, s_w, sy);
@@ -918,6 +935,33 @@ extern "C" int ftts_mega_trace_read(void* host, size_t bytes) {
     return hipMemcpyFromSymbol(host, HIP_SYMBOL(mega::g_mega_marks), sizeof(mega::g_mega_marks)) == hipSuccess ? 0 : -1;
 }
 #endif
+
+// Workgroups of the persistent step that fit one CU at once (the step needs 1:
+// its 256 groups must all be resident, one per CU, for the exchanges to end).
+int decode_mega_blocks_per_cu(int wdtype, int B) {
+    using namespace mega;
+    static int cache[3][2] = {{-1, -1}, {-1, -1}, {-1, -1}};
+    const int wi = wdtype == FTTS_BF16 ? 0 : wdtype == FTTS_W8A16 ? 1 : wdtype == FTTS_W4A16 ? 2 : -1;
+    if (wi < 0) return 0;
+    const int bi = B <= 1 ? 0 : 1;
+    if (cache[wi][bi] >= 0) return cache[wi][bi];
+    int n = 0;
+    hipError_t e = hipErrorInvalidValue;
+    switch (wi * 2 + bi) {
+        case 0: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_mega_kernel<FTTS_BF16, 1>, NT, 0); break;
+        case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_mega_kernel<FTTS_BF16, BM>, NT, 0); break;
+        case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_mega_kernel<FTTS_W8A16, 1>, NT, 0); break;
+        case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_mega_kernel<FTTS_W8A16, BM>, NT, 0); break;
+        case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_mega_kernel<FTTS_W4A16, 1>, NT, 0); break;
+        case 5: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_mega_kernel<FTTS_W4A16, BM>, NT, 0); break;
+    }
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        n = 0;
+    }
+    cache[wi][bi] = n;
+    return n;
+}
 
 hipError_t launch_decode_mega(int wdtype, const mega::Args& a, hipStream_t st) {
     using namespace mega;

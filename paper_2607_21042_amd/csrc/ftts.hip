@@ -303,6 +303,8 @@ bool mega_args(const ftts_weights* w, int B, mega::Args* a) {
     // LM-head rows per group must fit the two 50 KB LDS weight buffers (40 rows of 1280 bf16).
     if (B < 1 || B > BM || c.n_layer > 50 || c.vocab < G || c.vocab > G * 40) return false;
     if (device_cus() != G) return false;
+    // every one of the 256 workgroups must be resident at once (one per CU)
+    if (decode_mega_blocks_per_cu(c.wdtype, B) < 1) return false;
     bool ok = true;
     ok &= stride_of(w, [](const ftts_layer& L) { return L.ln1_g; }, &a->ln1_g);
     ok &= stride_of(w, [](const ftts_layer& L) { return L.ln1_b; }, &a->ln1_b);

@@ -342,5 +342,6 @@ struct Args {
 
 }
 hipError_t launch_decode_mega(int wdtype, const mega::Args& a, hipStream_t st);
+int decode_mega_blocks_per_cu(int wdtype, int B);
 
 }  // namespace ftts

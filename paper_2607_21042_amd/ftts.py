@@ -241,6 +241,31 @@ def check_workspace(ws, stream=None):
     _check(lib().ftts_check_workspace(_ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
+# Byte offset of the persistent step's abort word in a workspace (int32, 0 = no failure).
+ABORT_WORD_OFFSET = 4
+
+
+def abort_word(ws):
+    """A one-element int32 view of the workspace's abort word, for an asynchronous
+    device-to-host copy (ftts_check_workspace reads the same word after a sync)."""
+    return ws.view(torch.uint8)[ABORT_WORD_OFFSET:ABORT_WORD_OFFSET + 4].view(torch.int32)
+
+
+# Most decode steps captured into one HIP graph.  A batched step is about 125
+# kernel nodes; a single graph of a whole 755-step generation (about 94k nodes)
+# once ended its process without a result, while graphs of 16-64 steps have
+# always run, so longer loops are split into graphs of at most this many steps.
+MAX_GRAPH_STEPS = 64
+
+
+def graph_steps(n: int) -> int:
+    """Check a steps-per-graph request against MAX_GRAPH_STEPS; returns it."""
+    n = int(n)
+    if n < 1 or n > MAX_GRAPH_STEPS:
+        raise ValueError(f"steps per HIP graph must be in [1, {MAX_GRAPH_STEPS}] (got {n})")
+    return n
+
+
 def advance(tokens, positions, seq_lens, sampled, remaining=None, stop_token=0, history=None, step_counter=None,
             stream=None):
     """ftts_advance: device-side bookkeeping between decode steps."""

@@ -69,6 +69,8 @@ class Scheduler:
                  overlap: int = 0, hidden: bool = False, max_prefill_rows: int | None = None, graphs: bool = True):
         if chunk < 1 or overlap < 0 or overlap >= chunk:
             raise ValueError("need chunk >= 1 and 0 <= overlap < chunk")
+        if graphs:
+            ftts.graph_steps(chunk)                 # a chunk is one captured graph
         self.model, self.shape, self.B, self.chunk, self.overlap = model, shape, max_slots, chunk, overlap
         self.sampling, self.want_hidden = sampling, hidden
         self.max_pages = (max_ctx + ftts.PAGE - 1) // ftts.PAGE
@@ -93,6 +95,7 @@ class Scheduler:
         self.host_hist = [torch.empty((chunk, B), dtype=torch.int32).pin_memory() for _ in range(2)]
         self.host_hid = ([torch.empty((chunk, B, shape.d_model), dtype=torch.float32).pin_memory()
                           for _ in range(2)] if hidden else None)
+        self.host_abort = [torch.zeros(1, dtype=torch.int32).pin_memory() for _ in range(2)]
         self.done_ev = [torch.cuda.Event() for _ in range(2)]
         self.slot_req: list[Request | None] = [None] * B
         self.slot_pages: list[list[int]] = [[] for _ in range(B)]
@@ -175,6 +178,7 @@ class Scheduler:
         else:
             self._steps(buf)
         self.host_hist[buf].copy_(self.history[buf], non_blocking=True)
+        self.host_abort[buf].copy_(ftts.abort_word(self.ws), non_blocking=True)
         if self.want_hidden:
             self.host_hid[buf].copy_(self.hidden_buf[buf], non_blocking=True)
         self.done_ev[buf].record()
@@ -197,6 +201,10 @@ class Scheduler:
         """Hand chunk k's ids to their requests; retire the finished ones."""
         buf = k & 1
         self.done_ev[buf].synchronize()
+        if int(self.host_abort[buf][0]) != 0:
+            # a persistent step gave up waiting (its rows carry id -1): stop serving
+            raise ftts.FTTSError(-6, f"decode chunk {k}: a persistent decode step timed out; "
+                                     "its ids are invalid (ftts_prefill on a fresh workspace clears this)")
         hist = self.host_hist[buf].numpy()
         hid = self.host_hid[buf].numpy() if self.want_hidden else None
         for s, r in enumerate(self.slot_req):

@@ -3,6 +3,7 @@ every function include/ftts.h declares, sizes workspaces, and rejects bad
 arguments before anything is enqueued (every call below fails validation, so
 no kernel is launched and no pointer is dereferenced)."""
 import ctypes
+import os
 
 import pytest
 
@@ -247,3 +248,30 @@ def test_dit_step_argument_errors():
     assert _dit_step(w) == -1
     w.cfg.d_head = 32
     assert _dit_step(w) == -7
+
+
+def test_graph_step_cap():
+    """Steps per captured HIP graph are capped on the host: the binding refuses
+    larger requests, and bench.py exits with an error before touching a GPU."""
+    import subprocess
+    import sys
+    from paper_2607_21042_amd import ftts
+    assert ftts.graph_steps(1) == 1
+    assert ftts.graph_steps(ftts.MAX_GRAPH_STEPS) == ftts.MAX_GRAPH_STEPS
+    for bad in (0, -3, ftts.MAX_GRAPH_STEPS + 1, 755):
+        with pytest.raises(ValueError):
+            ftts.graph_steps(bad)
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--graph-steps", "755"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2, r.stdout + r.stderr
+    assert "steps per HIP graph" in r.stdout
+
+
+def test_abort_word_offset_matches_header():
+    """The binding's asynchronous view of the abort word sits where the header says."""
+    from paper_2607_21042_amd import ftts
+    with open(ftts.HEADER_PATH) as fh:
+        text = fh.read()
+    assert "byte offset\n * 4 of the workspace" in text or "byte offset 4" in text.replace("\n *", "")
+    assert ftts.ABORT_WORD_OFFSET == 4

@@ -643,3 +643,57 @@ def test_persistent_step_agrees_with_kernel_path(torch_cuda, decode_path, mid_ma
     assert np.max(np.abs(rk["logits"] - rp["logits"])) <= 1e-4 * scale
     np.testing.assert_array_equal(rp["logits"], rq["logits"])
     np.testing.assert_array_equal(rp["sampled"], rq["sampled"])
+
+
+@pytest.mark.parametrize("greedy", [True, False])
+def test_persistent_step_abort_is_visible(torch_cuda, decode_path, mid_master, greedy):
+    """The abort word a persistent step raises when its bounded wait runs out is
+    set here from the host before a step (so the kernel leaves at its first check
+    and enters no wait): that step and the next write sampled id -1 for every row
+    (greedy, and through the sampler when top_k > 1), ftts_check_workspace
+    reports FTTS_E_HIP, and ftts_prefill clears the condition, after which the
+    step reproduces the logits it gave before bit for bit."""
+    torch = torch_cuda
+    from paper_2607_21042_amd import ftts
+    decode_path(ftts.PATH_PERSISTENT)
+    inputs = model_inputs(MID, "bf16", mid_master)
+    lens = [70, 31]
+    B = len(lens)
+    flat = workload.prefix_embeddings(lens, MID.d_model, seed=1)
+    dm = ftts.DeviceModel(inputs, MID, ftts.BF16)
+    bt_np, n_pages = helpers.make_block_table([n + 4 for n in lens])
+    kv = ftts.KVCache(MID, ftts.BF16, n_pages)
+    pt = ftts.PageTableView(torch.from_numpy(bt_np).cuda(), torch.zeros(B, dtype=torch.int32, device="cuda"))
+    ws = torch.empty(ftts.workspace_bytes(dm.cfg, B, sum(lens)), dtype=torch.uint8, device="cuda")
+    prefix = torch.from_numpy(flat).cuda().to(torch.bfloat16)
+    samp = ftts.Sampling(1.0, 1, 1.0) if greedy else ftts.Sampling(0.8, 30, 0.8)
+    tok = torch.full((B,), MID.start_token, dtype=torch.int32, device="cuda")
+    pos = torch.zeros(B, dtype=torch.int32, device="cuda")
+    u = torch.full((B,), 0.5, dtype=torch.float32, device="cuda")
+    logits = torch.empty((B, MID.vocab), dtype=torch.float32, device="cuda")
+    sampled = torch.empty(B, dtype=torch.int32, device="cuda")
+
+    def fresh_step():
+        ftts.prefill(dm, prefix, lens, pt, kv, None, ws)
+        pt.seq_lens.copy_(torch.tensor(lens, dtype=torch.int32))
+        ftts.decode_step(dm, tok, pos, pt, kv, logits, sampled, u, samp, ws)
+        torch.cuda.synchronize()
+        return logits.clone(), sampled.clone()
+
+    say(f"abort visibility, greedy={greedy}")
+    good_logits, good_ids = fresh_step()
+    ftts.check_workspace(ws)
+    assert bool((good_ids >= 0).all())
+    for _ in range(2):
+        ftts.abort_word(ws).fill_(1)
+        sampled.fill_(123)
+        ftts.decode_step(dm, tok, pos, pt, kv, logits, sampled, u, samp, ws)
+        torch.cuda.synchronize()
+        assert sampled.cpu().tolist() == [-1] * B
+        with pytest.raises(ftts.FTTSError) as ei:
+            ftts.check_workspace(ws)
+        assert ei.value.code == -6
+    again_logits, again_ids = fresh_step()
+    ftts.check_workspace(ws)
+    np.testing.assert_array_equal(again_ids.cpu().numpy(), good_ids.cpu().numpy())
+    np.testing.assert_array_equal(again_logits.cpu().numpy(), good_logits.cpu().numpy())

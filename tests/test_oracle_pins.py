@@ -425,3 +425,112 @@ def test_sampler_distribution_chi2():
     assert counts[~keep].sum() == 0
     chi2, pval = stats.chisquare(counts[keep], law[keep] * draws)
     assert pval > 1e-3, (chi2, pval)
+
+
+# --------------------------------------------------------------------------- quantised tensors
+def test_dequantized_model_touches_exactly_the_four_linears():
+    """Weight-only quantisation applies to the GPT's linear layers (Table I caption,
+    Sec. III-B) and the reading is: the four per-layer matrices, nothing else.  Every
+    other tensor (embeddings, LayerNorm, biases, LM head) must come back bit for bit;
+    each of the 4 x L matrices must change and lie on the code grid of its mode:
+    W8 rows are integer multiples in [-127, 127] of one bf16 scale per row (the largest
+    |code| is 127), W4 groups of 128 are (q - z) * s with integer q, z in 0..15."""
+    shape = workload.ModelShape(n_layer=3, d_model=128, n_head=2, d_head=64, d_ff=256, vocab=64, n_pos=32)
+    w = workload.master_weights(shape, seed=3, threads=2)
+    mats = ("w_qkv", "w_out", "w_fc1", "w_fc2")
+
+    def bits(a):
+        return np.ascontiguousarray(a, np.float32).view(np.uint32)
+
+    for mode in ("w8", "w4"):
+        dq = quant.dequantized_model(w, mode)
+        assert set(dq) == set(w)
+        for k in w:
+            if k != "layers":
+                np.testing.assert_array_equal(bits(dq[k]), bits(w[k]), err_msg=(mode, k))
+        assert len(dq["layers"]) == shape.n_layer
+        for l, (a, b) in enumerate(zip(w["layers"], dq["layers"])):
+            assert set(a) == set(b)
+            for k in a:
+                if k in mats:
+                    continue
+                np.testing.assert_array_equal(bits(b[k]), bits(a[k]), err_msg=(mode, l, k))
+            for k in mats:
+                m = np.asarray(b[k], np.float64)
+                assert m.shape == a[k].shape and not np.array_equal(bits(b[k]), bits(a[k])), (mode, l, k)
+                if mode == "w8":
+                    amax = np.max(np.abs(m), axis=1, keepdims=True)
+                    s = amax / 127.0  # the row's largest code is +-127, so this is its scale
+                    assert np.all(bits(s.astype(np.float32)) & 0xFFFF == 0), "scale is not a bf16"
+                    c = m / s
+                    np.testing.assert_array_equal(c, np.rint(c))
+                    assert np.max(np.abs(c)) <= 127
+                else:
+                    N, K = m.shape
+                    g = m.reshape(N, K // 128, 128)
+                    # within a group the values are (q - z) s: their differences are multiples
+                    # of s, and the 16 levels span at most 15 s around zero
+                    lo, hi = g.min(axis=2), g.max(axis=2)
+                    step = np.where(hi > lo, (hi - lo), 1.0)
+                    for n in range(0, N, max(1, N // 7)):
+                        for j in range(K // 128):
+                            v = np.unique(g[n, j])
+                            d = np.diff(v)
+                            s = d.min() if d.size else 1.0
+                            r = (v - v[0]) / s
+                            np.testing.assert_allclose(r, np.rint(r), atol=1e-6)
+                            assert np.rint(r[-1]) <= 15 and step[n, j] > 0
+                            assert np.any(np.abs(v / s - np.rint(v / s)) < 1e-6), "no level at a multiple of s"
+
+
+def test_dequantized_model_pin_catches_a_quantised_head(monkeypatch):
+    """The pin above fails when the LM head or a bias is quantised too, or when a
+    matrix is skipped (planted in a copy of the oracle, on the CPU)."""
+    real = quant.dequantized_model
+
+    def with_head(weights, mode, group=128):
+        out = real(weights, mode, group)
+        out["w_head"] = quant.dequantize_w8(*quant.quantize_w8(weights["w_head"]))
+        return out
+
+    def skip_out(weights, mode, group=128):
+        out = real(weights, mode, group)
+        for a, b in zip(weights["layers"], out["layers"]):
+            b["w_out"] = a["w_out"]
+        return out
+
+    for planted in (with_head, skip_out):
+        monkeypatch.setattr(quant, "dequantized_model", planted)
+        with pytest.raises(AssertionError):
+            test_dequantized_model_touches_exactly_the_four_linears()
+    monkeypatch.setattr(quant, "dequantized_model", real)
+
+
+def test_near_boundary_band():
+    """The excuse band of the sampler parity check: a draw is 'near' exactly when
+    r = u * c_n, or the top-p threshold p * c_k, lies within rel * c_k of a
+    cumulative sum.  Built by hand: three kept weights with known partial sums."""
+    lg = np.log(np.array([0.5, 0.3, 0.2], dtype=np.float64)).astype(np.float32)
+    # cum = e / e_1 summed: [1, 1.6, 2.0] (to fp32 rounding); p = 1 so the threshold is c_3
+    _, det = sample.sample(lg, 1.0, 3, 1.0, np.float32(0.25))
+    cum = det["cum"].astype(np.float64)
+    np.testing.assert_allclose(cum, [1.0, 1.6, 2.0], rtol=1e-6)
+    c_k = cum[-1]
+    # the threshold equals c_3 itself, so every draw of a p = 1 cut is within the band
+    assert sample.near_boundary(det)
+    # with p = 0.9 the threshold 1.8 sits 0.2 from every sum: only r decides
+    for u, near in ((0.25, False), (0.5, True), (0.8, True), (0.3, False), (0.999, False)):
+        _, d = sample.sample(lg, 1.0, 3, 0.9, np.float32(u))
+        assert abs(float(d["thresh"]) - 1.8) < 1e-6
+        r = float(d["r"])
+        want = bool(np.any(np.abs(np.array(d["cum"], np.float64) - r) <= 1e-5 * c_k))
+        assert want == near, (u, r)
+        assert sample.near_boundary(d) == near, (u, r)
+    # just inside and just outside the band around c_1 = 1 (n = 3, so r = u * c_3 = 2 u)
+    for off, near in ((0.5e-5, True), (3e-5, False)):
+        u = np.float32((1.0 + off * c_k) / c_k)
+        _, d = sample.sample(lg, 1.0, 3, 0.9, u)
+        assert sample.near_boundary(d) == near, (off, float(d["r"]))
+    # greedy has no band
+    _, d = sample.sample(lg, 1.0, 1, 0.9, np.float32(0.5))
+    assert not sample.near_boundary(d)
