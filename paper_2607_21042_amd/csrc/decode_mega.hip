@@ -484,48 +484,41 @@ __device__ __forceinline__ void copy_wave(const Args& a, char* s_w, Sync& sy) {
         // P0
         bar();
         MEGA_LMARK(l, 0);
-        dma_rows(a.out_w.at(l), RD, d0, D / G, s_w + kBuf);
         if (l == 0) bar();
         else if (!follow(sy)) goto out;
+        dma_rows(a.out_w.at(l), RD, d0, D / G, s_w + kBuf);
         wait_vm<O::PO>();  // q/k/v share in LDS
         MEGA_LMARK(l, 1);
         bar();             // LN1 done
-        // P1: no weight traffic while the attention phase runs (its q/k/v and
-        // output exchanges and KV page reads are the critical path; measured
-        // faster than spreading the FC1 share over the phase)
+        // P1
         bar();
         MEGA_LMARK(l, 2);
+        if (!is_att) dma_rows(a.fc1_w.at(l), RD, f0, FF / G, s_w);
         if (is_att) {
             if (!follow(sy)) goto out;
             bar();  // wave partials in LDS
         }
         // P2
-        bar();  // every partial's done-word seen: attention is over
-        dma_rows(a.fc1_w.at(l), RD, f0, FF / G, s_w);
-        wait_vm<O::P1>();  // out-proj share in LDS
+        if (is_att) wait_vm<0>(); else wait_vm<O::P1>();  // out-proj share in LDS
         MEGA_LMARK(l, 3);
         if (!follow(sy)) goto out;
-        bar();  // attention partials merged
+        if (is_att) dma_rows(a.fc1_w.at(l), RD, f0, FF / G, s_w);
         // P3
         bar();
         MEGA_LMARK(l, 4);
-        dma_rows(a.fc2_w.at(l), RF, d0, D / G, s_w + kBuf);
         if (!follow(sy)) goto out;
+        dma_rows(a.fc2_w.at(l), RF, d0, D / G, s_w + kBuf);
         wait_vm<O::P2>();  // FC1 share in LDS
         MEGA_LMARK(l, 5);
         bar();             // LN2 done
         // P4
         bar();
         MEGA_LMARK(l, 6);
-        if (l + 1 < a.n_layer) {
-            dma_rows(a.qkv_w.at(l + 1), RD, q0, 3 * D / G, s_w);
-            wait_vm<O::PQ>();  // FC2 share in LDS
-            MEGA_LMARK(l, 7);
-        } else {
-            wait_vm<0>();
-            dma_rows(a.head_w, 2 * D, v0, nA, s_w);
-        }
+        wait_vm<0>();  // FC2 share in LDS
+        MEGA_LMARK(l, 7);
         if (!follow(sy)) goto out;
+        if (l + 1 < a.n_layer) dma_rows(a.qkv_w.at(l + 1), RD, q0, 3 * D / G, s_w);
+        else dma_rows(a.head_w, 2 * D, v0, nA, s_w);
     }
     // head
     bar();
@@ -745,7 +738,7 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
             MEGA_LMARK(l, 16);
             bar();
             MEGA_LMARK(l, 5);
-            if (wave == 0) {  // log-sum-exp merge of the wave partials, published unnormalised
+            if (wave == 0) {  // log-sum-exp merge of the wave partials: the head's output, normalised
                 float M = -INFINITY;
 #pragma unroll
                 for (int i = 0; i < NWC; ++i) M = fmaxf(M, s_pm[i]);
@@ -758,44 +751,13 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
                         acc = fmaf(s_po[i][lane], wgt, acc);
                     }
                 }
-                const size_t pi = ((size_t)b * NH + h) * S + att_s;
-                uint64_t* part = a.ex_o + pi * kPartWords;
-                put(part + lane, E(5 * l + 2), acc);
-                if (lane == 0) put(part + 64, E(5 * l + 2), M);
-                if (lane == 1) put(part + 65, E(5 * l + 2), L);
-                if (lane >= 2 && lane < 2 + kDoneReplicas)  // a hint only: the words carry their own epoch
-                    put(a.ex_odone + (lane - 2) * kDoneStride + pi, E(5 * l + 2), 0.f);
+                put(a.ex_o + (size_t)b * D + h * 64 + lane, E(5 * l + 2), (s_active[b] && L > 0.f) ? acc / L : 0.f);
             }
         }
         // ---------------- P2: out-proj + residual --------------------------------------------
-        // (s_in was last read by P0's dot, before P1's barrier)
-        float* s_part = s_in + BMAX * D;  // the S partials of every (sequence, head)
-        // (groups outside attention wait here through the whole attention phase:
-        // they watch the contiguous done-words of up to 64 partials, a few cache
-        // lines, before reading all the partials)
-        if (!gather<uo<BMAX>()>(a.ex_o, B * NH * S * kPartWords, Flat{}, E(5 * l + 2), s_part, a.ctl, sy,
-                                Sentinels{a.ex_odone + (wg % kDoneReplicas) * kDoneStride, min(B * NH * S, 64)},
-                                1 + l * kMarksPerLayer + 17))
-            return;
-        for (int i = tid; i < B * D; i += NC) {  // o = sum_s w_s acc_s / sum_s w_s L_s, w_s = exp(M_s - max M)
-            const int b = i / D, c = i - b * D;
-            const float* pp = s_part + (b * NH + c / 64) * S * kPartWords;
-            float M = -INFINITY;
-            for (int sp = 0; sp < S; ++sp) M = fmaxf(M, pp[sp * kPartWords + 64]);
-            float L = 0.f, acc = 0.f;
-            if (M > -INFINITY) {
-                for (int sp = 0; sp < S; ++sp) {
-                    const float Ms = pp[sp * kPartWords + 64];
-                    if (Ms > -INFINITY) {
-                        const float wgt = expf(Ms - M);
-                        L = fmaf(pp[sp * kPartWords + 65], wgt, L);
-                        acc = fmaf(pp[sp * kPartWords + (c & 63)], wgt, acc);
-                    }
-                }
-            }
-            s_in[i] = (s_active[b] && L > 0.f) ? acc / L : 0.f;
-        }
-        bar();
+        // o of every head, straight from the attention groups (s_in was last read
+        // by P0's dot, before P1's barrier)
+        if (!gather<ux<BMAX>()>(a.ex_o, B * D, Flat{}, E(5 * l + 2), s_in, a.ctl, sy)) return;
         MEGA_LMARK(l, 6);
         {
             float acc[BMAX];

@@ -543,9 +543,7 @@ static int decode_step(const ftts_weights* w, const int32_t* tokens, const int32
         MegaWs M;
         mega_bytes(&M, reinterpret_cast<char*>(ws));
         ma.max_pages = pt->max_pages;
-        // Enough workgroups per (sequence, head) that each of a group's seven
-        // attention waves holds at most one page, as far as kMaxSplit allows.
-        ma.att_split = std::min(mega::kMaxSplit, std::max(1, (pt->max_pages + 6) / 7));
+        ma.att_split = 1;  // one workgroup per (sequence, head)
         ma.n_pages = kv->n_pages;
         ma.greedy = samp->top_k == 1;
         ma.tokens = tokens;
