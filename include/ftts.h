@@ -288,6 +288,35 @@ int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t
                      int32_t* sampled_out, const float* uniforms, const ftts_sampling* samp,
                      int32_t B, void* ws, size_t ws_bytes, void* stream);
 
+/* Size of the static scratch of ftts_decode_step_static, per GPU. */
+#define FTTS_STATIC_SCRATCH_BYTES (12u << 20)
+
+/*
+ * ftts_decode_step for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.  It
+ * takes no workspace; its scratch (the persistent step's control words and
+ * exchange buffers, the per-phase activations and split-K partials of the
+ * other decode paths) is a static device array of FTTS_STATIC_SCRATCH_BYTES
+ * that each GPU holds, once the first call on it has set it up, until the
+ * process ends.  The call allocates nothing and calls no allocating routine.
+ * Every argument, the result and the graph-capture safety are those of
+ * ftts_decode_step, whose results it reproduces bit for bit.
+ *   FTTS_E_WORKSPACE  when the model and batch need more scratch than
+ *                     FTTS_STATIC_SCRATCH_BYTES (ftts_workspace_bytes(cfg, B, 0)
+ *                     is the need; 8.9 MB for the 24 x 1280 GPT at B = 64).
+ * All calls on one GPU share that GPU's array, which keeps the last call's
+ * contents: calls that overlap on one GPU (several host threads, or streams
+ * whose work can run concurrently) race and must not be issued.  Each call
+ * first runs a one-workgroup kernel on `stream` that, after a persistent step
+ * gave up waiting (its sampled ids are -1) or every 2^24 steps, clears the
+ * array's control words, so a later call starts afresh; no prefill is needed
+ * for that (ftts_prefill works on its own workspace as usual).
+ */
+int ftts_decode_step_static(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
+                            const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out,
+                            int32_t* sampled_out, const float* uniforms, const ftts_sampling* samp,
+                            int32_t B, void* stream);
+
 /*
  * ftts_decode_step that also hands out the step's last-layer hidden state,
  * which the model's mel stage takes as a condition next to the semantic tokens

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 
+#include "decode_entry.hpp"
 #include "ftts_internal.hpp"
 
 using namespace ftts;
@@ -514,10 +515,24 @@ int ftts_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t
     return FTTS_OK;
 }
 
-static int decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
-                       const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out, float* hidden_out,
-                       int32_t* sampled_out, const float* uniforms, const ftts_sampling* samp, int32_t B, void* ws,
-                       size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace ftts {
+
+size_t decode_control_bytes() { return mega_bytes(nullptr, nullptr); }
+
+int set_error(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* positions, const ftts_page_table* pt,
+                const ftts_kv_pool* kv, float* logits_out, float* hidden_out, int32_t* sampled_out,
+                const float* uniforms, const ftts_sampling* samp, int32_t B, void* ws, size_t ws_bytes, void* stream,
+                int (*prepare)(void* ws, hipStream_t st)) {
     TRY(check_weights(w));
     if (reinterpret_cast<uintptr_t>(hidden_out) % 16) return fail(FTTS_E_ALIGN, "hidden_out must be 16-byte aligned");
     const ftts_config& c = w->cfg;
@@ -531,6 +546,7 @@ static int decode_step(const ftts_weights* w, const int32_t* tokens, const int32
     if (ws_bytes < need) return fail(FTTS_E_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
 
     hipStream_t st = (hipStream_t)stream;
+    if (prepare) TRY(prepare(ws, st));
     DecodeWs W;
     decode_bytes(c, B, &W, reinterpret_cast<char*>(ws));
     const int d = c.d_model, H = c.n_head, F = c.d_ff, V = c.vocab;
@@ -635,12 +651,16 @@ static int decode_step(const ftts_weights* w, const int32_t* tokens, const int32
     return FTTS_OK;
 }
 
+}  // namespace ftts
+
+extern "C" {
+
 int ftts_decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
                      const ftts_page_table* pt, const ftts_kv_pool* kv, float* logits_out, int32_t* sampled_out,
                      const float* uniforms, const ftts_sampling* samp, int32_t B, void* ws, size_t ws_bytes,
                      void* stream) {
     return decode_step(w, tokens, positions, pt, kv, logits_out, nullptr, sampled_out, uniforms, samp, B, ws,
-                       ws_bytes, stream);
+                       ws_bytes, stream, nullptr);
 }
 
 int ftts_decode_step_hidden(const ftts_weights* w, const int32_t* tokens, const int32_t* positions,
@@ -648,7 +668,7 @@ int ftts_decode_step_hidden(const ftts_weights* w, const int32_t* tokens, const 
                             int32_t* sampled_out, const float* uniforms, const ftts_sampling* samp, int32_t B,
                             void* ws, size_t ws_bytes, void* stream) {
     return decode_step(w, tokens, positions, pt, kv, logits_out, hidden_out, sampled_out, uniforms, samp, B, ws,
-                       ws_bytes, stream);
+                       ws_bytes, stream, nullptr);
 }
 
 // Where the prefill's input rows come from: ready embeddings, or the model's

@@ -102,6 +102,9 @@ def lib():
         L.ftts_prefill_ids.restype = _c.c_int
         L.ftts_prefill_ids.argtypes = [P(Weights), vp, P(i32), vp, P(i32), i32, i32, i32, P(PageTable), P(KvPool),
                                        vp, vp, _c.c_size_t, vp]
+        L.ftts_decode_step_static.restype = _c.c_int
+        L.ftts_decode_step_static.argtypes = [P(Weights), vp, vp, P(PageTable), P(KvPool), vp, vp, vp, P(Sampling),
+                                              i32, vp]
         L.ftts_decode_step_hidden.restype = _c.c_int
         L.ftts_decode_step_hidden.argtypes = [P(Weights), vp, vp, P(PageTable), P(KvPool), vp, vp, vp, vp,
                                               P(Sampling), i32, vp, _c.c_size_t, vp]
@@ -219,6 +222,18 @@ def decode_step(model, tokens, positions, page_table, kv, logits_out, sampled_ou
                                              _ptr(hidden_out), _ptr(sampled_out), _ptr(uniforms),
                                              _c.byref(sampling), B, _ptr(ws), ws.numel() * ws.element_size(),
                                              _stream(stream)))
+
+
+def decode_step_static(model, tokens, positions, page_table, kv, logits_out, sampled_out, uniforms,
+                       sampling: Sampling, stream=None):
+    """ftts_decode_step_static: ftts_decode_step with the library's static scratch
+    instead of a workspace (for callers that cannot allocate)."""
+    _check(lib().ftts_decode_step_static(_c.byref(model.c), _ptr(tokens), _ptr(positions), _c.byref(page_table.c),
+                                         _c.byref(kv.c), _ptr(logits_out), _ptr(sampled_out), _ptr(uniforms),
+                                         _c.byref(sampling), tokens.numel(), _stream(stream)))
+
+
+STATIC_SCRATCH_BYTES = 12 << 20
 
 
 PATH_AUTO, PATH_KERNELS, PATH_PERSISTENT = 0, 1, 2
