@@ -3,41 +3,46 @@
 //
 // Why: at batch 1 one step is about 121 dependent phases (5 per layer plus the
 // head) over 0.97 GB of bf16 weights.  Separate kernels pay a launch gap and a
-// cold memory ramp per phase; here one launch covers the whole step, and each
-// workgroup's weight share for a phase is already in LDS when that phase's
-// input arrives.
+// cold memory ramp per phase; here one launch covers the whole step.
 //
-// Layout: one 512-thread workgroup per CU (256).  Waves 0-6 compute; wave 7 only
-// moves weights: it copies each phase's share of a weight matrix into LDS with
-// direct global->LDS loads one or two phases ahead (none while attention runs:
-// the FC1 share goes out once every attention partial is done).  A wave's vector loads
-// retire in issue order, so keeping the weight stream in a wave of its own is
-// what lets the compute waves' polls, parameter loads and KV page loads return
-// without waiting behind it.  The copy wave takes part in every workgroup
-// barrier (it learns the outcome of each poll round from LDS) and, before the
-// barrier that releases a phase's dot products, waits with an explicit vmcnt for
-// the share that phase needs, leaving the next share in flight.
-// Workgroup barriers are bare s_barrier (plus an LDS wait), never __syncthreads,
-// whose memory fence would wait for every outstanding load of the wave.
+// Layout: one 512-thread workgroup per CU (256), in two roles.
+//  * Attention groups, one per (sequence, head) (the first B x 20 groups), do
+//    only attention: all 8 waves hold the sequence's cached KV pages of the
+//    head (one page per wave in registers, one more per wave in LDS), loaded
+//    for layer l + 1 as soon as layer l's output is published, so when the new
+//    token's q, k, v arrive only arithmetic is left.  Each publishes its head's
+//    normalised 64 outputs.
+//  * GEMV groups (the other 236, or 216 at batch 2) own every weight row: each
+//    takes a contiguous range of the rows of every matrix (16-18 q/k/v rows,
+//    5-6 out-projection rows, 21-24 FC1 rows, 5-6 FC2 rows, 34-48 LM-head rows).
+//    Waves 0-6 compute; wave 7 only moves weights: it copies each phase's share
+//    of a weight matrix into LDS with direct global->LDS loads, a phase or more
+//    ahead, at points where no exchange of the group is waiting behind them.
+//    A wave's vector loads retire in issue order, so keeping the weight stream
+//    in a wave of its own lets the compute waves' polls and parameter loads
+//    return without waiting behind it.  The copy wave takes part in every
+//    workgroup barrier and, before the barrier that releases a phase's dot
+//    products, waits with an explicit vmcnt for the share that phase needs.
+// Workgroup barriers are bare s_barrier (plus an LDS wait), never
+// __syncthreads, whose memory fence would wait for every outstanding load.
 //
 // Exchange: every value crossing workgroups travels as one 64-bit word
 // (fp32 value | epoch << 32) written and read with device-coherent (sc1)
 // accesses.  A consumer knows its data has arrived when every word carries the
 // epoch of the current (step, event); no flags, counters or fences are needed.
-// Each phase depends on all workgroups of the previous one, so a single buffer
+// Each phase depends on all producers of the previous one, so a single buffer
 // per kind of data is never overwritten before every reader has consumed it.
 // Waits are bounded: on timeout a workgroup raises the abort word and every
 // workgroup leaves at its next wait (ftts_check_workspace reports it).
 //
-// Work split per layer (rows of a matrix split evenly over the 256 groups):
-//   P0  LN1 + q/k/v rows (15 per group), k/v also appended to the KV pool
-//   P1  attention, one group per (sequence, head); the new token's k/v come from
-//       the exchange, older slots from the pool (written by earlier launches)
-//   P2  out-proj rows (5 per group) + residual of the group's own x rows
-//   P3  LN2 + FC1 rows (20 per group) + GELU
-//   P4  FC2 rows (5 per group) + residual
-// then LN_f + LM head rows (<= 40 per group) and, for greedy decoding, the
-// argmax over all groups' candidates.
+// Per layer (GEMV groups; activations enter the dot products as bf16):
+//   P0  LN1 + q/k/v rows, k/v also appended to the KV pool
+//   P1  (attention groups) attention over the cached pages and the new token
+//   P2  out-proj rows + residual of the group's own x rows
+//   P3  LN2 + FC1 rows + GELU
+//   P4  FC2 rows + residual
+// then LN_f + LM head rows and, for greedy decoding, the argmax over every
+// GEMV group's candidates.
 #include "gemv_impl.hpp"
 #include "kv_page.hpp"
 
@@ -45,12 +50,27 @@ namespace ftts {
 namespace mega {
 
 constexpr int NT = 512;                    // threads per workgroup (8 waves)
-constexpr int NC = 448;                    // compute threads (waves 0-6)
+constexpr int NC = 448;                    // compute threads of a GEMV group (waves 0-6)
 constexpr int NWC = NC / 64;               // compute waves
 constexpr int DW = NWC;                    // the copy wave
+constexpr int NAW = NT / 64;               // attention waves of an attention group
 constexpr unsigned kSpinLimit = 1u << 19;  // about a second of polling
-constexpr int kBuf = 51200;                // one LDS weight buffer: 20 x 1280 or 5 x 5120 bf16
-constexpr int kHeadRowsMax = 2 * kBuf / (2 * D);  // LM-head rows a group holds (both buffers)
+constexpr int kBuf = 61440;                // one LDS weight buffer: 24 x 1280 or 6 x 5120 bf16
+constexpr int kPageBytes = 2 * kPage * kHeadDim * 2;  // one page of one head: K then V, bf16
+constexpr int kLdsPages = 2 * kBuf / kPageBytes;       // pages an attention group stages in LDS (7)
+static_assert(kLdsPages < NAW, "one staged page per wave at most");
+
+// Workgroups per role for a kernel instantiated for batches up to BMAX.
+template <int BMAX> struct Roles {
+    static constexpr int NA = BMAX * NH;  // attention groups
+    static constexpr int NG = G - NA;     // GEMV groups
+};
+// Rows [r0, r0 + n) of an N-row matrix held by GEMV group k of NG.
+__device__ __forceinline__ void rows_of(int N, int k, int NG, int& r0, int& n) {
+    r0 = (int)((long long)N * k / NG);
+    n = (int)((long long)N * (k + 1) / NG) - r0;
+}
+constexpr int max_rows(int N, int NG) { return (N + NG - 1) / NG; }
 
 template <int WT> struct Tiles;  // (lanes per row, 16-byte chunks per lane) per phase, <= NC threads
 template <> struct Tiles<FTTS_BF16> {
@@ -66,27 +86,31 @@ constexpr int HL = 8, HC = 20;  // LM head (bf16)
 
 template <int WT, int K>
 constexpr int row_bytes() { return WT == FTTS_W4A16 ? K / 2 : WT == FTTS_W8A16 ? K : 2 * K; }
-// Direct-to-LDS instructions the copy wave issues for `bytes` (1 KB each).
+// Direct-to-LDS instructions (1 KB each) that copy `bytes`.
 constexpr int dma_ops(int bytes) { return (bytes + 1023) / 1024; }
-template <int WT> struct Ops {  // per share, fixed by the shape: rows per group = 15, 5, 20, 5
-    static constexpr int PQ = dma_ops(3 * D / G * row_bytes<WT, D>());
-    static constexpr int PO = dma_ops(D / G * row_bytes<WT, D>());
-    static constexpr int P1 = dma_ops(FF / G * row_bytes<WT, D>());
-    static constexpr int P2 = dma_ops(D / G * row_bytes<WT, FF>());
+// Every share of a phase is copied with the same number of instructions (that of
+// the largest), so the copy wave's vmcnt waits are compile-time constants.
+template <int WT, int BMAX> struct Ops {
+    static constexpr int NG = Roles<BMAX>::NG;
+    static constexpr int PQ = dma_ops(max_rows(3 * D, NG) * row_bytes<WT, D>());
+    static constexpr int PO = dma_ops(max_rows(D, NG) * row_bytes<WT, D>());
+    static constexpr int P1 = dma_ops(max_rows(FF, NG) * row_bytes<WT, D>());
+    static constexpr int P2 = dma_ops(max_rows(D, NG) * row_bytes<WT, FF>());
     static_assert(PQ <= 63 && PO <= 63 && P1 <= 63 && P2 <= 63, "vmcnt holds 63");
-    static_assert(3 * D / G * row_bytes<WT, D>() <= kBuf && FF / G * row_bytes<WT, D>() <= kBuf &&
-                      D / G * row_bytes<WT, FF>() <= kBuf, "share exceeds an LDS buffer");
+    static_assert(PQ * 1024 <= kBuf && PO * 1024 <= kBuf && P1 * 1024 <= kBuf && P2 * 1024 <= kBuf,
+                  "share exceeds an LDS buffer");
+    static_assert(max_rows(3 * D, NG) * 16 <= NC && max_rows(FF, NG) * 16 <= NC && max_rows(D, NG) * 64 <= NC,
+                  "a phase's rows fit the compute threads");
 };
-static_assert(3 * D % G == 0 && D % G == 0 && FF % G == 0, "rows split evenly over the groups");
-static_assert(D + NH * kMaxSplit * kPartWords <= FF, "merged o and the attention partials share s_in");
-static_assert(BM * NH * kMaxSplit <= G, "attention groups fit the grid");
-static_assert(BM * NH * kMaxSplit <= kDoneStride && kDoneReplicas + 2 <= 64, "done-word layout");
+constexpr int kHeadRowsPerBuf = kBuf / (2 * D);  // LM-head rows in one buffer
+static_assert(BM * NH < G, "attention groups leave GEMV groups");
+static_assert(2 * kHeadRowsPerBuf * (G - BM * NH) >= 10240, "LM-head rows of the largest vocabulary fit");
 
-// Optional phase timeline (built only with FTTS_MEGA_TRACE): thread 0 of each
-// group stamps the 100 MHz wall clock at fixed points of every layer.
+// Optional phase timeline (built only with FTTS_MEGA_TRACE): thread 0 of wave 0
+// and of wave 7 stamps the 100 MHz wall clock at fixed points of every layer.
 constexpr int kMarksPerLayer = 20, kMarkSlots = 1 + 50 * kMarksPerLayer + 8;
 #ifdef FTTS_MEGA_TRACE
-__device__ unsigned long long g_mega_marks[G][2][kMarkSlots];  // [group][compute wave 0 | copy wave]
+__device__ unsigned long long g_mega_marks[G][2][kMarkSlots];  // [group][wave 0 | wave 7]
 #define MEGA_MARK(slot)                                                                                   \
     do {                                                                                                  \
         if ((threadIdx.x & 63) == 0 && threadIdx.x / 64 % 7 == 0)                                          \
@@ -128,20 +152,33 @@ __device__ __forceinline__ void wait_vm() {
 
 typedef __attribute__((address_space(3))) char lds_char;
 
+
 // Copy wave: rows [r0, r0 + nrows) of a row-major matrix (row_b bytes a row,
-// 16-byte aligned) into LDS, 1 KB per instruction.  Lanes past the end repeat
-// the last 16 bytes, so up to 1 KB - 16 bytes past the share are written.
+// 16-byte aligned) into LDS with exactly OPS instructions of 1 KB.  Lanes past
+// the share repeat its last 16 bytes, so OPS KB are written in all.
+template <int OPS>
 __device__ __forceinline__ void dma_rows(const void* W, int row_b, int r0, int nrows, char* dst) {
     const int lane = threadIdx.x & 63;
     const int n = nrows * row_b >> 4;
     const char* s = reinterpret_cast<const char*>(W) + (size_t)r0 * row_b;
     lds_char* d = (lds_char*)(dst);
-    for (int c0 = 0; c0 < n; c0 += 64) {
-        const int c = min(c0 + lane, n - 1);
+#pragma unroll 2
+    for (int i = 0; i < OPS; ++i) {
+        const int c = min(i * 64 + lane, n - 1);
         // cache policy 2 = nt: weights are read once per step, and streaming them
         // non-temporally keeps them from evicting the exchange words being polled
-        __builtin_amdgcn_global_load_lds(s + (size_t)c * 16, d + c0 * 16, 16, 0, 2);
+        __builtin_amdgcn_global_load_lds(s + (size_t)c * 16, d + i * 1024, 16, 0, 2);
     }
+}
+
+// One 8 KB block (one head's keys or values of one page) into LDS.
+__device__ __forceinline__ void dma_block(const void* src, char* dst) {
+    const int lane = threadIdx.x & 63;
+    const char* s = reinterpret_cast<const char*>(src);
+    lds_char* d = (lds_char*)(dst);
+#pragma unroll
+    for (int c0 = 0; c0 < kPage * kHeadDim * 2 / 16; c0 += 64)
+        __builtin_amdgcn_global_load_lds(s + (size_t)(c0 + lane) * 16, d + c0 * 16, 16, 0, 0);
 }
 
 // Workgroup agreement on a failed wait: a flag in LDS, set by any wave that
@@ -164,55 +201,23 @@ __device__ __forceinline__ void give_up(const Sync& sy, uint32_t* ctl) {
     }
 }
 
-// Compute waves: wait until the n exchange words all carry `epoch` and leave their
-// values in dst (LDS); idx(j) maps value j to its word.  Each wave polls its own
-// words (device-scope relaxed atomic loads) with two rounds in flight -- the next
-// round goes out before the previous one is checked, re-reading only words not
-// yet seen -- so a word is picked up about half a round trip after it lands
-// rather than up to a full one.  The workgroup then meets at one barrier.
-// Returns false when a wave's wait ran out or another group gave up.
-//
-// With sentinels (sent.n > 0, at most 64), wave 0 first polls only those
-// consecutive words (one per producer, stored after its data; each group reads
-// the replica of its own index mod kDoneReplicas, so that the many waiting groups
-// do not all hammer the same few lines), the workgroup meets at a barrier, and
-// then every wave reads its share of the full set.  A group that waits through a
-// long phase thus sends one small request per round instead of many.
-struct NoSentinels {
-    static constexpr int n = 0;
-    const uint64_t* w = nullptr;
-};
-struct Sentinels {
-    const uint64_t* w;  // n consecutive words
-    int n;
-};
-template <int U, typename Idx, typename Sent = NoSentinels>
-__device__ __forceinline__ bool gather(const uint64_t* src, int n, Idx idx, uint32_t epoch, float* dst, uint32_t* ctl,
-                                       Sync& sy, Sent sent = Sent{}, int mark = -1) {
+__device__ __forceinline__ void store_to(float* dst, int j, float v) { dst[j] = v; }
+__device__ __forceinline__ void store_to(uint16_t* dst, int j, float v) { dst[j] = f32_to_bf16(v); }
+
+// The NTH threads that poll: wait until the n exchange words all carry `epoch`
+// and leave their values in dst (LDS, fp32 or rounded to bf16); idx(j) maps value
+// j to its word.  Each wave polls its own words (device-scope relaxed atomic
+// loads) with two rounds in flight -- the next round goes out before the
+// previous one is checked, re-reading only words not yet seen -- so a word is
+// picked up about half a round trip after it lands rather than up to a full
+// one.  The workgroup then meets at one barrier.  Returns false when a wave's
+// wait ran out or another group gave up.
+template <int U, int NTH, typename Idx, typename Dst>
+__device__ __forceinline__ bool gather(const uint64_t* src, int n, Idx idx, uint32_t epoch, Dst* dst, uint32_t* ctl,
+                                       Sync& sy) {
     const int tid = fresh_tid();
     bool failed = false;
-    if (sent.n > 0) {
-        if (tid < 64) {
-            const uint64_t* w = sent.w + min(tid, sent.n - 1);
-            unsigned spins = 0;
-            uint64_t a0 = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            while (true) {
-                const uint32_t ab = ld_agent(ctl + 1);
-                const uint64_t a1 = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (__all((uint32_t)(a0 >> 32) == epoch)) break;
-                if (++spins > kSpinLimit || ab != 0) {
-                    failed = true;
-                    break;
-                }
-                a0 = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (__all((uint32_t)(a1 >> 32) == epoch)) break;
-            }
-            if (failed && tid == 0) give_up(sy, ctl);
-        }
-        bar();
-        failed = *sy.fail != 0;
-    }
-    for (int base = 0; base < n && !failed; base += NC * U) {
+    for (int base = 0; base < n && !failed; base += NTH * U) {
         uint64_t va[U], vb[U];
         bool seen[U];
 #pragma unroll
@@ -222,7 +227,7 @@ __device__ __forceinline__ bool gather(const uint64_t* src, int n, Idx idx, uint
         auto issue = [&](uint64_t (&v)[U]) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int j = min(base + tid + NC * u, n - 1);
+                const int j = min(base + tid + NTH * u, n - 1);
                 v[u] = __hip_atomic_load(src + idx(j), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         };
@@ -232,8 +237,8 @@ __device__ __forceinline__ bool gather(const uint64_t* src, int n, Idx idx, uint
             for (int u = 0; u < U; ++u) {
                 if (!seen[u] && (uint32_t)(v[u] >> 32) == epoch) {
                     seen[u] = true;
-                    const int j = base + tid + NC * u;
-                    if (j < n) dst[j] = __uint_as_float((uint32_t)v[u]);
+                    const int j = base + tid + NTH * u;
+                    if (j < n) store_to(dst, j, __uint_as_float((uint32_t)v[u]));
                 }
                 all = all && seen[u];
             }
@@ -253,7 +258,6 @@ __device__ __forceinline__ bool gather(const uint64_t* src, int n, Idx idx, uint
             if (take(vb)) break;
         }
     }
-    if (mark >= 0) MEGA_MARK(mark + 1);
     if (failed && (tid & 63) == 0) give_up(sy, ctl);
     bar();
     return *sy.fail == 0;
@@ -268,13 +272,18 @@ __device__ __forceinline__ bool follow(Sync& sy) {
     return *sy.fail == 0;
 }
 
-// One phase's share of a weight matrix: rows [r0, r0 + R) in an LDS buffer
-// (copied there by the copy wave); per-row bias and quantisation parameters of
-// this thread's row in registers.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+// a.x * b.x + a.y * b.y + c over packed bf16 pairs, accumulated in fp32
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c,
+                                           false);
+}
+
 // W4A16 dot of one 4-byte chunk (8 codes, columns 8c .. 8c+7, one quantisation
-// group): the zero-point enters through the chunk's own activation sum.
+// group) with 8 bf16 activations: the zero-point enters through the chunk's own
+// activation sum.
 template <int B_>
-__device__ __forceinline__ void dot_w4_word(uint32_t word, const float* xs, int stride, int B, float (&acc)[B_],
+__device__ __forceinline__ void dot_w4_word(uint32_t word, const uint16_t* xs, int stride, int B, float (&acc)[B_],
                                             float s4, float z4) {
     float wf[8];
 #pragma unroll
@@ -282,19 +291,56 @@ __device__ __forceinline__ void dot_w4_word(uint32_t word, const float* xs, int 
 #pragma unroll
     for (int b = 0; b < B_; ++b) {
         if (b < B) {
-            const float4 x0 = *reinterpret_cast<const float4*>(xs + b * stride);
-            const float4 x1 = *reinterpret_cast<const float4*>(xs + b * stride + 4);
+            const uint4 xv = *reinterpret_cast<const uint4*>(xs + b * stride);
+            const float x[8] = {bf16lo(xv.x), bf16hi(xv.x), bf16lo(xv.y), bf16hi(xv.y),
+                                bf16lo(xv.z), bf16hi(xv.z), bf16lo(xv.w), bf16hi(xv.w)};
             float t = 0.f;
-            t = fmaf(wf[0], x0.x, t);
-            t = fmaf(wf[1], x0.y, t);
-            t = fmaf(wf[2], x0.z, t);
-            t = fmaf(wf[3], x0.w, t);
-            t = fmaf(wf[4], x1.x, t);
-            t = fmaf(wf[5], x1.y, t);
-            t = fmaf(wf[6], x1.z, t);
-            t = fmaf(wf[7], x1.w, t);
-            const float sx = ((x0.x + x0.y) + (x0.z + x0.w)) + ((x1.x + x1.y) + (x1.z + x1.w));
+#pragma unroll
+            for (int i = 0; i < 8; ++i) t = fmaf(wf[i], x[i], t);
+            const float sx = ((x[0] + x[1]) + (x[2] + x[3])) + ((x[4] + x[5]) + (x[6] + x[7]));
             acc[b] = fmaf(s4, fmaf(-z4, sx, t), acc[b]);
+        }
+    }
+}
+
+// One 16-byte weight chunk (8 bf16 or 16 int8 weights) against bf16 activations.
+template <int WT, int B_>
+__device__ __forceinline__ void dot_chunk16(const uint4 wv, const uint16_t* xs, int stride, int B, float (&acc)[B_]) {
+    if constexpr (WT == FTTS_BF16) {
+#pragma unroll
+        for (int b = 0; b < B_; ++b) {
+            if (b < B) {
+                const uint4 xv = *reinterpret_cast<const uint4*>(xs + b * stride);
+                float t = acc[b];
+                t = dot2_bf16(wv.x, xv.x, t);
+                t = dot2_bf16(wv.y, xv.y, t);
+                t = dot2_bf16(wv.z, xv.z, t);
+                t = dot2_bf16(wv.w, xv.w, t);
+                acc[b] = t;
+            }
+        }
+    } else {  // FTTS_W8A16: 16 int8 codes
+        const uint32_t wd[4] = {wv.x, wv.y, wv.z, wv.w};
+        float wf[16];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) wf[4 * j + i] = (float)(int32_t)((int32_t)(wd[j] << (24 - 8 * i)) >> 24);
+        }
+#pragma unroll
+        for (int b = 0; b < B_; ++b) {
+            if (b < B) {
+                const uint4 x0 = *reinterpret_cast<const uint4*>(xs + b * stride);
+                const uint4 x1 = *reinterpret_cast<const uint4*>(xs + b * stride + 8);
+                const uint32_t xw[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+                float t = acc[b];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    t = fmaf(wf[2 * e], bf16lo(xw[e]), t);
+                    t = fmaf(wf[2 * e + 1], bf16hi(xw[e]), t);
+                }
+                acc[b] = t;
+            }
         }
     }
 }
@@ -333,9 +379,9 @@ struct Share {
             }
         }
     }
-    // acc[b] = dot product of this thread's row with s_in[b] (+ bias); every lane of the row gets it.
+    // acc[b] = dot product of this thread's row with the bf16 row s_in[b] (+ bias); every lane of the row gets it.
     template <int B_>
-    __device__ __forceinline__ void dot(const float* s_in, int B, float (&acc)[B_]) const {
+    __device__ __forceinline__ void dot(const uint16_t* s_in, int B, float (&acc)[B_]) const {
         const int t = fresh_tid();
         const int li = t & (LPR - 1);
         const int slot = min(t / LPR, R - 1);
@@ -355,7 +401,7 @@ struct Share {
 #pragma unroll
             for (int i = 0; i < NCH; ++i) {
                 const int c = li + i * LPR;
-                dot_chunk<WT, B_>(wrow[c], s_in + c * EPC, K, B, acc, 0.f, 0.f, nullptr, 0);
+                dot_chunk16<WT, B_>(wrow[c], s_in + c * EPC, K, B, acc);
             }
         }
 #pragma unroll
@@ -373,12 +419,14 @@ struct LnCols {
     }
 };
 
-// LayerNorm of the B rows of s_x into s_in.  Thread t < 320 (waves 0-4) normalises columns
+// LayerNorm of the B rows of s_x into s_in (bf16, the linears' input; the
+// optional hid receives the same rows in fp32).  Thread t < 320 (waves 0-4) normalises columns
 // 4t .. 4t+3 of every row, so consecutive lanes touch consecutive LDS words;
 // each of those waves forms every row's mean and variance itself, so no
 // barrier is needed until the result is complete.
 template <int BMAX>
-__device__ __forceinline__ void layer_norm(const float* s_x, float* s_in, const LnCols& ln, float eps, int B) {
+__device__ __forceinline__ void layer_norm(const float* s_x, uint16_t* s_in, const LnCols& ln, float eps, int B,
+                                           float* hid = nullptr) {
     const int tid = fresh_tid(), lane = tid & 63;
     if (tid >= D / 4) return;  // whole waves
 #pragma unroll
@@ -409,7 +457,11 @@ __device__ __forceinline__ void layer_norm(const float* s_x, float* s_in, const 
             y.y = fmaf((v.y - m) * r, bf16hi(ln.g.x), bf16hi(ln.b.x));
             y.z = fmaf((v.z - m) * r, bf16lo(ln.g.y), bf16lo(ln.b.y));
             y.w = fmaf((v.w - m) * r, bf16hi(ln.g.y), bf16hi(ln.b.y));
-            *reinterpret_cast<float4*>(s_in + b * D + tid * 4) = y;
+            uint2 pk;
+            pk.x = (uint32_t)f32_to_bf16(y.x) | ((uint32_t)f32_to_bf16(y.y) << 16);
+            pk.y = (uint32_t)f32_to_bf16(y.z) | ((uint32_t)f32_to_bf16(y.w) << 16);
+            *reinterpret_cast<uint2*>(s_in + b * D + tid * 4) = pk;
+            if (hid) *reinterpret_cast<float4*>(hid + b * D + tid * 4) = y;  // fp32, before rounding
         }
     }
 }
@@ -462,73 +514,191 @@ __device__ __forceinline__ void attend_page(PageRegs<false>& pg, bool ok, int p,
 
 template <int BMAX> constexpr int ux() { return (BMAX * D + NC - 1) / NC; }           // words per thread: x, o
 template <int BMAX> constexpr int uh() { return (BMAX * FF + NC - 1) / NC < 12 ? (BMAX * FF + NC - 1) / NC : 12; }  // h
-template <int BMAX> constexpr int uo() {  // attention partials, S <= kMaxSplit
-    return (BMAX * NH * kMaxSplit * kPartWords + NC - 1) / NC;
-}
 template <int BMAX> constexpr int ua() { return (G * BMAX * 2 + NC - 1) / NC; }        // argmax candidates
 
-// The copy wave's program: every share copy, and the barriers of the compute
-// waves' program in the same order.
-template <int WT, int BMAX>
-__device__ __forceinline__ void copy_wave(const Args& a, char* s_w, Sync& sy) {
-    using O = Ops<WT>;
-    const int wg = blockIdx.x, B = a.B;
-    const int q0 = 3 * D / G * wg, d0 = D / G * wg, f0 = FF / G * wg;
-    const int v0 = a.V * wg / G, nv = a.V * (wg + 1) / G - v0;
-    const int nA = min(nv, kBuf / (2 * D));
-    const bool is_att = wg < B * NH * a.att_split;
-    constexpr int RD = row_bytes<WT, D>(), RF = row_bytes<WT, FF>();
+// An attention group: sequence b, head h, all 8 waves.  Wave w attends to the
+// sequence's cached pages w, w + 8, w + 16, ...: the first in registers and the
+// second (waves 0-6) in an LDS slot, both requested for layer l + 1 as soon as
+// layer l's output is out, so a step's attention waits only for the new
+// token's q, k, v; further pages (contexts beyond 15 pages) are read in turn.
+template <int BMAX>
+__device__ __forceinline__ void attention_group(const Args& a, int b, int h, int ncache, bool active, uint32_t step,
+                                                char* s_w, float* s_q, float* s_pm, float* s_pl,
+                                                float (*s_po)[kHeadDim], Sync& sy) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int grp = lane >> 3, sub = lane & 7;
+    auto E = [&](int ev) { return (step << 8) | (uint32_t)ev; };
+    const int npg = (ncache + kPage - 1) / kPage;
+    const int32_t* bt = a.block_table + (size_t)b * a.max_pages;
+    // lane j holds the physical id of this wave's j-th page (page wave + 8 j)
+    const int lp = wave + NAW * lane;
+    const int my_phys = lp < npg ? bt[lp] : -1;
+    const int my_pages = npg > wave ? (npg - wave + NAW - 1) / NAW : 0;
+    const bool staged = wave < kLdsPages && my_pages > 1;  // this wave's second page comes through LDS
+    char* slot = s_w + wave * kPageBytes;
+    auto bases = [&](int l, int j, size_t& kb, size_t& vb) {
+        int phys = __builtin_amdgcn_readlane(my_phys, j);
+        const bool ok = phys >= 0 && phys < a.n_pages;
+        phys = ok ? phys : 0;
+        kb = kv_offset(l, a.n_pages, phys, 0, NH, h, 0);
+        vb = kv_offset(l, a.n_pages, phys, 1, NH, h, 0);
+        return ok;
+    };
+    PageRegs<false> cur;
+    bool ok0 = false;
+    auto prefetch = [&](int l) {
+        size_t kb, vb;
+        if (my_pages > 0) {
+            ok0 = bases(l, 0, kb, vb);
+            load_page<false>(a.kv, kb, vb, lane, cur);
+        }
+        if (staged) {
+            bases(l, 1, kb, vb);
+            const uint16_t* kv = reinterpret_cast<const uint16_t*>(a.kv);
+            dma_block(kv + kb, slot);
+            dma_block(kv + vb, slot + kPageBytes / 2);
+        }
+    };
+    prefetch(0);
+    const uint64_t* src = a.ex_qkv + (size_t)b * 3 * D + h * 64;
+    auto seg = [](int j) { return (j >> 6) * D + (j & 63); };  // q, k, v of head h
+    for (int l = 0; l < a.n_layer; ++l) {
+        MEGA_LMARK(l, 0);
+        if (!gather<1, NT>(src, 3 * 64, seg, E(5 * l + 1), s_q, a.ctl, sy)) return;
+        MEGA_LMARK(l, 1);
+        float q[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) q[j] = s_q[sub * 8 + j] * 0.125f;  // 1/sqrt(64), exact
+        // The cache holds keys and values in bf16; attend to the new token as cached.
+        auto cached = [](float v) { return bf16_to_f32(f32_to_bf16(v)); };
+        float m = -INFINITY, lsum = 0.f, o[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[j] = 0.f;
+        if (wave == 0 && active) {  // the new token itself, straight from the exchange
+            float t = 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) t = fmaf(q[j], cached(s_q[64 + sub * 8 + j]), t);
+            m = group_sum<8>(t);
+            if (grp == 0) {
+                lsum = 1.f;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) o[j] = cached(s_q[128 + sub * 8 + j]);
+            }
+        }
+        if (my_pages > 0) attend_page(cur, ok0, wave, ncache, q, grp, m, lsum, o);
+        for (int j = 1; j < my_pages; ++j) {
+            size_t kb, vb;
+            const bool ok = bases(l, j, kb, vb);
+            if (j == 1 && staged) {
+                wait_vm<0>();  // this wave's own copy of the page has landed
+                const uint4* pg = reinterpret_cast<const uint4*>(slot);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) cur.k[i] = pg[i * 64 + lane];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) cur.v[i] = pg[kPageBytes / 32 + i * 64 + lane];
+            } else {
+                load_page<false>(a.kv, kb, vb, lane, cur);
+            }
+            attend_page(cur, ok, wave + NAW * j, ncache, q, grp, m, lsum, o);
+        }
+        MEGA_LMARK(l, 2);
+#pragma unroll
+        for (int d = 0; d < 8; ++d) o[d] = stride8_sum(o[d]);
+        lsum = stride8_sum(lsum);
+        if (lane < 8) {
+#pragma unroll
+            for (int d = 0; d < 8; ++d) s_po[wave][lane * 8 + d] = o[d];
+        }
+        if (lane == 0) {
+            s_pm[wave] = m;
+            s_pl[wave] = lsum;
+        }
+        bar();  // wave partials in LDS; every wave is done with its LDS page
+        if (wave == 0) {  // log-sum-exp merge of the wave partials: the head's output, normalised
+            float M = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < NAW; ++i) M = fmaxf(M, s_pm[i]);
+            float L = 0.f, acc = 0.f;
+#pragma unroll
+            for (int i = 0; i < NAW; ++i) {
+                if (s_pm[i] > -INFINITY) {
+                    const float wgt = expf(s_pm[i] - M);
+                    L = fmaf(s_pl[i], wgt, L);
+                    acc = fmaf(s_po[i][lane], wgt, acc);
+                }
+            }
+            put(a.ex_o + (size_t)b * D + h * 64 + lane, E(5 * l + 2), (active && L > 0.f) ? acc / L : 0.f);
+        }
+        MEGA_LMARK(l, 3);
+        bar();  // the head's output is on its way before any page request of the next layer
+        if (l + 1 < a.n_layer) prefetch(l + 1);
+    }
+    wait_vm<0>();
+}
 
-    dma_rows(a.qkv_w.at(0), RD, q0, 3 * D / G, s_w);
+// The copy wave of a GEMV group: every share copy, and the barriers of the
+// compute waves' program in the same order.  Shares: q/k/v rows and FC1 rows
+// alternate in buffer 0, out-projection and FC2 rows in buffer 1; each is
+// requested right after a gather completes (or, FC1, while attention runs),
+// never just before one, so that no exchange's polls wait behind it.
+template <int WT, int BMAX>
+__device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync& sy) {
+    using O = Ops<WT, BMAX>;
+    constexpr int NG = Roles<BMAX>::NG;
+    constexpr int RD = row_bytes<WT, D>(), RF = row_bytes<WT, FF>();
+    constexpr int HO = dma_ops(kHeadRowsPerBuf * 2 * D);
+    int q0, nq, d0, nd, f0, nf, v0, nv;
+    rows_of(3 * D, k, NG, q0, nq);
+    rows_of(D, k, NG, d0, nd);
+    rows_of(FF, k, NG, f0, nf);
+    rows_of(a.V, k, NG, v0, nv);
+    const int nA = min(nv, kHeadRowsPerBuf);
+
+    dma_rows<O::PQ>(a.qkv_w.at(0), RD, q0, nq, s_w);
     for (int l = 0; l < a.n_layer; ++l) {
         // P0
         bar();
         MEGA_LMARK(l, 0);
         if (l == 0) bar();
-        else if (!follow(sy)) goto out;
-        dma_rows(a.out_w.at(l), RD, d0, D / G, s_w + kBuf);
+        else if (!follow(sy)) goto out;  // x gathered
+        dma_rows<O::PO>(a.out_w.at(l), RD, d0, nd, s_w + kBuf);
         wait_vm<O::PO>();  // q/k/v share in LDS
         MEGA_LMARK(l, 1);
         bar();             // LN1 done
-        // P1
-        bar();
+        // P1: the FC1 share goes out while attention runs
+        bar();             // the q/k/v share has been read
         MEGA_LMARK(l, 2);
-        if (!is_att) dma_rows(a.fc1_w.at(l), RD, f0, FF / G, s_w);
-        if (is_att) {
-            if (!follow(sy)) goto out;
-            bar();  // wave partials in LDS
-        }
-        // P2
-        if (is_att) wait_vm<0>(); else wait_vm<O::P1>();  // out-proj share in LDS
+        dma_rows<O::P1>(a.fc1_w.at(l), RD, f0, nf, s_w);
+        wait_vm<O::P1>();  // out-proj share in LDS
         MEGA_LMARK(l, 3);
-        if (!follow(sy)) goto out;
-        if (is_att) dma_rows(a.fc1_w.at(l), RD, f0, FF / G, s_w);
+        if (!follow(sy)) goto out;  // o of every head gathered
         // P3
-        bar();
+        bar();  // the out-proj share has been read
         MEGA_LMARK(l, 4);
-        if (!follow(sy)) goto out;
-        dma_rows(a.fc2_w.at(l), RF, d0, D / G, s_w + kBuf);
+        if (!follow(sy)) goto out;  // x gathered
+        dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + kBuf);
         wait_vm<O::P2>();  // FC1 share in LDS
         MEGA_LMARK(l, 5);
         bar();             // LN2 done
         // P4
-        bar();
+        bar();  // the FC1 share has been read
         MEGA_LMARK(l, 6);
         wait_vm<0>();  // FC2 share in LDS
         MEGA_LMARK(l, 7);
-        if (!follow(sy)) goto out;
-        if (l + 1 < a.n_layer) dma_rows(a.qkv_w.at(l + 1), RD, q0, 3 * D / G, s_w);
-        else dma_rows(a.head_w, 2 * D, v0, nA, s_w);
+        if (!follow(sy)) goto out;  // h gathered
+        if (l + 1 < a.n_layer) dma_rows<O::PQ>(a.qkv_w.at(l + 1), RD, q0, nq, s_w);
+        else dma_rows<HO>(a.head_w, 2 * D, v0, nA, s_w);
     }
     // head
-    bar();
-    if (nv > nA) dma_rows(a.head_w, 2 * D, v0 + nA, nv - nA, s_w + kBuf);
-    if (!follow(sy)) goto out;
+    bar();  // the FC2 share has been read
+    if (nv > nA) dma_rows<HO>(a.head_w, 2 * D, v0 + nA, nv - nA, s_w + kBuf);
+    if (!follow(sy)) goto out;  // x gathered
     wait_vm<0>();
     bar();  // LN_f done
     if (a.greedy) {
         bar();  // candidates in LDS
-        if (wg == 0) follow(sy);
+        if (k == 0) follow(sy);
     }
 out:
     wait_vm<0>();
@@ -537,11 +707,12 @@ out:
 template <int WT, int BMAX>
 __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
     using T = Tiles<WT>;
-    __shared__ __attribute__((aligned(1024))) char s_w[2 * kBuf];     // weight shares, two buffers
-    __shared__ __attribute__((aligned(16))) float s_in[BMAX * FF];    // phase input (normalised for LN phases)
+    constexpr int NA = Roles<BMAX>::NA, NG = Roles<BMAX>::NG;
+    __shared__ __attribute__((aligned(1024))) char s_w[2 * kBuf];     // weight shares / staged KV pages
+    __shared__ __attribute__((aligned(16))) uint16_t s_in[BMAX * FF];  // phase input, bf16 (normalised for LN phases)
     __shared__ __attribute__((aligned(16))) float s_x[BMAX * D];      // residual stream as last gathered
     __shared__ __attribute__((aligned(16))) float s_q[3 * 64];        // attention: q, k, v of the new token
-    __shared__ float s_pm[NWC], s_pl[NWC], s_po[NWC][64];             // attention wave partials
+    __shared__ float s_pm[NAW], s_pl[NAW], s_po[NAW][kHeadDim];       // attention wave partials
     __shared__ float s_cv[BMAX][NC / HL];                             // head: per-slot best value
     __shared__ int s_ci[BMAX][NC / HL];                               //       and its row
     __shared__ int s_active[BMAX], s_tok[BMAX], s_pos[BMAX], s_slot[BMAX], s_phys[BMAX];  // per sequence
@@ -584,65 +755,52 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
     if (s_abort) return;
     Sync sy{&s_fail, a.sampled, a.active_out, B};
     MEGA_MARK(0);
+    if (wg < NA) {
+        const int b = wg / NH, h = wg % NH;
+        const bool act = b < B && s_active[b];
+        attention_group<BMAX>(a, b, h, act ? s_slot[b] : 0, act, step, s_w, s_q, s_pm, s_pl, s_po, sy);
+        return;
+    }
+    const int k = wg - NA;  // GEMV group index
     if (wave == DW) {
-        copy_wave<WT, BMAX>(a, s_w, sy);
+        copy_wave<WT, BMAX>(a, k, s_w, sy);
         return;
     }
 
-    const int q0 = 3 * D / G * wg, q1 = q0 + 3 * D / G;
-    const int d0 = D / G * wg, d1 = d0 + D / G;
-    const int f0 = FF / G * wg, f1 = f0 + FF / G;
-    const int v0 = a.V * wg / G, v1 = a.V * (wg + 1) / G;
-    // Attention: S groups per (sequence, head); split s takes the sequence's pages
-    // s, s + S, s + 2S, ..., and its wave w every seventh of those from the w-th.
-    const int S = a.att_split;
-    const bool is_att = wg < B * NH * S;
-    const int att_b = wg / (NH * S), att_h = wg / S % NH, att_s = wg % S;
-
+    int q0, nq, d0, nd, f0, nf, v0, nv;
+    rows_of(3 * D, k, NG, q0, nq);
+    rows_of(D, k, NG, d0, nd);
+    rows_of(FF, k, NG, f0, nf);
+    rows_of(a.V, k, NG, v0, nv);
     Share<WT, T::QL, T::QC, D> pq;
     Share<WT, T::OL, T::OC, D> po;
     Share<WT, T::AL, T::AC, D> p1;
     Share<WT, T::BL, T::BC, FF> p2;
     const int sq = tid / T::QL, so = tid / T::OL, s1 = tid / T::AL, s2 = tid / T::BL, sh = tid / HL;
     LnCols ln;
-    pq.params(a.qkv_s.at(0), a.qkv_z.at(0), a.qkv_b.at(0), q0, q1 - q0, s_w);
-    // Attention groups: the sequence's cached slots (the new token excluded) are
-    // the same in every layer; this wave's pages are wave, wave + 7, ... and lane
-    // j holds the physical id of its j-th (and j+64-th) one.
-    int ncache = 0, my_pages = 0, my_phys0 = -1, my_phys1 = -1;
-    if (is_att && s_active[att_b]) {
-        ncache = s_slot[att_b];
-        const int npg = (ncache + kPage - 1) / kPage;
-        const int nsplit = npg > att_s ? (npg - att_s + S - 1) / S : 0;  // pages of this split
-        const int32_t* bt = a.block_table + (size_t)att_b * a.max_pages;
-        const int lp0 = att_s + S * (wave + NWC * lane), lp1 = att_s + S * (wave + NWC * (lane + 64));
-        my_phys0 = lp0 < npg ? bt[lp0] : -1;
-        my_phys1 = lp1 < npg ? bt[lp1] : -1;
-        my_pages = nsplit > wave ? (nsplit - wave + NWC - 1) / NWC : 0;
-    }
+    pq.params(a.qkv_s.at(0), a.qkv_z.at(0), a.qkv_b.at(0), q0, nq, s_w);
 
     for (int l = 0; l < a.n_layer; ++l) {
         // ---------------- P0: LN1 + q/k/v -------------------------------------------------
         bar();  // P4's reads of s_w[1], s_in and s_x are done
         MEGA_LMARK(l, 0);
         ln.load(a.ln1_g.at(l), a.ln1_b.at(l));
-        po.params(a.out_s.at(l), a.out_z.at(l), a.out_b.at(l), d0, d1 - d0, s_w + kBuf);
+        po.params(a.out_s.at(l), a.out_z.at(l), a.out_b.at(l), d0, nd, s_w + kBuf);
         if (l == 0) {  // the embedding, computed locally by every group
             for (int b = 0; b < B; ++b) {
                 const bool act = s_active[b];
                 const int t = s_tok[b], p = s_pos[b];
-                for (int k = tid; k < D; k += NC)
-                    s_x[b * D + k] = act ? ld_act<false>(a.tok_emb, (size_t)t * D + k) +
-                                               ld_act<false>(a.pos_emb, (size_t)p * D + k)
+                for (int c = tid; c < D; c += NC)
+                    s_x[b * D + c] = act ? ld_act<false>(a.tok_emb, (size_t)t * D + c) +
+                                               ld_act<false>(a.pos_emb, (size_t)p * D + c)
                                          : 0.f;
             }
             bar();
-        } else if (!gather<ux<BMAX>()>(a.ex_x, B * D, Flat{}, E(5 * l), s_x, a.ctl, sy)) {
+        } else if (!gather<ux<BMAX>(), NC>(a.ex_x, B * D, Flat{}, E(5 * l), s_x, a.ctl, sy)) {
             return;
         }
         MEGA_LMARK(l, 1);
         layer_norm<BMAX>(s_x, s_in, ln, a.eps, B);
-        MEGA_LMARK(l, 13);
         bar();  // s_in complete; the copy wave has waited for the q/k/v share
         MEGA_LMARK(l, 2);
         {
@@ -650,7 +808,7 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
             pq.template dot<BMAX>(s_in, B, acc);
             const int row = q0 + sq;
             const int li = tid & (T::QL - 1);
-            if (sq < q1 - q0) {
+            if (sq < nq) {
 #pragma unroll
                 for (int b = 0; b < BMAX; ++b) {
                     if (b < B && li == b) {
@@ -667,104 +825,19 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
                 }
             }
         }
-        // ---------------- P1: attention, one group per (sequence, head) ---------------------
+        // ---------------- P1 + P2: attention elsewhere; out-proj + residual ------------------
         bar();  // P0's reads of s_w[0] are done
         MEGA_LMARK(l, 3);
-        p1.params(a.fc1_s.at(l), a.fc1_z.at(l), a.fc1_b.at(l), f0, f1 - f0, s_w);
-        if (is_att) {
-            const int b = att_b, h = att_h;
-            const int grp = lane >> 3, sub = lane & 7;
-            auto bases = [&](int j, size_t& kb, size_t& vb) {
-                int phys = j < 64 ? __builtin_amdgcn_readlane(my_phys0, j & 63)
-                                  : __builtin_amdgcn_readlane(my_phys1, j & 63);
-                const bool ok = phys >= 0 && phys < a.n_pages;
-                phys = ok ? phys : 0;
-                kb = kv_offset(l, a.n_pages, phys, 0, NH, h, 0);
-                vb = kv_offset(l, a.n_pages, phys, 1, NH, h, 0);
-                return ok;
-            };
-            PageRegs<false> cur;
-            bool ok_cur = false;
-            size_t kb, vb;
-            // the first page goes out before the new token's q/k/v arrive
-            if (my_pages > 0) {
-                ok_cur = bases(0, kb, vb);
-                load_page<false>(a.kv, kb, vb, lane, cur);
-            }
-            const uint64_t* src = a.ex_qkv + (size_t)b * 3 * D + h * 64;
-            auto seg = [](int j) { return (j >> 6) * D + (j & 63); };  // q, k, v of head h
-            if (!gather<1>(src, 3 * 64, seg, E(5 * l + 1), s_q, a.ctl, sy)) return;
-            MEGA_LMARK(l, 4);
-            float q[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) q[j] = s_q[sub * 8 + j] * 0.125f;  // 1/sqrt(64), exact
-            // The cache holds keys and values in bf16; attend to the new token as cached.
-            auto cached = [](float v) { return bf16_to_f32(f32_to_bf16(v)); };
-            float m = -INFINITY, lsum = 0.f, o[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) o[j] = 0.f;
-            if (att_s == 0 && wave == 0 && s_active[b]) {  // the new token itself, straight from the exchange
-                float t = 0.f;
-#pragma unroll
-                for (int j = 0; j < 8; ++j) t = fmaf(q[j], cached(s_q[64 + sub * 8 + j]), t);
-                m = group_sum<8>(t);
-                if (grp == 0) {
-                    lsum = 1.f;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) o[j] = cached(s_q[128 + sub * 8 + j]);
-                }
-            }
-            MEGA_LMARK(l, 14);
-            for (int j = 0; j < my_pages; ++j) {
-                const int p = att_s + S * (wave + NWC * j);
-                if (j > 0) {
-                    ok_cur = bases(j, kb, vb);
-                    load_page<false>(a.kv, kb, vb, lane, cur);
-                }
-                attend_page(cur, ok_cur, p, ncache, q, grp, m, lsum, o);
-            }
-            MEGA_LMARK(l, 15);
-#pragma unroll
-            for (int d = 0; d < 8; ++d) o[d] = stride8_sum(o[d]);
-            lsum = stride8_sum(lsum);
-            if (lane < 8) {
-#pragma unroll
-                for (int d = 0; d < 8; ++d) s_po[wave][lane * 8 + d] = o[d];
-            }
-            if (lane == 0) {
-                s_pm[wave] = m;
-                s_pl[wave] = lsum;
-            }
-            MEGA_LMARK(l, 16);
-            bar();
-            MEGA_LMARK(l, 5);
-            if (wave == 0) {  // log-sum-exp merge of the wave partials: the head's output, normalised
-                float M = -INFINITY;
-#pragma unroll
-                for (int i = 0; i < NWC; ++i) M = fmaxf(M, s_pm[i]);
-                float L = 0.f, acc = 0.f;
-#pragma unroll
-                for (int i = 0; i < NWC; ++i) {
-                    if (s_pm[i] > -INFINITY) {
-                        const float wgt = expf(s_pm[i] - M);
-                        L = fmaf(s_pl[i], wgt, L);
-                        acc = fmaf(s_po[i][lane], wgt, acc);
-                    }
-                }
-                put(a.ex_o + (size_t)b * D + h * 64 + lane, E(5 * l + 2), (s_active[b] && L > 0.f) ? acc / L : 0.f);
-            }
-        }
-        // ---------------- P2: out-proj + residual --------------------------------------------
-        // o of every head, straight from the attention groups (s_in was last read
-        // by P0's dot, before P1's barrier)
-        if (!gather<ux<BMAX>()>(a.ex_o, B * D, Flat{}, E(5 * l + 2), s_in, a.ctl, sy)) return;
-        MEGA_LMARK(l, 6);
+        p1.params(a.fc1_s.at(l), a.fc1_z.at(l), a.fc1_b.at(l), f0, nf, s_w);
+        // o of every head, straight from the attention groups (s_in was last read by P0's dot)
+        if (!gather<ux<BMAX>(), NC>(a.ex_o, B * D, Flat{}, E(5 * l + 2), s_in, a.ctl, sy)) return;
+        MEGA_LMARK(l, 4);
         {
             float acc[BMAX];
             po.template dot<BMAX>(s_in, B, acc);
             const int row = d0 + so;
             const int li = tid & (T::OL - 1);
-            if (so < d1 - d0) {
+            if (so < nd) {
 #pragma unroll
                 for (int b = 0; b < BMAX; ++b)
                     if (b < B && li == b) put(a.ex_x + (size_t)b * D + row, E(5 * l + 3), s_x[b * D + row] + acc[b]);
@@ -772,20 +845,20 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         }
         // ---------------- P3: LN2 + FC1 + GELU -----------------------------------------------
         bar();  // P2's reads of s_in / s_x / s_w[1] are done
-        MEGA_LMARK(l, 7);
+        MEGA_LMARK(l, 5);
         ln.load(a.ln2_g.at(l), a.ln2_b.at(l));
-        p2.params(a.fc2_s.at(l), a.fc2_z.at(l), a.fc2_b.at(l), d0, d1 - d0, s_w + kBuf);
-        if (!gather<ux<BMAX>()>(a.ex_x, B * D, Flat{}, E(5 * l + 3), s_x, a.ctl, sy)) return;
-        MEGA_LMARK(l, 8);
+        p2.params(a.fc2_s.at(l), a.fc2_z.at(l), a.fc2_b.at(l), d0, nd, s_w + kBuf);
+        if (!gather<ux<BMAX>(), NC>(a.ex_x, B * D, Flat{}, E(5 * l + 3), s_x, a.ctl, sy)) return;
+        MEGA_LMARK(l, 6);
         layer_norm<BMAX>(s_x, s_in, ln, a.eps, B);
         bar();  // s_in complete; the copy wave has waited for the FC1 share
-        MEGA_LMARK(l, 9);
+        MEGA_LMARK(l, 7);
         {
             float acc[BMAX];
             p1.template dot<BMAX>(s_in, B, acc);
             const int row = f0 + s1;
             const int li = tid & (T::AL - 1);
-            if (s1 < f1 - f0) {
+            if (s1 < nf) {
 #pragma unroll
                 for (int b = 0; b < BMAX; ++b)
                     if (b < B && li == b) put(a.ex_h + (size_t)b * FF + row, E(5 * l + 4), gelu_tanh(acc[b]));
@@ -793,45 +866,41 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         }
         // ---------------- P4: FC2 + residual -------------------------------------------------
         bar();  // P3's reads of s_in / s_w[0] are done
-        MEGA_LMARK(l, 10);
-        if (l + 1 < a.n_layer)
-            pq.params(a.qkv_s.at(l + 1), a.qkv_z.at(l + 1), a.qkv_b.at(l + 1), q0, q1 - q0, s_w);
-        if (!gather<uh<BMAX>()>(a.ex_h, B * FF, Flat{}, E(5 * l + 4), s_in, a.ctl, sy)) return;
-        MEGA_LMARK(l, 11);
+        MEGA_LMARK(l, 8);
+        if (l + 1 < a.n_layer) pq.params(a.qkv_s.at(l + 1), a.qkv_z.at(l + 1), a.qkv_b.at(l + 1), q0, nq, s_w);
+        if (!gather<uh<BMAX>(), NC>(a.ex_h, B * FF, Flat{}, E(5 * l + 4), s_in, a.ctl, sy)) return;
+        MEGA_LMARK(l, 9);
         {
             float acc[BMAX];
             p2.template dot<BMAX>(s_in, B, acc);
             const int row = d0 + s2;
             const int li = tid & (T::BL - 1);
-            if (s2 < d1 - d0) {
+            if (s2 < nd) {
 #pragma unroll
                 for (int b = 0; b < BMAX; ++b)
                     if (b < B && li == b) put(a.ex_x + (size_t)b * D + row, E(5 * l + 5), s_x[b * D + row] + acc[b]);
             }
         }
-        MEGA_LMARK(l, 12);
+        MEGA_LMARK(l, 10);
     }
 
     // ---------------- LN_f + LM head (+ greedy argmax) -------------------------------------
     bar();  // the last FC2's reads of s_w[1] / s_in / s_x are done
     Share<FTTS_BF16, HL, HC, D> ph;
-    ph.params(nullptr, nullptr, a.head_b, v0, v1 - v0, s_w);
+    ph.params(nullptr, nullptr, a.head_b, v0, nv, s_w);
     ln.load(a.lnf_g, a.lnf_b);
-    if (!gather<ux<BMAX>()>(a.ex_x, B * D, Flat{}, E(5 * a.n_layer), s_x, a.ctl, sy)) return;
+    if (!gather<ux<BMAX>(), NC>(a.ex_x, B * D, Flat{}, E(5 * a.n_layer), s_x, a.ctl, sy)) return;
     MEGA_MARK(1 + a.n_layer * kMarksPerLayer);
-    layer_norm<BMAX>(s_x, s_in, ln, a.eps, B);
+    // the step's last-layer hidden state (every group forms the same rows; GEMV group 0 writes them)
+    layer_norm<BMAX>(s_x, s_in, ln, a.eps, B, k == 0 ? a.hidden : nullptr);
     bar();  // s_in complete; the copy wave has waited for the head share
     MEGA_MARK(2 + a.n_layer * kMarksPerLayer);
-    if (a.hidden && wg == 0) {  // the step's last-layer hidden state (every group holds the same rows)
-        for (int i = tid; i < B * D / 4; i += NC)
-            reinterpret_cast<float4*>(a.hidden)[i] = reinterpret_cast<const float4*>(s_in)[i];
-    }
     {
         float acc[BMAX];
         ph.template dot<BMAX>(s_in, B, acc);
         const int row = v0 + sh;
         const int li = tid & (HL - 1);
-        const bool mine = sh < v1 - v0;
+        const bool mine = sh < nv;
 #pragma unroll
         for (int b = 0; b < BMAX; ++b) {
             if (b < B && li == b) {
@@ -842,7 +911,7 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         }
     }
     if (!a.greedy) {
-        if (wg == 0 && tid == 0) st_agent(a.ctl, step + 1);
+        if (k == 0 && tid == 0) st_agent(a.ctl, step + 1);
         return;
     }
     bar();
@@ -857,18 +926,19 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
                 bi = i;
             }
         }
-        put(a.ex_arg + ((size_t)wg * B + tid) * 2, E(5 * a.n_layer + 1), bv);
-        put(a.ex_arg + ((size_t)wg * B + tid) * 2 + 1, E(5 * a.n_layer + 1), __int_as_float(bi));
+        put(a.ex_arg + ((size_t)k * B + tid) * 2, E(5 * a.n_layer + 1), bv);
+        put(a.ex_arg + ((size_t)k * B + tid) * 2 + 1, E(5 * a.n_layer + 1), __int_as_float(bi));
     }
-    if (wg != 0) return;
-    if (!gather<ua<BMAX>()>(a.ex_arg, G * B * 2, Flat{}, E(5 * a.n_layer + 1), s_in, a.ctl, sy)) return;
+    if (k != 0) return;
+    float* s_cand = reinterpret_cast<float*>(s_w);  // the head share has been read (barrier above)
+    if (!gather<ua<BMAX>(), NC>(a.ex_arg, NG * B * 2, Flat{}, E(5 * a.n_layer + 1), s_cand, a.ctl, sy)) return;
     if (wave < B) {
         const int b = wave;
         float bv = -INFINITY;
         int bi = 0x7FFFFFFF;
-        for (int g = lane; g < G; g += 64) {
-            const float v = s_in[(g * B + b) * 2];
-            const int i = __float_as_int(s_in[(g * B + b) * 2 + 1]);
+        for (int g = lane; g < NG; g += 64) {
+            const float v = s_cand[(g * B + b) * 2];
+            const int i = __float_as_int(s_cand[(g * B + b) * 2 + 1]);
             if (v > bv || (v == bv && i < bi)) {
                 bv = v;
                 bi = i;

@@ -616,9 +616,10 @@ def test_persistent_step_split_attention(torch_cuda, decode_path, mid_master, mo
 
 
 def test_persistent_step_agrees_with_kernel_path(torch_cuda, decode_path, mid_master):
-    """Same inputs through both decode implementations: logits agree to fp32
-    reduction-order noise, and the persistent step is independent of where the
-    pages live and bit-reproducible."""
+    """Same inputs through both decode implementations (the persistent step takes
+    its linears' inputs in bf16, the per-phase GEMVs in fp32): both agree with
+    the oracle within the bf16 bar, and the persistent step is independent of
+    where the pages live and bit-reproducible."""
     from paper_2607_21042_amd import ftts
     inputs = model_inputs(MID, "bf16", mid_master)
     lens = [100, 37]
@@ -639,8 +640,9 @@ def test_persistent_step_agrees_with_kernel_path(torch_cuda, decode_path, mid_ma
     rp = helpers.run_gpu(dm, MID, prefixes, fed, block_table=bt0, n_pages=n_pages)
     rq = helpers.run_gpu(dm, MID, prefixes, fed, block_table=bt1, n_pages=n_pages)
     ftts.check_workspace(rq["ws"])
-    scale = np.max(np.abs(rk["logits"]))
-    assert np.max(np.abs(rk["logits"] - rp["logits"])) <= 1e-4 * scale
+    om = ogpt.GPT(helpers.oracle_weights(inputs, "bf16"), MID.n_head, MID.d_head, dtype=np.float32)
+    for res in (rk, rp):
+        compare_run(res, om, prefixes, fed, "bf16")
     np.testing.assert_array_equal(rp["logits"], rq["logits"])
     np.testing.assert_array_equal(rp["sampled"], rq["sampled"])
 
