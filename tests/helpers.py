@@ -42,12 +42,15 @@ def oracle_teacher_forced(model: ogpt.GPT, prefix: np.ndarray, fed: np.ndarray, 
 # One rounding to bf16 leaves a relative error uniform in +-2^-9, standard
 # deviation 2^-9 / sqrt(3) = 1.1e-3; summed with random signs over the ~4 L + 3
 # roundings a frame's velocity passes through (55 at 13 blocks) the normwise
-# relative error is about sqrt(55) * 1.1e-3 = 8e-3, and guidance of strength w
-# scales the two branches' errors by up to |w| + |1 - w| (3 at w = 2).  The bar
-# keeps a further factor of ~1 over that, at 2.5e-2; element-wise the velocity
-# (values of order 1, tails to ~4) must stay within 1e-1.
-DIT_REL_TOL = 2.5e-2
-DIT_ABS_TOL = 1e-1
+# relative error is about sqrt(55) * 1.1e-3 = 8e-3 at most, and guidance of
+# strength w scales the two branches' errors by up to |w| + |1 - w|.  Measured
+# over every DiT parity case (96M x 500 frames, 32 packed utterances, w up to 3):
+# at worst 4.0e-3 normwise and 1.8e-2 element-wise (velocities of order 1, tails
+# to ~4), below the model's estimate because the roundings partly cancel.  The
+# bars are three times the measured worst: a regression that doubles the error
+# still passes, one that multiplies it by 3 or more does not.
+DIT_REL_TOL = 1.2e-2
+DIT_ABS_TOL = 6e-2
 
 
 def dit_tolerance_ok(gpu, ref):
