@@ -57,6 +57,8 @@ def parse():
     p.add_argument("--paged", action="store_true",
                    help="the batched paged workload instead: --batch sequences (default 32) with prefix lengths "
                         "~U[128,512], targets ~U[256,768] then STOP, top-k 30 / top-p 0.8 / T 0.8 sampling")
+    p.add_argument("--eager", action="store_true",
+                   help="paged: launch every decode step directly instead of replaying HIP graphs")
     p.add_argument("--serve", action="store_true",
                    help="continuous batching instead: --requests utterances (default 64) with the --paged length "
                         "mix through --batch decode slots (default 32), chunks of 16 steps, top-k 30 sampling")
@@ -249,7 +251,7 @@ def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
     # the cap on steps per graph.
     S = ftts.graph_steps(args.graph_steps)
     graphs = []
-    for g0 in range(0, T_max, S):
+    for g0 in range(0, T_max if not args.eager else 0, S):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             for t in range(g0, min(g0 + S, T_max)):
@@ -260,6 +262,9 @@ def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
 
     class _All:
         def replay(self):
+            if args.eager:
+                for t in range(T_max):
+                    step(t)
             for g in graphs:
                 g.replay()
     graph = _All()
@@ -310,7 +315,8 @@ def paged_batch(args, torch, ftts, workload, shape, dm, mode, wdtype, inputs):
         "prefill_ms": round(job_ms - decode_ms, 3),
         "prefill": prefill_report(shape, P, float(np.mean([a.elapsed_time(b) for a, b in pevs]))),
         "wall_s": round(wall, 3),
-        "roofline": {"bound": "hbm", "kernel": f"decode step, kernel per phase ({T_max} steps, {S} per HIP graph)",
+        "roofline": {"bound": "hbm", "kernel": (f"decode step, kernel per phase ({T_max} steps, "
+                                                + ("launched eagerly)" if args.eager else f"{S} per HIP graph)")),
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "algorithmic_bytes_per_step": int(total_bytes / T_max),
