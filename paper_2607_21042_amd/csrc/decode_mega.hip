@@ -71,6 +71,14 @@ __device__ __forceinline__ void rows_of(int N, int k, int NG, int& r0, int& n) {
     n = (int)((long long)N * (k + 1) / NG) - r0;
 }
 constexpr int max_rows(int N, int NG) { return (N + NG - 1) / NG; }
+// The same for FC1, in whole pairs of rows: its outputs cross the device two
+// bf16 values to an exchange word, so no word straddles two groups.
+__device__ __forceinline__ void pair_rows_of(int N, int k, int NG, int& r0, int& n) {
+    rows_of(N / 2, k, NG, r0, n);
+    r0 *= 2;
+    n *= 2;
+}
+constexpr int max_pair_rows(int N, int NG) { return 2 * max_rows(N / 2, NG); }
 
 template <int WT> struct Tiles;  // (lanes per row, 16-byte chunks per lane) per phase, <= NC threads
 template <> struct Tiles<FTTS_BF16> {
@@ -94,12 +102,12 @@ template <int WT, int BMAX> struct Ops {
     static constexpr int NG = Roles<BMAX>::NG;
     static constexpr int PQ = dma_ops(max_rows(3 * D, NG) * row_bytes<WT, D>());
     static constexpr int PO = dma_ops(max_rows(D, NG) * row_bytes<WT, D>());
-    static constexpr int P1 = dma_ops(max_rows(FF, NG) * row_bytes<WT, D>());
+    static constexpr int P1 = dma_ops(max_pair_rows(FF, NG) * row_bytes<WT, D>());
     static constexpr int P2 = dma_ops(max_rows(D, NG) * row_bytes<WT, FF>());
     static_assert(PQ <= 63 && PO <= 63 && P1 <= 63 && P2 <= 63, "vmcnt holds 63");
     static_assert(PQ * 1024 <= kBuf && PO * 1024 <= kBuf && P1 * 1024 <= kBuf && P2 * 1024 <= kBuf,
                   "share exceeds an LDS buffer");
-    static_assert(max_rows(3 * D, NG) * 16 <= NC && max_rows(FF, NG) * 16 <= NC && max_rows(D, NG) * 64 <= NC,
+    static_assert(max_rows(3 * D, NG) * 16 <= NC && max_pair_rows(FF, NG) * 16 <= NC && max_rows(D, NG) * 64 <= NC,
                   "a phase's rows fit the compute threads");
 };
 constexpr int kHeadRowsPerBuf = kBuf / (2 * D);  // LM-head rows in one buffer
@@ -130,6 +138,12 @@ __device__ __forceinline__ void st_agent(uint32_t* p, uint32_t v) {
 __device__ __forceinline__ void put(uint64_t* p, uint32_t epoch, float v) {
     __hip_atomic_store(p, ((uint64_t)epoch << 32) | __float_as_uint(v), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Two values as bf16 in one exchange word: lo in the low half (the even column).
+__device__ __forceinline__ void put2(uint64_t* p, uint32_t epoch, float lo, float hi) {
+    const uint32_t v = (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+    __hip_atomic_store(p, ((uint64_t)epoch << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // threadIdx.x as a value the compiler cannot prove loop-invariant: addresses
@@ -201,8 +215,11 @@ __device__ __forceinline__ void give_up(const Sync& sy, uint32_t* ctl) {
     }
 }
 
-__device__ __forceinline__ void store_to(float* dst, int j, float v) { dst[j] = v; }
-__device__ __forceinline__ void store_to(uint16_t* dst, int j, float v) { dst[j] = f32_to_bf16(v); }
+// A word's 32 value bits into LDS: an fp32 value as is or rounded to bf16, or a
+// pair of bf16 values as they were packed.
+__device__ __forceinline__ void store_to(float* dst, int j, uint32_t v) { dst[j] = __uint_as_float(v); }
+__device__ __forceinline__ void store_to(uint16_t* dst, int j, uint32_t v) { dst[j] = f32_to_bf16(__uint_as_float(v)); }
+__device__ __forceinline__ void store_to(uint32_t* dst, int j, uint32_t v) { dst[j] = v; }
 
 // The NTH threads that poll: wait until the n exchange words all carry `epoch`
 // and leave their values in dst (LDS, fp32 or rounded to bf16); idx(j) maps value
@@ -238,7 +255,7 @@ __device__ __forceinline__ bool gather(const uint64_t* src, int n, Idx idx, uint
                 if (!seen[u] && (uint32_t)(v[u] >> 32) == epoch) {
                     seen[u] = true;
                     const int j = base + tid + NTH * u;
-                    if (j < n) store_to(dst, j, __uint_as_float((uint32_t)v[u]));
+                    if (j < n) store_to(dst, j, (uint32_t)v[u]);
                 }
                 all = all && seen[u];
             }
@@ -512,8 +529,9 @@ __device__ __forceinline__ void attend_page(PageRegs<false>& pg, bool ok, int p,
     }
 }
 
-template <int BMAX> constexpr int ux() { return (BMAX * D + NC - 1) / NC; }           // words per thread: x, o
-template <int BMAX> constexpr int uh() { return (BMAX * FF + NC - 1) / NC < 12 ? (BMAX * FF + NC - 1) / NC : 12; }  // h
+template <int BMAX> constexpr int ux() { return (BMAX * D + NC - 1) / NC; }           // words per thread: x
+template <int BMAX> constexpr int uo() { return (BMAX * D / 2 + NC - 1) / NC; }       // o (bf16 pairs)
+template <int BMAX> constexpr int uh() { return (BMAX * FF / 2 + NC - 1) / NC < 12 ? (BMAX * FF / 2 + NC - 1) / NC : 12; }  // h (bf16 pairs)
 template <int BMAX> constexpr int ua() { return (G * BMAX * 2 + NC - 1) / NC; }        // argmax candidates
 
 // An attention group: sequence b, head h, all 8 waves.  Wave w attends to the
@@ -628,7 +646,9 @@ __device__ __forceinline__ void attention_group(const Args& a, int b, int h, int
                     acc = fmaf(s_po[i][lane], wgt, acc);
                 }
             }
-            put(a.ex_o + (size_t)b * D + h * 64 + lane, E(5 * l + 2), (active && L > 0.f) ? acc / L : 0.f);
+            const float ov = (active && L > 0.f) ? acc / L : 0.f;
+            const float on = __shfl_down(ov, 1, kWave);
+            if (!(lane & 1)) put2(a.ex_o + ((size_t)b * D + h * 64 + lane) / 2, E(5 * l + 2), ov, on);
         }
         MEGA_LMARK(l, 3);
         bar();  // the head's output is on its way before any page request of the next layer
@@ -651,7 +671,7 @@ __device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync&
     int q0, nq, d0, nd, f0, nf, v0, nv;
     rows_of(3 * D, k, NG, q0, nq);
     rows_of(D, k, NG, d0, nd);
-    rows_of(FF, k, NG, f0, nf);
+    pair_rows_of(FF, k, NG, f0, nf);
     rows_of(a.V, k, NG, v0, nv);
     const int nA = min(nv, kHeadRowsPerBuf);
 
@@ -770,7 +790,7 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
     int q0, nq, d0, nd, f0, nf, v0, nv;
     rows_of(3 * D, k, NG, q0, nq);
     rows_of(D, k, NG, d0, nd);
-    rows_of(FF, k, NG, f0, nf);
+    pair_rows_of(FF, k, NG, f0, nf);
     rows_of(a.V, k, NG, v0, nv);
     Share<WT, T::QL, T::QC, D> pq;
     Share<WT, T::OL, T::OC, D> po;
@@ -830,7 +850,9 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         MEGA_LMARK(l, 3);
         p1.params(a.fc1_s.at(l), a.fc1_z.at(l), a.fc1_b.at(l), f0, nf, s_w);
         // o of every head, straight from the attention groups (s_in was last read by P0's dot)
-        if (!gather<ux<BMAX>(), NC>(a.ex_o, B * D, Flat{}, E(5 * l + 2), s_in, a.ctl, sy)) return;
+        if (!gather<uo<BMAX>(), NC>(a.ex_o, B * D / 2, Flat{}, E(5 * l + 2), reinterpret_cast<uint32_t*>(s_in), a.ctl,
+                                    sy))
+            return;
         MEGA_LMARK(l, 4);
         {
             float acc[BMAX];
@@ -856,19 +878,24 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         {
             float acc[BMAX];
             p1.template dot<BMAX>(s_in, B, acc);
-            const int row = f0 + s1;
+            const int row = f0 + s1;  // even for even s1: the row pair (s1, s1 + 1) sits in one wave
             const int li = tid & (T::AL - 1);
-            if (s1 < nf) {
+            static_assert(64 % (2 * T::AL) == 0, "an FC1 row pair within a wave");
 #pragma unroll
-                for (int b = 0; b < BMAX; ++b)
-                    if (b < B && li == b) put(a.ex_h + (size_t)b * FF + row, E(5 * l + 4), gelu_tanh(acc[b]));
+            for (int b = 0; b < BMAX; ++b) {
+                const float g = gelu_tanh(acc[b]);
+                const float gn = __shfl_down(g, T::AL, kWave);
+                if (b < B && li == b && !(s1 & 1) && s1 < nf)
+                    put2(a.ex_h + ((size_t)b * FF + row) / 2, E(5 * l + 4), g, gn);
             }
         }
         // ---------------- P4: FC2 + residual -------------------------------------------------
         bar();  // P3's reads of s_in / s_w[0] are done
         MEGA_LMARK(l, 8);
         if (l + 1 < a.n_layer) pq.params(a.qkv_s.at(l + 1), a.qkv_z.at(l + 1), a.qkv_b.at(l + 1), q0, nq, s_w);
-        if (!gather<uh<BMAX>(), NC>(a.ex_h, B * FF, Flat{}, E(5 * l + 4), s_in, a.ctl, sy)) return;
+        if (!gather<uh<BMAX>(), NC>(a.ex_h, B * FF / 2, Flat{}, E(5 * l + 4), reinterpret_cast<uint32_t*>(s_in), a.ctl,
+                                    sy))
+            return;
         MEGA_LMARK(l, 9);
         {
             float acc[BMAX];
