@@ -26,9 +26,10 @@
 // Workgroup barriers are bare s_barrier (plus an LDS wait), never
 // __syncthreads, whose memory fence would wait for every outstanding load.
 //
-// Exchange: every value crossing workgroups travels as one 64-bit word
-// (fp32 value | epoch << 32) written and read with device-coherent (sc1)
-// accesses.  A consumer knows its data has arrived when every word carries the
+// Exchange: every value crossing workgroups travels in a 64-bit word
+// (32 value bits | epoch << 32) written and read with device-coherent (sc1)
+// accesses; the value bits are one fp32 (residual stream, q/k/v) or two bf16
+// (attention and FC1 outputs, which only ever enter a linear as bf16).  A consumer knows its data has arrived when every word carries the
 // epoch of the current (step, event); no flags, counters or fences are needed.
 // Each phase depends on all producers of the previous one, so a single buffer
 // per kind of data is never overwritten before every reader has consumed it.
@@ -109,6 +110,23 @@ template <int WT, int BMAX> struct Ops {
                   "share exceeds an LDS buffer");
     static_assert(max_rows(3 * D, NG) * 16 <= NC && max_pair_rows(FF, NG) * 16 <= NC && max_rows(D, NG) * 64 <= NC,
                   "a phase's rows fit the compute threads");
+};
+// LDS of a GEMV group's weight shares.  For bf16 weights at batch 1 there are
+// three regions -- A: q/k/v then FC1, B: out-projection, C: FC2 -- so every
+// share of a layer but q/k/v can be requested while attention runs; otherwise
+// FC2 follows the out-projection in B (the quantised shares are small enough
+// to go out after a gather without holding up the next barrier for long, and
+// measured faster that way).  The LM head takes [0, kBuf) and [kBuf, 2 kBuf)
+// once the last layer's shares have been read.
+template <int WT, int BMAX> struct Lds {
+    using O = Ops<WT, BMAX>;
+    static constexpr bool kThree = BMAX == 1 && WT == FTTS_BF16;
+    static constexpr int kA = (O::PQ > O::P1 ? O::PQ : O::P1) * 1024;
+    static constexpr int kOffB = kThree ? kA : kBuf;
+    static constexpr int kEnd = kOffB + (O::PO + O::P2) * 1024;
+    static constexpr int kBytes = kThree && kEnd > 2 * kBuf ? kEnd : 2 * kBuf;
+    static constexpr int kOffC = kThree ? kBytes - O::P2 * 1024 : kBuf;  // C at the top
+    static_assert(!kThree || kOffB + O::PO * 1024 <= kOffC, "regions apart");
 };
 constexpr int kHeadRowsPerBuf = kBuf / (2 * D);  // LM-head rows in one buffer
 static_assert(BM * NH < G, "attention groups leave GEMV groups");
@@ -302,20 +320,32 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
 template <int B_>
 __device__ __forceinline__ void dot_w4_word(uint32_t word, const uint16_t* xs, int stride, int B, float (&acc)[B_],
                                             float s4, float z4) {
-    float wf[8];
+    // Codes c0..c7 sit at bits 4i, so c_i and c_{i+4} are 16 bits apart: masking
+    // the word shifted by 4i with 0x000F000F and setting 0x4300 in both halves
+    // gives the bf16 pair (128 + c_i, 128 + c_{i+4}), exactly.  The products
+    // with x are exact too, and the 128 is taken out with the chunk's sum of x.
+    uint32_t cp[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) wf[i] = (float)((word >> (4 * i)) & 0xFu);
+    for (int i = 0; i < 4; ++i) cp[i] = ((word >> (4 * i)) & 0x000F000Fu) | 0x43004300u;
+    constexpr uint32_t kOnes = 0x3F803F80u;  // bf16 (1, 1)
 #pragma unroll
     for (int b = 0; b < B_; ++b) {
         if (b < B) {
             const uint4 xv = *reinterpret_cast<const uint4*>(xs + b * stride);
-            const float x[8] = {bf16lo(xv.x), bf16hi(xv.x), bf16lo(xv.y), bf16hi(xv.y),
-                                bf16lo(xv.z), bf16hi(xv.z), bf16lo(xv.w), bf16hi(xv.w)};
-            float t = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) t = fmaf(wf[i], x[i], t);
-            const float sx = ((x[0] + x[1]) + (x[2] + x[3])) + ((x[4] + x[5]) + (x[6] + x[7]));
-            acc[b] = fmaf(s4, fmaf(-z4, sx, t), acc[b]);
+            // (x_i, x_{i+4}) pairs from the (x_2j, x_2j+1) pairs in LDS
+            const uint32_t x04 = __builtin_amdgcn_perm(xv.z, xv.x, 0x05040100u);
+            const uint32_t x15 = __builtin_amdgcn_perm(xv.z, xv.x, 0x07060302u);
+            const uint32_t x26 = __builtin_amdgcn_perm(xv.w, xv.y, 0x05040100u);
+            const uint32_t x37 = __builtin_amdgcn_perm(xv.w, xv.y, 0x07060302u);
+            float t = dot2_bf16(cp[0], x04, 0.f);
+            t = dot2_bf16(cp[1], x15, t);
+            t = dot2_bf16(cp[2], x26, t);
+            t = dot2_bf16(cp[3], x37, t);
+            float sx = dot2_bf16(xv.x, kOnes, 0.f);
+            sx = dot2_bf16(xv.y, kOnes, sx);
+            sx = dot2_bf16(xv.z, kOnes, sx);
+            sx = dot2_bf16(xv.w, kOnes, sx);
+            acc[b] = fmaf(s4, fmaf(-(128.f + z4), sx, t), acc[b]);
         }
     }
 }
@@ -489,8 +519,8 @@ __device__ __forceinline__ void layer_norm(const float* s_x, uint16_t* s_in, con
 // invalid page, may hold anything (NaN included): their scores are replaced by
 // -inf (a select, so a NaN key never reaches the max) and, on a page that has
 // such slots, their values are zeroed first, so 0 * value stays 0.
-__device__ __forceinline__ void attend_page(PageRegs<false>& pg, bool ok, int p, int ncache, const float (&q)[8],
-                                            int grp, float& m, float& lsum, float (&o)[8]) {
+__device__ __forceinline__ void attend_page(PageRegs<false>& pg, bool ok, int p, int ncache, const uint32_t (&qh)[4],
+                                            const uint32_t (&ql)[4], int grp, float& m, float& lsum, float (&o)[8]) {
     if (!(ok && (p + 1) * kPage <= ncache)) {
 #pragma unroll
         for (int i = 0; i < 8; ++i)
@@ -500,11 +530,17 @@ __device__ __forceinline__ void attend_page(PageRegs<false>& pg, bool ok, int p,
     float pm = -INFINITY;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        float kv[8];
-        unpack8<false>(pg, false, i, kv);
-        float t = 0.f;
-#pragma unroll
-        for (int d = 0; d < 8; ++d) t = fmaf(q[d], kv[d], t);
+        // bf16 key pairs against the query's bf16 high and low halves: the
+        // products are exact and q = hi + lo to about 2^-17 of its size
+        const uint4 kw = pg.k[i];
+        float t = dot2_bf16(kw.x, qh[0], 0.f);
+        t = dot2_bf16(kw.y, qh[1], t);
+        t = dot2_bf16(kw.z, qh[2], t);
+        t = dot2_bf16(kw.w, qh[3], t);
+        t = dot2_bf16(kw.x, ql[0], t);
+        t = dot2_bf16(kw.y, ql[1], t);
+        t = dot2_bf16(kw.z, ql[2], t);
+        t = dot2_bf16(kw.w, ql[3], t);
         t = group_sum<8>(t);
         sc[i] = (ok && p * kPage + i * 8 + grp < ncache) ? t : -INFINITY;
         pm = fmaxf(pm, sc[i]);
@@ -588,6 +624,14 @@ __device__ __forceinline__ void attention_group(const Args& a, int b, int h, int
         float q[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) q[j] = s_q[sub * 8 + j] * 0.125f;  // 1/sqrt(64), exact
+        uint32_t qh[4], ql[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint16_t h0 = f32_to_bf16(q[2 * j]), h1 = f32_to_bf16(q[2 * j + 1]);
+            qh[j] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+            ql[j] = (uint32_t)f32_to_bf16(q[2 * j] - bf16_to_f32(h0)) |
+                    ((uint32_t)f32_to_bf16(q[2 * j + 1] - bf16_to_f32(h1)) << 16);
+        }
         // The cache holds keys and values in bf16; attend to the new token as cached.
         auto cached = [](float v) { return bf16_to_f32(f32_to_bf16(v)); };
         float m = -INFINITY, lsum = 0.f, o[8];
@@ -604,7 +648,7 @@ __device__ __forceinline__ void attention_group(const Args& a, int b, int h, int
                 for (int j = 0; j < 8; ++j) o[j] = cached(s_q[128 + sub * 8 + j]);
             }
         }
-        if (my_pages > 0) attend_page(cur, ok0, wave, ncache, q, grp, m, lsum, o);
+        if (my_pages > 0) attend_page(cur, ok0, wave, ncache, qh, ql, grp, m, lsum, o);
         for (int j = 1; j < my_pages; ++j) {
             size_t kb, vb;
             const bool ok = bases(l, j, kb, vb);
@@ -618,7 +662,7 @@ __device__ __forceinline__ void attention_group(const Args& a, int b, int h, int
             } else {
                 load_page<false>(a.kv, kb, vb, lane, cur);
             }
-            attend_page(cur, ok, wave + NAW * j, ncache, q, grp, m, lsum, o);
+            attend_page(cur, ok, wave + NAW * j, ncache, qh, ql, grp, m, lsum, o);
         }
         MEGA_LMARK(l, 2);
 #pragma unroll
@@ -637,14 +681,15 @@ __device__ __forceinline__ void attention_group(const Args& a, int b, int h, int
             float M = -INFINITY;
 #pragma unroll
             for (int i = 0; i < NAW; ++i) M = fmaxf(M, s_pm[i]);
+            // lane i < 8 forms wave i's weight once; every lane takes the eight from them
+            const float mi = s_pm[lane & (NAW - 1)];
+            const float wl = mi > -INFINITY ? __expf(mi - M) : 0.f;
             float L = 0.f, acc = 0.f;
 #pragma unroll
             for (int i = 0; i < NAW; ++i) {
-                if (s_pm[i] > -INFINITY) {
-                    const float wgt = expf(s_pm[i] - M);
-                    L = fmaf(s_pl[i], wgt, L);
-                    acc = fmaf(s_po[i][lane], wgt, acc);
-                }
+                const float wgt = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wl), i));
+                L = fmaf(s_pl[i], wgt, L);
+                acc = fmaf(s_po[i][lane], wgt, acc);
             }
             const float ov = (active && L > 0.f) ? acc / L : 0.f;
             const float on = __shfl_down(ov, 1, kWave);
@@ -658,13 +703,19 @@ __device__ __forceinline__ void attention_group(const Args& a, int b, int h, int
 }
 
 // The copy wave of a GEMV group: every share copy, and the barriers of the
-// compute waves' program in the same order.  Shares: q/k/v rows and FC1 rows
-// alternate in buffer 0, out-projection and FC2 rows in buffer 1; each is
-// requested right after a gather completes (or, FC1, while attention runs),
-// never just before one, so that no exchange's polls wait behind it.
+// compute waves' program in the same order.  A share request holds up the
+// wave's memory operations behind it (the exchange words' polls and stores of
+// the same CU wait for the copies ahead of them, and every group's copies load
+// the memory system the exchanges cross), so where a share goes out is a trade
+// between holding up a barrier and slowing an exchange.  With three regions:
+// q/k/v while x is gathered, the out-projection during LN1, FC1 and FC2
+// together while attention runs elsewhere.  With two: FC2 waits for the
+// out-projection's buffer and goes out after x is gathered, and q/k/v of the
+// next layer once h is gathered.
 template <int WT, int BMAX>
 __device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync& sy) {
     using O = Ops<WT, BMAX>;
+    using L = Lds<WT, BMAX>;
     constexpr int NG = Roles<BMAX>::NG;
     constexpr int RD = row_bytes<WT, D>(), RF = row_bytes<WT, FF>();
     constexpr int HO = dma_ops(kHeadRowsPerBuf * 2 * D);
@@ -680,24 +731,28 @@ __device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync&
         // P0
         bar();
         MEGA_LMARK(l, 0);
+        if constexpr (L::kThree) {
+            if (l > 0) dma_rows<O::PQ>(a.qkv_w.at(l), RD, q0, nq, s_w);
+        }
         if (l == 0) bar();
         else if (!follow(sy)) goto out;  // x gathered
-        dma_rows<O::PO>(a.out_w.at(l), RD, d0, nd, s_w + kBuf);
+        dma_rows<O::PO>(a.out_w.at(l), RD, d0, nd, s_w + L::kOffB);
         wait_vm<O::PO>();  // q/k/v share in LDS
         MEGA_LMARK(l, 1);
         bar();             // LN1 done
-        // P1: the FC1 share goes out while attention runs
+        // P1: the FC1 share (and at batch 1 the FC2 share) go out while attention runs
         bar();             // the q/k/v share has been read
         MEGA_LMARK(l, 2);
         dma_rows<O::P1>(a.fc1_w.at(l), RD, f0, nf, s_w);
         wait_vm<O::P1>();  // out-proj share in LDS
+        if constexpr (L::kThree) dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + L::kOffC);
         MEGA_LMARK(l, 3);
         if (!follow(sy)) goto out;  // o of every head gathered
         // P3
         bar();  // the out-proj share has been read
         MEGA_LMARK(l, 4);
         if (!follow(sy)) goto out;  // x gathered
-        dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + kBuf);
+        if constexpr (!L::kThree) dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + L::kOffC);
         wait_vm<O::P2>();  // FC1 share in LDS
         MEGA_LMARK(l, 5);
         bar();             // LN2 done
@@ -707,11 +762,14 @@ __device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync&
         wait_vm<0>();  // FC2 share in LDS
         MEGA_LMARK(l, 7);
         if (!follow(sy)) goto out;  // h gathered
-        if (l + 1 < a.n_layer) dma_rows<O::PQ>(a.qkv_w.at(l + 1), RD, q0, nq, s_w);
-        else dma_rows<HO>(a.head_w, 2 * D, v0, nA, s_w);
+        if constexpr (!L::kThree) {
+            if (l + 1 < a.n_layer) dma_rows<O::PQ>(a.qkv_w.at(l + 1), RD, q0, nq, s_w);
+            else dma_rows<HO>(a.head_w, 2 * D, v0, nA, s_w);
+        }
     }
     // head
     bar();  // the FC2 share has been read
+    if constexpr (L::kThree) dma_rows<HO>(a.head_w, 2 * D, v0, nA, s_w);
     if (nv > nA) dma_rows<HO>(a.head_w, 2 * D, v0 + nA, nv - nA, s_w + kBuf);
     if (!follow(sy)) goto out;  // x gathered
     wait_vm<0>();
@@ -728,7 +786,8 @@ template <int WT, int BMAX>
 __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
     using T = Tiles<WT>;
     constexpr int NA = Roles<BMAX>::NA, NG = Roles<BMAX>::NG;
-    __shared__ __attribute__((aligned(1024))) char s_w[2 * kBuf];     // weight shares / staged KV pages
+    using L = Lds<WT, BMAX>;
+    __shared__ __attribute__((aligned(1024))) char s_w[L::kBytes];    // weight shares / staged KV pages
     __shared__ __attribute__((aligned(16))) uint16_t s_in[BMAX * FF];  // phase input, bf16 (normalised for LN phases)
     __shared__ __attribute__((aligned(16))) float s_x[BMAX * D];      // residual stream as last gathered
     __shared__ __attribute__((aligned(16))) float s_q[3 * 64];        // attention: q, k, v of the new token
@@ -805,7 +864,7 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         bar();  // P4's reads of s_w[1], s_in and s_x are done
         MEGA_LMARK(l, 0);
         ln.load(a.ln1_g.at(l), a.ln1_b.at(l));
-        po.params(a.out_s.at(l), a.out_z.at(l), a.out_b.at(l), d0, nd, s_w + kBuf);
+        po.params(a.out_s.at(l), a.out_z.at(l), a.out_b.at(l), d0, nd, s_w + L::kOffB);
         if (l == 0) {  // the embedding, computed locally by every group
             for (int b = 0; b < B; ++b) {
                 const bool act = s_active[b];
@@ -869,7 +928,7 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         bar();  // P2's reads of s_in / s_x / s_w[1] are done
         MEGA_LMARK(l, 5);
         ln.load(a.ln2_g.at(l), a.ln2_b.at(l));
-        p2.params(a.fc2_s.at(l), a.fc2_z.at(l), a.fc2_b.at(l), d0, nd, s_w + kBuf);
+        p2.params(a.fc2_s.at(l), a.fc2_z.at(l), a.fc2_b.at(l), d0, nd, s_w + L::kOffC);
         if (!gather<ux<BMAX>(), NC>(a.ex_x, B * D, Flat{}, E(5 * l + 3), s_x, a.ctl, sy)) return;
         MEGA_LMARK(l, 6);
         layer_norm<BMAX>(s_x, s_in, ln, a.eps, B);
