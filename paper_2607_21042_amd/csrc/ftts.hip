@@ -242,7 +242,8 @@ void gemm_scratch(const ftts_config& c, int M, size_t* part_floats, size_t* coun
                 const GemmPlan p = gemm_plan(rows, t[0], t[1]);
                 if (p.splits > 1) {
                     split = true;
-                    pf = std::max(pf, (size_t)p.splits * rows * t[0]);
+                    // partial tiles are whole (64 mt) x 128 tiles, past the matrix edges too
+                    pf = std::max(pf, (size_t)p.splits * p.tiles_m * p.tiles_n * (64 * p.mt) * 128);
                     cn = std::max(cn, (size_t)p.tiles_m * p.tiles_n);
                 }
             }
@@ -911,7 +912,8 @@ void dit_gemm_scratch(const ftts_dit_config& c, int M, size_t* part_floats, size
         for (const auto& t : NK) {
             const GemmPlan p = gemm_plan(rows, t[0], t[1]);
             if (p.splits > 1) {
-                pf = std::max(pf, (size_t)p.splits * rows * t[0]);
+                // partial tiles are whole (64 mt) x 128 tiles, past the matrix edges too
+                pf = std::max(pf, (size_t)p.splits * p.tiles_m * p.tiles_n * (64 * p.mt) * 128);
                 cn = std::max(cn, (size_t)p.tiles_m * p.tiles_n);
             }
         }

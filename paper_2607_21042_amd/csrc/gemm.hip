@@ -83,6 +83,14 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, int m, int n, f
     }
 }
 
+// The tanh GELU written as u * sigmoid(2 c (u + 0.044715 u^3)) -- the same
+// function, since 0.5 (1 + tanh z) = 1 / (1 + exp(-2 z)) -- on one exponential
+// and one hardware reciprocal (the result is rounded to bf16).
+__device__ __forceinline__ float gelu_one_exp(float u) {
+    const float c2 = 2.0f * 0.7978845608028654f;
+    return u * __builtin_amdgcn_rcpf(1.0f + __expf(-c2 * (u + 0.044715f * u * u * u)));
+}
+
 // Raw staging of one thread's share of a 128 x 64 W tile: 4 chunks of 8 k.
 template <int WT> struct WStage;
 template <> struct WStage<FTTS_BF16> { uint4 v[4]; };
@@ -91,6 +99,16 @@ template <> struct WStage<FTTS_W4A16> { uint32_t v[4]; uint16_t z[4]; };
 
 constexpr int G2N = 128, G2K = 64, G2LD = G2K + 8;  // tile columns, K step, LDS row pitch (bf16)
 constexpr int kGemmMaxSplits = 8;
+constexpr int kGemmEpiBytes = 8192;  // a wave's epilogue staging: 32 rows x 64 columns of fp32
+
+// Device-coherent 8-byte store / load (two fp32) for the split-K partials.
+__device__ __forceinline__ void st_dev2(float* p, float x, float y) {
+    const uint64_t v = (uint64_t)__float_as_uint(x) | ((uint64_t)__float_as_uint(y) << 32);
+    __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_dev2(const float* p) {
+    return __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 template <int WT>
 __device__ __forceinline__ WStage<WT> stage_w(const GemmArgs& a, int n0, int k0) {
@@ -163,23 +181,33 @@ __device__ __forceinline__ void store_stage(const AStage<AV>& ra, const WStage<W
 template <int WT, int EPI, int MT>
 __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const GemmArgs a) {
     constexpr int BM = 64 * MT, AV = BM * G2K / 8 / 256;  // A uint4 per thread per step
-    __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * G2LD];
-    __shared__ __attribute__((aligned(16))) uint16_t sB[2][G2N * G2LD];
+    constexpr int SA = BM * G2LD, SB = G2N * G2LD;          // bf16 elements of one A / W buffer
+    // both operand buffers in one array: the epilogue reuses it, 8 KB per wave
+    __shared__ __attribute__((aligned(16))) uint16_t s_ab[2 * SA + 2 * SB];
+    static_assert((2 * SA + 2 * SB) * 2 >= 4 * kGemmEpiBytes, "epilogue staging fits the operand buffers");
+    auto sA = [&](int b) { return s_ab + b * SA; };
+    auto sB = [&](int b) { return s_ab + 2 * SA + b * SB; };
     __shared__ int s_last;
     __shared__ RowSlot s_rows[EPI == EPI_QKV ? BM : 1];  // KV destination of each row of the tile
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     // Workgroups are dealt to the 8 XCDs round-robin by linear id: give each XCD a
     // contiguous run of tiles in row-major order, so the column tiles of one row
-    // block share an XCD's L2 and the activation block is fetched there once.
+    // block share an XCD's L2 and the activation block is fetched there once
+    // (column-major with at most 8 row blocks, where the weights are the bulk).
     // Every K slice of a tile maps alike, so the split-K pairing is unchanged.
     int m0, n0;
     {
         const int T = gridDim.x * gridDim.y, b = blockIdx.y * gridDim.x + blockIdx.x;
         const int x = b & 7, l = b >> 3, q = T >> 3, r = T & 7;
         const int t = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + l;
-        m0 = (t / gridDim.x) * BM;
-        n0 = (t % gridDim.x) * G2N;
+        if (gridDim.y <= 8) {  // few row blocks: a weight tile's row blocks share an XCD instead
+            m0 = (t % gridDim.y) * BM;
+            n0 = (t / gridDim.y) * G2N;
+        } else {
+            m0 = (t / gridDim.x) * BM;
+            n0 = (t % gridDim.x) * G2N;
+        }
     }
     if constexpr (EPI == EPI_QKV) {
         if (tid < BM) s_rows[tid] = row_slot(a, min(m0 + tid, a.M - 1));  // read after the first barrier
@@ -207,7 +235,7 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const GemmArgs a) {
 
     AStage<AV> ra = stage_a<AV>(A, a, m0, kb0 * G2K);
     WStage<WT> rw = stage_w<WT>(a, n0, kb0 * G2K);
-    store_stage<WT, AV>(ra, rw, sA[0], sB[0]);
+    store_stage<WT, AV>(ra, rw, sA(0), sB(0));
     __syncthreads();
     float sc[2] = {0.f, 0.f};
     for (int kt = kb0; kt < kb1; ++kt) {
@@ -228,10 +256,10 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const GemmArgs a) {
             bf16x8_t av[MT], bv[2];
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
-                av[mt] = *reinterpret_cast<const bf16x8_t*>(&sA[buf][(wm * 32 * MT + mt * 32 + fr) * G2LD + kk + fh * 8]);
+                av[mt] = *reinterpret_cast<const bf16x8_t*>(&sA(buf)[(wm * 32 * MT + mt * 32 + fr) * G2LD + kk + fh * 8]);
 #pragma unroll
             for (int nt = 0; nt < 2; ++nt)
-                bv[nt] = *reinterpret_cast<const bf16x8_t*>(&sB[buf][(wn * 64 + nt * 32 + fr) * G2LD + kk + fh * 8]);
+                bv[nt] = *reinterpret_cast<const bf16x8_t*>(&sB(buf)[(wn * 64 + nt * 32 + fr) * G2LD + kk + fh * 8]);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -255,37 +283,39 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const GemmArgs a) {
                         }
             }
         }
-        if (kt + 1 < kb1) store_stage<WT, AV>(ra, rw, sA[buf ^ 1], sB[buf ^ 1]);  // last read before the previous barrier
+        if (kt + 1 < kb1) store_stage<WT, AV>(ra, rw, sA(buf ^ 1), sB(buf ^ 1));  // last read before the previous barrier
         __syncthreads();
     }
 
     auto row_of = [&](int mt, int i) { return m0 + wm * 32 * MT + mt * 32 + (i >> 2) * 8 + fh * 4 + (i & 3); };
     if (MT == 1 && S > 1) {  // the plan splits K only with 64-row tiles
-        // partial tiles go out with device-coherent stores, waited for before the
-        // arrival count, so the last workgroup reads them without a cache flush
+        // The accumulators go out in fragment order -- pair e of thread t at
+        // (e * 256 + t) * 2, so each store instruction covers 512 contiguous bytes
+        // and the thread in the same position of the tile's last workgroup reads
+        // them back -- with device-coherent 8-byte stores waited for before the
+        // arrival count, so the last workgroup reads them without a cache flush.
+        constexpr int NV = MT * 2 * 16;
+        const int T = gridDim.x * gridDim.y, tile = blockIdx.y * gridDim.x + blockIdx.x;
+        auto slot = [&](int ss) { return a.part + ((size_t)ss * T + tile) * 256 * NV + 2 * tid; };
+        {
+            float* pp = slot(sl);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+            for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int nt = 0; nt < 2; ++nt) {
-                const int n = nt ? nl1 : nl0;
+                for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int m = row_of(mt, i);
-                    if (m < a.M && n < a.N)
-                        __hip_atomic_store(a.part + ((size_t)sl * a.M + m) * a.N + n, acc[mt][nt][i], __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-                }
-            }
+                    for (int i = 0; i < 16; i += 2)
+                        st_dev2(pp + ((mt * 2 + nt) * 8 + i / 2) * 512, acc[mt][nt][i], acc[mt][nt][i + 1]);
+        }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        const int tile = blockIdx.y * gridDim.x + blockIdx.x;
         if (tid == 0)
             s_last = __hip_atomic_fetch_add(a.count + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
                      (unsigned)(S - 1);
         __syncthreads();
         if (!s_last) return;
         // sum the S partials in slice order, RJ slices' loads in flight at a time
-        constexpr int RJ = 2;
+        constexpr int RJ = 4;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -293,21 +323,12 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const GemmArgs a) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) acc[mt][nt][i] = 0.f;
         for (int s0 = 0; s0 < S; s0 += RJ) {
-            float pv[RJ][MT][2][16];
+            uint64_t pv[RJ][NV / 2];
 #pragma unroll
             for (int j = 0; j < RJ; ++j) {
-                const int ss = min(s0 + j, S - 1);
+                const float* pp = slot(min(s0 + j, S - 1));
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                    for (int nt = 0; nt < 2; ++nt) {
-                        const int n = min(nt ? nl1 : nl0, a.N - 1);
-#pragma unroll
-                        for (int i = 0; i < 16; ++i)
-                            pv[j][mt][nt][i] = __hip_atomic_load(
-                                a.part + ((size_t)ss * a.M + min(row_of(mt, i), a.M - 1)) * a.N + n, __ATOMIC_RELAXED,
-                                __HIP_MEMORY_SCOPE_AGENT);
-                    }
+                for (int e = 0; e < NV / 2; ++e) pv[j][e] = ld_dev2(pp + e * 512);
             }
 #pragma unroll
             for (int j = 0; j < RJ; ++j)
@@ -317,10 +338,102 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const GemmArgs a) {
 #pragma unroll
                         for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-                            for (int i = 0; i < 16; ++i) acc[mt][nt][i] += pv[j][mt][nt][i];
+                            for (int i = 0; i < 16; i += 2) {
+                                const uint64_t v = pv[j][((mt * 2 + nt) * 16 + i) / 2];
+                                acc[mt][nt][i] += __uint_as_float((uint32_t)v);
+                                acc[mt][nt][i + 1] += __uint_as_float((uint32_t)(v >> 32));
+                            }
                 }
         }
         if (tid == 0) __hip_atomic_store(a.count + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+
+    if ((a.N & 7) == 0) {
+        // Epilogue through LDS (the operand buffers are free: every wave passed the
+        // loop's last barrier): each wave writes its (32 MT) x 64 sub-tile in
+        // row-major order and reads it back as 16-byte row pieces for coalesced
+        // stores -- output rows and, for q/k/v, the new keys and values into their
+        // KV pages (64 columns are one head); for the residual update x += y, 32
+        // rows at a time, all old values loaded before the stores.  Pieces are
+        // XOR-swizzled by row so that the column-wise writes of the MFMA layout do
+        // not collide in banks.
+        char* eb = reinterpret_cast<char*>(s_ab) + wave * kGemmEpiBytes;
+        const int rw0 = m0 + wm * 32 * MT, cw0 = n0 + wn * 64;
+        float bias[2], rs[2] = {1.f, 1.f};
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+            const int n = min(cw0 + nt * 32 + fr, a.N - 1);
+            bias[nt] = ld_act<false>(a.bias, n);
+            if constexpr (WT == FTTS_W8A16) rs[nt] = bf16_to_f32(a.scale[n]);
+        }
+        if constexpr (EPI != EPI_RESID) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        float y = acc[mt][nt][i] * rs[nt] + bias[nt];
+                        if constexpr (EPI == EPI_GELU) y = gelu_one_exp(y);
+                        const int rl = mt * 32 + (i >> 2) * 8 + fh * 4 + (i & 3), cl = nt * 32 + fr;
+                        *reinterpret_cast<uint16_t*>(eb + rl * 128 + (((cl >> 3) ^ (rl & 7)) << 4) + (cl & 7) * 2) =
+                            f32_to_bf16(y);
+                    }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            uint16_t* out = reinterpret_cast<uint16_t*>(a.out);
+#pragma unroll
+            for (int it = 0; it < 4 * MT; ++it) {
+                const int j = lane + 64 * it, rl = j >> 3, q = j & 7;
+                const uint4 v = *reinterpret_cast<const uint4*>(eb + rl * 128 + ((q ^ (rl & 7)) << 4));
+                const int m = rw0 + rl, n = cw0 + q * 8;
+                if (m < a.M && n < a.N) {
+                    *reinterpret_cast<uint4*>(out + (size_t)m * a.N + n) = v;
+                    if constexpr (EPI == EPI_QKV) {
+                        const int d = a.kv.d_model;
+                        const RowSlot r_s = s_rows[m - m0];
+                        if (n >= d && r_s.phys >= 0) {
+                            const int kvsel = n >= 2 * d, r = n - d - kvsel * d;
+                            const size_t off = kv_offset(a.kv.layer, a.kv.n_pages, r_s.phys, kvsel, a.kv.n_head,
+                                                         r / kHeadDim, r_s.slot) + (r % kHeadDim);
+                            *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.kv.base) + off) = v;
+                        }
+                    }
+                }
+            }
+        } else {
+            float* x = reinterpret_cast<float*>(a.out);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+                for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const int rl = (i >> 2) * 8 + fh * 4 + (i & 3), cl = nt * 32 + fr;
+                        const int sl4 = (cl >> 2) ^ (((rl >> 2) & 1) << 3);
+                        *reinterpret_cast<float*>(eb + rl * 256 + sl4 * 16 + (cl & 3) * 4) =
+                            acc[mt][nt][i] * rs[nt] + bias[nt];
+                    }
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                float4 y[8], old[8];
+#pragma unroll
+                for (int it = 0; it < 8; ++it) {
+                    const int j = lane + 64 * it, rl = j >> 4, q = j & 15;
+                    y[it] = *reinterpret_cast<const float4*>(eb + rl * 256 + ((q ^ (((rl >> 2) & 1) << 3)) << 4));
+                    const int m = min(rw0 + mt * 32 + rl, a.M - 1), n = min(cw0 + q * 4, a.N - 4);
+                    old[it] = *reinterpret_cast<const float4*>(x + (size_t)m * a.N + n);
+                }
+#pragma unroll
+                for (int it = 0; it < 8; ++it) {
+                    const int j = lane + 64 * it, rl = j >> 4, q = j & 15;
+                    const int m = rw0 + mt * 32 + rl, n = cw0 + q * 4;
+                    if (m < a.M && n < a.N)
+                        *reinterpret_cast<float4*>(x + (size_t)m * a.N + n) = make_float4(
+                            old[it].x + y[it].x, old[it].y + y[it].y, old[it].z + y[it].z, old[it].w + y[it].w);
+                }
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this pass's reads done before the next writes
+            }
+        }
+        return;
     }
 
     constexpr bool F32 = false;
@@ -421,13 +534,8 @@ __device__ __forceinline__ char* big_epi_buf(int w) {
     }
 }
 
-// The tanh GELU written as u * sigmoid(2 c (u + 0.044715 u^3)) -- the same
-// function, since 0.5 (1 + tanh z) = 1 / (1 + exp(-2 z)) -- on one exponential
-// and one hardware reciprocal (the result is rounded to bf16).
-__device__ __forceinline__ float gelu_sigmoid_form(float u) {
-    const float c2 = 2.0f * 0.7978845608028654f;
-    return u * __builtin_amdgcn_rcpf(1.0f + __expf(-c2 * (u + 0.044715f * u * u * u)));
-}
+// The GELU of the large-tile epilogue (gelu_one_exp, above).
+__device__ __forceinline__ float gelu_sigmoid_form(float u) { return gelu_one_exp(u); }
 
 // Two fp32 values to packed bf16 (round to nearest even) in one gfx950 instruction.
 __device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
