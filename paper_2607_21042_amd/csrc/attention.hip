@@ -579,6 +579,9 @@ __device__ __forceinline__ FaTile fa_tile() {
     return FaTile{(int)(t % gridDim.x), (int)(t / gridDim.x)};
 }
 
+// CAUSAL: the prefill's masked form -- query tile j sees key tiles 0 .. j only,
+// and in tile j (keys and queries aligned, 32 each) key k only for queries >= k.
+template <bool CAUSAL>
 __global__ __launch_bounds__(kFaWaves * 64, 3) void attn_full_mfma_kernel(const AttnPrefillArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t vt[kFaWaves][kHeadDim][kVtStride];
     __shared__ float mrg[kFaWaves - 1][34][64];  // waves 1..3: 32 output values, max, sum per lane
@@ -616,7 +619,9 @@ __global__ __launch_bounds__(kFaWaves * 64, 3) void attn_full_mfma_kernel(const 
             vr[2 * e + 1] = *reinterpret_cast<const uint4*>(vrow + 8);
         }
     };
-    const int nt = (len + kFaK - 1) / kFaK;
+    static_assert(kFaK == kFaQ, "the causal diagonal is one key tile");
+    const int kend = CAUSAL ? min(len, tile * kFaQ + kFaQ) : len;  // keys any query of the tile sees
+    const int nt = (kend + kFaK - 1) / kFaK;
     const int t0 = wave;
 
     pf_f32x16 o0, o1;
@@ -651,11 +656,15 @@ __global__ __launch_bounds__(kFaWaves * 64, 3) void attn_full_mfma_kernel(const 
         for (int i = 0; i < 16; ++i) s[i] = 0.f;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pf_op(kc[kk]), pf_op(qr[kk]), s, 0, 0, 0);
-        // raw scores; keys past the end exist only in a sequence's last tile
-        if (k0 + kFaK > len) {
+        // raw scores; keys past the end exist only in a sequence's last tile, and
+        // (causal) keys after the query only in the diagonal tile, whose first key
+        // every query of the tile sees
+        if (k0 + kFaK > len || (CAUSAL && t == tile)) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i)
-                if (k0 + (i >> 2) * 8 + hh * 4 + (i & 3) >= len) s[i] = -INFINITY;
+            for (int i = 0; i < 16; ++i) {
+                const int key = k0 + (i >> 2) * 8 + hh * 4 + (i & 3);
+                if (key >= len || (CAUSAL && key > qi)) s[i] = -INFINITY;
+            }
         }
         float tmax = s[0];
 #pragma unroll
@@ -889,9 +898,29 @@ __global__ __launch_bounds__(kFaWaves * 64, 2) void attn_full_shared_kernel(cons
 int prefill_tile_rows(int wdtype) { return wdtype == FTTS_F32 ? 64 : kPfQ; }
 
 hipError_t launch_attn_prefill(int wdtype, const AttnPrefillArgs& a, int total_tiles, hipStream_t st) {
-    const dim3 g(total_tiles, a.n_head);
-    if (wdtype == FTTS_F32) hipLaunchKernelGGL(attn_prefill_kernel<true>, g, dim3(64), 0, st, a);
-    else hipLaunchKernelGGL(attn_prefill_mfma_kernel, g, dim3(kPfWaves * 64), 0, st, a);
+    if (wdtype == FTTS_F32) {
+        hipLaunchKernelGGL(attn_prefill_kernel<true>, dim3(total_tiles, a.n_head), dim3(64), 0, st, a);
+        return hipGetLastError();
+    }
+    // 128-query tiles sharing each key tile once they give at least one workgroup
+    // per compute unit, else (short prefixes) 32-query tiles with the keys split
+    // over the waves, so a query tile's dependent chain is a quarter of its keys
+    constexpr int kFillGroups = 256;
+    AttnPrefillArgs b = a;
+    auto tiles = [&](int q) {
+        b.tiles_cu[0] = 0;
+        for (int i = 0; i < a.seqs.n; ++i)
+            b.tiles_cu[i + 1] = b.tiles_cu[i] + (a.seqs.cu[i + 1] - a.seqs.cu[i] + q - 1) / q;
+        return b.tiles_cu[a.seqs.n];
+    };
+    const int t128 = tiles(kPfQ);
+    if (t128 == 0) return hipSuccess;
+    if ((long)t128 * a.n_head >= kFillGroups) {
+        hipLaunchKernelGGL(attn_prefill_mfma_kernel, dim3(t128, a.n_head), dim3(kPfWaves * 64), 0, st, b);
+    } else {
+        const int t32 = tiles(kFaQ);
+        hipLaunchKernelGGL(attn_full_mfma_kernel<true>, dim3(t32, a.n_head), dim3(kFaWaves * 64), 0, st, b);
+    }
     return hipGetLastError();
 }
 
@@ -912,7 +941,7 @@ hipError_t launch_attn_full_bf16(const AttnPrefillArgs& a, hipStream_t st) {
         hipLaunchKernelGGL(attn_full_shared_kernel, dim3(t128, a.n_head), dim3(kFaWaves * 64), 0, st, b);
     } else {
         const int t32 = tiles(kFaQ);
-        hipLaunchKernelGGL(attn_full_mfma_kernel, dim3(t32, a.n_head), dim3(kFaWaves * 64), 0, st, b);
+        hipLaunchKernelGGL(attn_full_mfma_kernel<false>, dim3(t32, a.n_head), dim3(kFaWaves * 64), 0, st, b);
     }
     return hipGetLastError();
 }
