@@ -344,7 +344,10 @@ int ftts_decode_step_hidden(const ftts_weights* w, const int32_t* tokens, const 
  *   seq_lens[b] += 1 and positions[b] += 1 (the slot and position just used);
  *   if remaining != NULL, remaining[b] -= 1, and when it reaches 0 the sampled id
  *   is replaced by stop_token (in sampled[b] too) and the sequence retires:
- *   tokens[b] = -1; otherwise tokens[b] = sampled[b];
+ *   tokens[b] = -1;
+ *   if retire_on_stop != 0 and sampled[b] == stop_token, the sequence retires
+ *   too (the generation loop of Sec. II-C ends an utterance at its stop code);
+ *   otherwise tokens[b] = sampled[b];
  *   if history != NULL and *step_counter < max_steps,
  *   history[*step_counter][b] = sampled[b].
  * Sequences with tokens[b] < 0 are left unchanged (history entry -1).  When
@@ -352,8 +355,8 @@ int ftts_decode_step_hidden(const ftts_weights* w, const int32_t* tokens, const 
  * arrays of B entries (history: [max_steps][B]); 1 <= B <= 1024.
  */
 int ftts_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled,
-                 int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,
-                 int32_t max_steps, int32_t B, void* stream);
+                 int32_t* remaining, int32_t stop_token, int32_t retire_on_stop, int32_t* history,
+                 int32_t* step_counter, int32_t max_steps, int32_t B, void* stream);
 
 /*
  * The sampler of ftts_decode_step on its own: logits [B][V] fp32, uniforms [B]

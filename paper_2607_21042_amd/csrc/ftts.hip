@@ -503,15 +503,15 @@ int ftts_sample(const float* logits, int32_t B, int32_t V, const ftts_sampling* 
 }
 
 int ftts_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled, int32_t* remaining,
-                 int32_t stop_token, int32_t* history, int32_t* step_counter, int32_t max_steps, int32_t B,
-                 void* stream) {
+                 int32_t stop_token, int32_t retire_on_stop, int32_t* history, int32_t* step_counter,
+                 int32_t max_steps, int32_t B, void* stream) {
     if (!tokens || !positions || !seq_lens || !sampled) return fail(FTTS_E_INVALID_ARG, "advance: NULL pointer");
     if (B < 1 || B > 1024) return fail(FTTS_E_SHAPE, "advance: B must be in [1, 1024]");
     if (history && (max_steps < 1 || !step_counter))
         return fail(FTTS_E_INVALID_ARG, "advance: history needs step_counter and max_steps >= 1");
     (void)hipGetLastError();
-    hipError_t e = launch_advance(tokens, positions, seq_lens, sampled, remaining, stop_token, history, step_counter,
-                                  max_steps, B, (hipStream_t)stream);
+    hipError_t e = launch_advance(tokens, positions, seq_lens, sampled, remaining, stop_token, retire_on_stop != 0,
+                                  history, step_counter, max_steps, B, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "advance launch");
     return FTTS_OK;
 }

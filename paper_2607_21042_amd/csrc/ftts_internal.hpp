@@ -286,8 +286,8 @@ int prefill_tile_rows(int wdtype);  // queries per prefill-attention workgroup
 hipError_t launch_attn_full_bf16(const AttnPrefillArgs& a, hipStream_t st);
 hipError_t launch_gather_rows(const float* x, int d, const SeqTable& seqs, float* out, hipStream_t st);
 hipError_t launch_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled,
-                          int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,
-                          int max_steps, int B, hipStream_t st);
+                          int32_t* remaining, int32_t stop_token, bool retire_on_stop, int32_t* history,
+                          int32_t* step_counter, int max_steps, int B, hipStream_t st);
 hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t st);
 hipError_t launch_bgemm(int wdtype, int epi, const BgemmArgs& a, hipStream_t st);
 int bgemm_splits(int wdtype, int N, int K, bool ln);

@@ -446,8 +446,8 @@ hipError_t launch_sample(const float* logits, int B, int V, const ftts_sampling&
 // ---- generation-loop bookkeeping -----------------------------------------------------------
 __global__ __launch_bounds__(1024) void advance_kernel(int32_t* tokens, int32_t* positions, int32_t* seq_lens,
                                                        int32_t* sampled, int32_t* remaining, int32_t stop_token,
-                                                       int32_t* history, int32_t* step_counter, int max_steps,
-                                                       int B) {
+                                                       bool retire_on_stop, int32_t* history, int32_t* step_counter,
+                                                       int max_steps, int B) {
     const int step = step_counter ? *step_counter : 0;
     __syncthreads();  // every thread has read the counter before it moves
     for (int b = threadIdx.x; b < B; b += blockDim.x) {
@@ -456,17 +456,17 @@ __global__ __launch_bounds__(1024) void advance_kernel(int32_t* tokens, int32_t*
             seq_lens[b] += 1;
             positions[b] += 1;
             int next = sampled[b];
+            bool retire = retire_on_stop && next == stop_token;  // the model's own stop code
             if (remaining) {
                 const int r = remaining[b] - 1;
                 remaining[b] = r;
-                if (r <= 0) {
+                if (r <= 0) {  // the budget's last step: forced stop code
                     next = stop_token;
                     sampled[b] = stop_token;
+                    retire = true;
                 }
-                tokens[b] = r <= 0 ? -1 : next;
-            } else {
-                tokens[b] = next;
             }
+            tokens[b] = retire ? -1 : next;
             h = next;
         }
         if (history && step < max_steps) history[(size_t)step * B + b] = h;
@@ -475,10 +475,11 @@ __global__ __launch_bounds__(1024) void advance_kernel(int32_t* tokens, int32_t*
 }
 
 hipError_t launch_advance(int32_t* tokens, int32_t* positions, int32_t* seq_lens, int32_t* sampled,
-                          int32_t* remaining, int32_t stop_token, int32_t* history, int32_t* step_counter,
-                          int max_steps, int B, hipStream_t st) {
+                          int32_t* remaining, int32_t stop_token, bool retire_on_stop, int32_t* history,
+                          int32_t* step_counter, int max_steps, int B, hipStream_t st) {
     hipLaunchKernelGGL(advance_kernel, dim3(1), dim3(B < 64 ? 64 : (B + 63) / 64 * 64), 0, st, tokens, positions,
-                       seq_lens, sampled, remaining, stop_token, history, step_counter, max_steps, B);
+                       seq_lens, sampled, remaining, stop_token, retire_on_stop, history, step_counter, max_steps,
+                       B);
     return hipGetLastError();
 }
 

@@ -115,7 +115,7 @@ def lib():
         L.ftts_decode_path.restype = _c.c_int
         L.ftts_decode_path.argtypes = [P(Weights), i32]
         L.ftts_advance.restype = _c.c_int
-        L.ftts_advance.argtypes = [vp, vp, vp, vp, vp, i32, vp, vp, i32, i32, vp]
+        L.ftts_advance.argtypes = [vp, vp, vp, vp, vp, i32, i32, vp, vp, i32, i32, vp]
         L.ftts_sample.restype = _c.c_int
         L.ftts_sample.argtypes = [vp, i32, i32, P(Sampling), vp, vp, vp]
         L.ftts_dit_workspace_bytes.restype = _c.c_size_t
@@ -282,12 +282,14 @@ def graph_steps(n: int) -> int:
 
 
 def advance(tokens, positions, seq_lens, sampled, remaining=None, stop_token=0, history=None, step_counter=None,
-            stream=None):
-    """ftts_advance: device-side bookkeeping between decode steps."""
+            stream=None, retire_on_stop=False):
+    """ftts_advance: device-side bookkeeping between decode steps (retire_on_stop: a
+    sequence that samples stop_token retires at once, not only when its budget ends)."""
     B = tokens.numel()
     max_steps = history.shape[0] if history is not None else 0
     _check(lib().ftts_advance(_ptr(tokens), _ptr(positions), _ptr(seq_lens), _ptr(sampled), _ptr(remaining),
-                              stop_token, _ptr(history), _ptr(step_counter), max_steps, B, _stream(stream)))
+                              stop_token, 1 if retire_on_stop else 0, _ptr(history), _ptr(step_counter), max_steps,
+                              B, _stream(stream)))
 
 
 # --------------------------------------------------------------------------- device state

@@ -13,7 +13,9 @@ no host round trip.  Between chunks the host
 * hands the previous chunk's sampled ids (and hidden states) to each request,
   one device-to-host copy per chunk, while the current chunk already runs;
 * retires requests whose budget ran out (``ftts_advance`` forced STOP at their
-  last step and freed the slot on the device) and returns their pages;
+  last step and freed the slot on the device) or, with ``stop_on_token``, that
+  sampled the stop code (the device freed the slot at that step), and returns
+  their pages;
 * admits waiting requests into free slots: their pages (prefix + budget) come
   from the host page pool, their prefixes are prefilled together in one
   ``ftts_prefill`` call, and their slot state (START token, position 0, KV slot,
@@ -63,15 +65,20 @@ class Scheduler:
     hidden     also collect each step's last-layer hidden state (ftts_decode_step_hidden).
     graphs     replay each chunk's steps from a captured HIP graph (one per buffer parity)
                instead of launching every kernel from the host.
+    stop_on_token  end a request when it samples the stop code (stop_token, default the
+               shape's), not only when its budget runs out.
     """
 
     def __init__(self, model, shape, max_slots: int, n_pages: int, max_ctx: int, sampling, chunk: int = 16,
-                 overlap: int = 0, hidden: bool = False, max_prefill_rows: int | None = None, graphs: bool = True):
+                 overlap: int = 0, hidden: bool = False, max_prefill_rows: int | None = None, graphs: bool = True,
+                 stop_on_token: bool = False, stop_token: int | None = None):
         if chunk < 1 or overlap < 0 or overlap >= chunk:
             raise ValueError("need chunk >= 1 and 0 <= overlap < chunk")
         if graphs:
             ftts.graph_steps(chunk)                 # a chunk is one captured graph
         self.model, self.shape, self.B, self.chunk, self.overlap = model, shape, max_slots, chunk, overlap
+        self.stop_token = shape.stop_token if stop_token is None else stop_token
+        self.stop_on_token = stop_on_token
         self.sampling, self.want_hidden = sampling, hidden
         self.max_pages = (max_ctx + ftts.PAGE - 1) // ftts.PAGE
         self.pool = ftts.PagePool(n_pages)
@@ -195,7 +202,7 @@ class Scheduler:
                              self.uni[buf][t], self.sampling, self.ws,
                              hidden_out=self.hidden_buf[buf][t] if self.want_hidden else None)
             ftts.advance(self.tokens, self.positions, self.pt.seq_lens, self.sampled, self.remaining,
-                         self.shape.stop_token, self.history[buf], self.counter)
+                         self.stop_token, self.history[buf], self.counter, retire_on_stop=self.stop_on_token)
 
     def _collect(self, k: int):
         """Hand chunk k's ids to their requests; retire the finished ones."""
@@ -218,7 +225,8 @@ class Scheduler:
             if got:
                 w0 = max(0, start - self.overlap)
                 r.chunks.append((w0, np.array(r.tokens[w0:], dtype=np.int32)))
-            if len(r.tokens) >= r.max_new:       # the budget's last step forced STOP on the device
+            ended = self.stop_on_token and got and r.tokens[-1] == self.stop_token  # sampled stop code
+            if len(r.tokens) >= r.max_new or ended:  # (or the budget's last step forced it on the device)
                 r.finished_at = k
                 self.pool.release(self.slot_pages[s])
                 self.slot_pages[s] = []

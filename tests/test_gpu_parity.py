@@ -414,6 +414,27 @@ def test_advance_bookkeeping(torch_cuda):
     assert hist[:3].cpu().tolist() == ref_hist
     assert hist[3:].cpu().eq(77).all()
 
+    # retire_on_stop: a sampled stop code retires the sequence at once (budget left
+    # or no budget at all); other ids go on as before
+    for with_budget in (True, False):
+        tok = torch.tensor([3, 4, 5, -1, 7], dtype=torch.int32, device="cuda")
+        pos = torch.zeros(B, dtype=torch.int32, device="cuda")
+        lens = torch.full((B,), 8, dtype=torch.int32, device="cuda")
+        rem = torch.tensor([9, 1, 9, 9, 9], dtype=torch.int32, device="cuda") if with_budget else None
+        hist = torch.full((T, B), 77, dtype=torch.int32, device="cuda")
+        ctr = torch.zeros(1, dtype=torch.int32, device="cuda")
+        samp = torch.tensor([STOP, 11, 12, STOP, 14], dtype=torch.int32, device="cuda")
+        ftts.advance(tok, pos, lens, samp, rem, STOP, hist, ctr, retire_on_stop=True)
+        torch.cuda.synchronize()
+        # slot 0 sampled STOP; slot 1's budget ends (forced STOP); slot 3 was free
+        want_tok = [-1, -1 if with_budget else 11, 12, -1, 14]
+        want_hist = [STOP, STOP if with_budget else 11, 12, -1, 14]
+        assert tok.cpu().tolist() == want_tok, (with_budget, tok.cpu().tolist())
+        assert hist[0].cpu().tolist() == want_hist
+        assert lens.cpu().tolist() == [9, 9, 9, 8, 9] and pos.cpu().tolist() == [1, 1, 1, 0, 1]
+        if with_budget:
+            assert rem.cpu().tolist() == [8, 0, 8, 9, 8]
+
 
 def test_graph_replay_matches_eager(torch_cuda):
     """A captured HIP graph of decode+advance steps, replayed several times with
