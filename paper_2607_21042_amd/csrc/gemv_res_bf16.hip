@@ -1,4 +1,6 @@
 // Decode GEMV launchers: residual layers, FTTS_BF16 weights.
+// One weight type per translation unit: the dispatch instantiates every tiling and
+// epilogue of gemv_impl.hpp for it, minutes of compilation, so the types build in parallel.
 #include "gemv_impl.hpp"
 
 namespace ftts {
