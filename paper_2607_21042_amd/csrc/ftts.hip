@@ -160,7 +160,7 @@ struct PrefillWs {
 // with different batch sizes agree on where they are.
 struct MegaWs {
     uint32_t* ctl;
-    uint64_t *x, *qkv, *o, *h, *arg, *odone;
+    uint64_t *x, *qkv, *o, *h, *arg;
 };
 
 size_t mega_bytes(MegaWs* out, char* base) {
@@ -170,13 +170,11 @@ size_t mega_bytes(MegaWs* out, char* base) {
     char* ctl = take(256);
     char* x = take((size_t)BM * D * 8);
     char* qkv = take((size_t)BM * 3 * D * 8);
-    char* o = take((size_t)BM * NH * kMaxSplit * kPartWords * 8);
-    char* h = take((size_t)BM * FF * 8);
+    char* o = take((size_t)BM * (D / 2) * 8);  // bf16 pairs
+    char* h = take((size_t)BM * (FF / 2) * 8);
     char* arg = take((size_t)G * BM * 2 * 8);
-    char* odone = take((size_t)kDoneReplicas * kDoneStride * 8);
     if (out)
-        *out = MegaWs{(uint32_t*)ctl, (uint64_t*)x, (uint64_t*)qkv, (uint64_t*)o, (uint64_t*)h, (uint64_t*)arg,
-                      (uint64_t*)odone};
+        *out = MegaWs{(uint32_t*)ctl, (uint64_t*)x, (uint64_t*)qkv, (uint64_t*)o, (uint64_t*)h, (uint64_t*)arg};
     return off;
 }
 
@@ -560,7 +558,6 @@ int decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* pos
         MegaWs M;
         mega_bytes(&M, reinterpret_cast<char*>(ws));
         ma.max_pages = pt->max_pages;
-        ma.att_split = 1;  // one workgroup per (sequence, head)
         ma.n_pages = kv->n_pages;
         ma.greedy = samp->top_k == 1;
         ma.tokens = tokens;
@@ -577,7 +574,6 @@ int decode_step(const ftts_weights* w, const int32_t* tokens, const int32_t* pos
         ma.ex_o = M.o;
         ma.ex_h = M.h;
         ma.ex_arg = M.arg;
-        ma.ex_odone = M.odone;
         ma.ctl = M.ctl;
         (void)hipGetLastError();
         hipError_t e = launch_decode_mega(c.wdtype, ma, st);

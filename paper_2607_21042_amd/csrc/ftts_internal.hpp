@@ -317,13 +317,8 @@ namespace mega {
 constexpr int D = 1280, FF = 5120, NH = 20;
 constexpr int G = 256;   // workgroups of the persistent decode step, one per CU
 constexpr int BM = 2;    // largest batch it takes
-constexpr int kMaxSplit = 2;   // workgroups per (sequence, head) in attention
-constexpr int kPartWords = 66;  // one attention partial: 64 unnormalised sums, max score, weight sum
-constexpr int kDoneReplicas = 8;   // copies of the attention done-words (one read per group index mod 8)
-constexpr int kDoneStride = 512;   // words between copies (4 KB)
 struct Args {
     int n_layer, V, n_pos, B, max_pages, n_pages, greedy;
-    int att_split;  // S: workgroups per (sequence, head), 1..kMaxSplit
     float eps;
     Strided ln1_g, ln1_b, ln2_g, ln2_b;
     Strided qkv_w, qkv_s, qkv_z, qkv_b, out_w, out_s, out_z, out_b;
@@ -335,8 +330,9 @@ struct Args {
     float* hidden;           // [B][d] LN_f output of the step (the LM head's input), or null
     int32_t* sampled;
     int32_t* active_out;
+    // exchange words (32 value bits | epoch << 32): x [B][d] fp32, q/k/v [B][3d] fp32,
+    // o [B][d/2] and h [B][d_ff/2] bf16 pairs, argmax candidates [groups][B][2]
     uint64_t *ex_x, *ex_qkv, *ex_o, *ex_h, *ex_arg;
-    uint64_t* ex_odone;  // one word per attention partial, written after it
     uint32_t* ctl;  // [0] step counter, [1] abort
 };
 

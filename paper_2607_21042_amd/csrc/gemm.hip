@@ -287,7 +287,6 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const GemmArgs a) {
         __syncthreads();
     }
 
-    auto row_of = [&](int mt, int i) { return m0 + wm * 32 * MT + mt * 32 + (i >> 2) * 8 + fh * 4 + (i & 3); };
     if (MT == 1 && S > 1) {  // the plan splits K only with 64-row tiles
         // The accumulators go out in fragment order -- pair e of thread t at
         // (e * 256 + t) * 2, so each store instruction covers 512 contiguous bytes
@@ -348,8 +347,8 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const GemmArgs a) {
         if (tid == 0) __hip_atomic_store(a.count + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 
-    if ((a.N & 7) == 0) {
-        // Epilogue through LDS (the operand buffers are free: every wave passed the
+    {
+        // Epilogue through LDS (N is a multiple of 8: the launcher checks it) (the operand buffers are free: every wave passed the
         // loop's last barrier): each wave writes its (32 MT) x 64 sub-tile in
         // row-major order and reads it back as 16-byte row pieces for coalesced
         // stores -- output rows and, for q/k/v, the new keys and values into their
@@ -433,25 +432,6 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const GemmArgs a) {
                 asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this pass's reads done before the next writes
             }
         }
-        return;
-    }
-
-    constexpr bool F32 = false;
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-        const int n = nt ? nl1 : nl0;
-        if (n >= a.N) continue;
-        float rs = 1.f;
-        if constexpr (WT == FTTS_W8A16) rs = bf16_to_f32(a.scale[n]);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int m = row_of(mt, i);
-                if (m < a.M)
-                    gemm_epilogue<F32, EPI>(a, m, n, acc[mt][nt][i] * rs,
-                                            EPI == EPI_QKV ? s_rows[EPI == EPI_QKV ? m - m0 : 0] : RowSlot{-1, 0});
-            }
     }
 }
 
@@ -826,7 +806,7 @@ hipError_t launch_gemm(int wdtype, int epi, const GemmArgs& a, hipStream_t st) {
         }
         return hipGetLastError();
     }
-    if (!gemm_mfma_supported(a.K)) return hipErrorInvalidValue;
+    if (!gemm_mfma_supported(a.K) || a.N % 8) return hipErrorInvalidValue;  // 16-byte epilogue stores
     // bf16 weights with at least 128 tiles of 256 x 256: the large-tile kernel
     const long big_tiles = (long)((a.M + GB - 1) / GB) * ((a.N + GB - 1) / GB);
     if (wdtype == FTTS_BF16 && big_tiles >= 128 && a.N % 8 == 0) {
