@@ -208,7 +208,7 @@ size_t decode_bytes(const ftts_config& c, int B, DecodeWs* out, char* base) {
     char* o = take((size_t)B * c.d_model * 4);
     char* h = take((size_t)B * c.d_ff * 4);
     char* act = take((size_t)B * 4);
-    const bool batched = B >= kBatchedMin && c.wdtype != FTTS_F32 && c.d_model % 64 == 0 &&
+    const bool batched = B >= batched_min(c.wdtype) && c.wdtype != FTTS_F32 && c.d_model % 64 == 0 &&
                          bgemm_supported(c.wdtype, c.d_model, true) && bgemm_supported(c.wdtype, c.d_model, false) &&
                          bgemm_supported(c.wdtype, c.d_ff, false) && bgemm_supported(FTTS_BF16, c.d_model, true);
     char *stats = nullptr, *o16 = nullptr, *h16 = nullptr, *part = nullptr, *count = nullptr;
@@ -355,7 +355,7 @@ GemvArgs gemv_args(const ftts_linear& L, int N, int K, int B, const float* act, 
 
 }  // namespace
 
-// Decode step for batches of kBatchedMin or more (16-bit and quantised weights):
+// Decode step for batches of batched_min() or more (16-bit and quantised weights):
 // the MFMA linears, with each LayerNorm folded into the linear that reads it (the
 // residual updates leave per-tile row statistics behind).  Attention writes bf16
 // for the out-projection and FC1's GELU output is bf16 for FC2.

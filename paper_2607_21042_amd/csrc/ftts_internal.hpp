@@ -214,7 +214,9 @@ struct BgemmArgs {
     int stats_ld;
     float* hidden;           // with ln_x: [B][K] copy of the normalised rows (LM head), or null
 };
-constexpr int kBatchedMin = 8;  // decode batches of at least this many use the MFMA linears
+// Decode batches of at least this many take the MFMA linears: 5 (16-bit and
+// int8 weights: the GEMV tilings fall behind from 5 rows on), 3 for W4A16.
+inline int batched_min(int wdtype) { return wdtype == FTTS_W4A16 ? 3 : 5; }
 
 constexpr int kMaxPrefillSeqs = FTTS_MAX_BATCH;
 struct SeqTable {            // packed varlen sequences, passed by value

@@ -310,10 +310,12 @@ def test_prefill_from_ids(torch_cuda, mode):
         np.testing.assert_array_equal(res["logits"], ref_run["logits"])
 
 
-@pytest.mark.parametrize("mode,B", [("bf16", 33), ("w8a16", 8), ("w4a16", 33), ("bf16", 64), ("w4a16", 64)])
+@pytest.mark.parametrize("mode,B", [("bf16", 33), ("w8a16", 8), ("w4a16", 33), ("bf16", 64), ("w4a16", 64),
+                                    ("bf16", 5), ("w8a16", 6), ("w4a16", 3)])
 def test_batched_decode_matrix_core_linears(torch_cuda, mode, B):
-    """Batches of 8 or more take the MFMA linears (33 = a full group of 32 plus a
-    ragged one; 64, the largest batch, two full groups): ragged prefixes,
+    """Batches of 5 or more (3 or more for W4A16) take the MFMA linears (33 = a
+    full group of 32 plus a ragged one; 64, the largest batch, two full groups;
+    5, 6 and 3 the smallest, most of each 32-row tile idle): ragged prefixes,
     sequences retiring at different steps, every logit against the oracle, and
     bit-identical logits with the pages permuted and from run to run (the
     split-K sums have a fixed order)."""
