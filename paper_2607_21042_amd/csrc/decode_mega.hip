@@ -761,6 +761,11 @@ __device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync&
         MEGA_LMARK(l, 6);
         wait_vm<0>();  // FC2 share in LDS
         MEGA_LMARK(l, 7);
+        // three regions: after the last layer's FC1 share has been read, A and B hold
+        // nothing the FC2 phase reads, so the head's first rows go out now
+        if constexpr (L::kThree) {
+            if (l + 1 == a.n_layer) dma_rows<HO>(a.head_w, 2 * D, v0, nA, s_w);
+        }
         if (!follow(sy)) goto out;  // h gathered
         if constexpr (!L::kThree) {
             if (l + 1 < a.n_layer) dma_rows<O::PQ>(a.qkv_w.at(l + 1), RD, q0, nq, s_w);
@@ -769,7 +774,6 @@ __device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync&
     }
     // head
     bar();  // the FC2 share has been read
-    if constexpr (L::kThree) dma_rows<HO>(a.head_w, 2 * D, v0, nA, s_w);
     if (nv > nA) dma_rows<HO>(a.head_w, 2 * D, v0 + nA, nv - nA, s_w + kBuf);
     if (!follow(sy)) goto out;  // x gathered
     wait_vm<0>();
