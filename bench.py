@@ -59,7 +59,8 @@ def parse():
                    help="the batched paged workload instead: --batch sequences (default 32) with prefix lengths "
                         "~U[128,512], targets ~U[256,768] then STOP, top-k 30 / top-p 0.8 / T 0.8 sampling")
     p.add_argument("--eager", action="store_true",
-                   help="paged: launch every decode step directly instead of replaying HIP graphs")
+                   help="launch every kernel-per-phase decode step directly instead of replaying HIP graphs "
+                        "(the counter runs)")
     p.add_argument("--serve", action="store_true",
                    help="continuous batching instead: --requests utterances (default 64) with the --paged length "
                         "mix through --batch decode slots (default 32), chunks of 16 steps, top-k 30 sampling")
@@ -489,7 +490,7 @@ def model_inputs(workload, master, mode):
 
 
 def fixed_batch(torch, ftts, workload, shape, inputs, mode, B, P, T, steps, warmup, graph_steps=32,
-                cpu_steps=0, cpu_seqs=1):
+                cpu_steps=0, cpu_seqs=1, eager=False):
     """B sequences with the same prefix length P, T greedy steps each; one job =
     prefill + T steps with the sampled ids fed back on the device.  The
     persistent step is timed per launch; the kernel-per-phase step per graph
@@ -519,10 +520,12 @@ def fixed_batch(torch, ftts, workload, shape, inputs, mode, B, P, T, steps, warm
     pt.seq_lens = seq_lens  # keep the same storage: the graph reads these pointers
     pt.c = ftts.PageTable(bt.data_ptr(), seq_lens.data_ptr(), max_pages)
     persistent = ftts.decode_path(dm, B) == 2
-    # Launch timing: an event pair around every EV_EVERY-th persistent step (a pair
-    # on every step adds ~6 us per step to the whole job), around every replay on
-    # the graph path.
-    ev_every = EV_EVERY if persistent else 1
+    # kernel-per-phase steps replay HIP graphs unless `eager` (counter runs)
+    direct = persistent or eager
+    # Launch timing: an event pair around every EV_EVERY-th directly launched step
+    # (a pair on every step adds ~6 us per step to the whole job), around every
+    # replay on the graph path.
+    ev_every = EV_EVERY if direct else 1
 
     def reset():
         tokens.fill_(shape.start_token)
@@ -545,7 +548,7 @@ def fixed_batch(torch, ftts, workload, shape, inputs, mode, B, P, T, steps, warm
         step_kernel()
         step_advance()
     torch.cuda.synchronize()
-    if not persistent:
+    if not direct:
         # several kernels per step: capture S steps into one graph
         S = ftts.graph_steps(graph_steps) if T % graph_steps == 0 else 1
         graph = torch.cuda.CUDAGraph()
@@ -562,7 +565,7 @@ def fixed_batch(torch, ftts, workload, shape, inputs, mode, B, P, T, steps, warm
         ftts.prefill(dm, prefix, [P] * B, pt, kv, last, ws)
         if pev is not None:
             pev[1].record(stream)
-        if persistent:
+        if direct:
             for t in range(T):
                 timed = evs is not None and t % ev_every == 0
                 if timed:
@@ -582,7 +585,7 @@ def fixed_batch(torch, ftts, workload, shape, inputs, mode, B, P, T, steps, warm
     for _ in range(warmup):
         job()
     torch.cuda.synchronize()
-    n_units = len(range(0, T, ev_every)) if persistent else T // S
+    n_units = len(range(0, T, ev_every)) if direct else T // S
     evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_units)]
            for _ in range(steps)]
     pevs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
@@ -609,6 +612,10 @@ def fixed_batch(torch, ftts, workload, shape, inputs, mode, B, P, T, steps, warm
         unit_bytes = step_bytes[::ev_every]
         kernel = "decode_mega_kernel (persistent single-launch decode step)"
         sha = kernel_sources_sha(MEGA_SOURCES)
+    elif eager:
+        unit_bytes = step_bytes[::ev_every]
+        kernel = "decode step, kernel per phase (launched eagerly)"
+        sha = None  # the committed counters are per graph replay
     else:
         unit_bytes = step_bytes.reshape(T // S, S).sum(axis=1)
         kernel = f"decode step, kernel per phase ({S} steps per graph replay)"
@@ -616,7 +623,7 @@ def fixed_batch(torch, ftts, workload, shape, inputs, mode, B, P, T, steps, warm
     launch_us = float(unit_ms.mean() * 1e3)
     achieved = float(unit_bytes.sum() * steps / (unit_ms.sum() / 1e3) / 1e9)
     # decode time per job: the timed launches' mean times the step count (persistent)
-    decode_ms = float(unit_ms.mean() * T) if persistent else float(unit_ms.sum(axis=1).mean())
+    decode_ms = float(unit_ms.mean() * T) if direct else float(unit_ms.sum(axis=1).mean())
     workload_name = f"indextts2-gpt {mode} batch={B} prefix={P} greedy decode={T}"
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
@@ -720,7 +727,7 @@ def main():
         return
     out = fixed_batch(torch, ftts, workload, shape, inputs, mode, args.batch, args.prefix, args.decode, args.steps,
                       args.warmup, graph_steps=args.graph_steps,
-                      cpu_steps=0 if args.no_cpu_baseline else args.cpu_steps)
+                      cpu_steps=0 if args.no_cpu_baseline else args.cpu_steps, eager=args.eager)
     headline = mode == "bf16" and args.batch == 1 and args.prefix == 256 and args.decode == 512
     if headline and not args.no_legs:
         out["legs"] = legs(args, torch, ftts, workload, shape, master)
