@@ -315,18 +315,23 @@ __global__ __launch_bounds__(kSampThreads) void sample_kernel(const float* logit
     __shared__ int ri[kSampWaves];
     __shared__ int s_cnt[kSampWaves];
     const int b = blockIdx.x, tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
-    if (active && !active[b]) {
-        if (tid == 0) out[b] = -1;
-        return;
-    }
     const float* row = logits + (size_t)b * V;
     const bool greedy = top_k == 1;
+    // the row, the draw and the activity flag are requested together
     float z[kSampPer];
 #pragma unroll
     for (int j = 0; j < kSampPer; ++j) {
         const int i = tid + kSampThreads * j;
-        float v = i < V ? row[i] : -INFINITY;
-        v = greedy ? v : v / temperature;
+        z[j] = i < V ? row[i] : -INFINITY;
+    }
+    const float u = greedy ? 0.f : uniforms[b];
+    if (active && !active[b]) {
+        if (tid == 0) out[b] = -1;
+        return;
+    }
+#pragma unroll
+    for (int j = 0; j < kSampPer; ++j) {
+        const float v = greedy ? z[j] : z[j] / temperature;
         z[j] = v != v ? -INFINITY : v;
     }
     if (greedy) {
@@ -410,29 +415,24 @@ __global__ __launch_bounds__(kSampThreads) void sample_kernel(const float* logit
         }
         __syncthreads();
     }
-    if (tid != 0) return;
-    // Sequential fp32 part: weights, running sums, nucleus cut, inverse-CDF draw.
-    const float z1 = selv[0];
-    float acc = 0.f;
+    if (wave != 0) return;
+    // fp32 tail in wave 0, lane i holding rank i: the weights exp(z_i - z_1) side
+    // by side, then the running sums in rank order (the same additions as a
+    // sequential loop), the nucleus cut and the inverse-CDF draw by ballot.
+    const bool in = lane < top_k;
+    const float e = in ? expf(selv[lane] - selv[0]) : 0.f;
+    float acc = 0.f, cum = 0.f;
     for (int i = 0; i < top_k; ++i) {
-        acc = acc + expf(selv[i] - z1);
-        selv[i] = acc;  // cumulative sums replace the values
+        acc = acc + __int_as_float(__builtin_amdgcn_readlane(__float_as_int(e), i));
+        cum = lane == i ? acc : cum;
     }
-    const float thresh = top_p * selv[top_k - 1];
-    int n = top_k;
-    for (int i = 0; i < top_k; ++i)
-        if (selv[i] >= thresh) {
-            n = i + 1;
-            break;
-        }
-    const float rr = uniforms[b] * selv[n - 1];
-    int j = n - 1;
-    for (int i = 0; i < n; ++i)
-        if (selv[i] > rr) {
-            j = i;
-            break;
-        }
-    out[b] = seli[j] < V ? seli[j] : 0;
+    const float thresh = top_p * acc;
+    const uint64_t ge = __ballot(in && cum >= thresh);
+    const int n = ge ? (int)__builtin_ctzll(ge) + 1 : top_k;
+    const float rr = u * __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cum), n - 1));
+    const uint64_t gt = __ballot(lane < n && cum > rr);
+    const int j = gt ? (int)__builtin_ctzll(gt) : n - 1;
+    if (lane == 0) out[b] = seli[j] < V ? seli[j] : 0;
 }
 
 hipError_t launch_sample(const float* logits, int B, int V, const ftts_sampling& s, const float* uniforms,
