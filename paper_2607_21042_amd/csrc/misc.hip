@@ -27,9 +27,13 @@ __global__ __launch_bounds__(256) void embed_kernel(const void* tok_emb, const v
     if (threadIdx.x == 0) active[b] = ok ? 1 : 0;
     for (int i = b * 256 + threadIdx.x; i < n_zero; i += B * 256) zero[i] = 0u;
     float* xr = x + (size_t)b * d;
+    // the embedding rows are read at clamped indices without waiting for the page
+    // check (the value of an inactive row is dropped)
+    const int tc = min(max(t, 0), vocab - 1), pc = min(max(p, 0), n_pos - 1);
     // d is a multiple of 64, so every pass of this loop keeps whole waves active
     for (int k = threadIdx.x; k < d; k += blockDim.x) {
-        const float v = ok ? ld_act<F32>(tok_emb, (size_t)t * d + k) + ld_act<F32>(pos_emb, (size_t)p * d + k) : 0.f;
+        float v = ld_act<F32>(tok_emb, (size_t)tc * d + k) + ld_act<F32>(pos_emb, (size_t)pc * d + k);
+        v = ok ? v : 0.f;
         xr[k] = v;
         if (stats) {
             const float2 ts = tile_stats32(v);
@@ -449,13 +453,17 @@ __global__ __launch_bounds__(1024) void advance_kernel(int32_t* tokens, int32_t*
                                                        bool retire_on_stop, int32_t* history, int32_t* step_counter,
                                                        int max_steps, int B) {
     const int step = step_counter ? *step_counter : 0;
+    // this thread's first row, requested with the counter (a row is read and
+    // written by its own thread only)
+    const int b0 = threadIdx.x;
+    const int tok0 = b0 < B ? tokens[b0] : -1, smp0 = b0 < B ? sampled[b0] : -1;
     __syncthreads();  // every thread has read the counter before it moves
     for (int b = threadIdx.x; b < B; b += blockDim.x) {
         int h = -1;
-        if (tokens[b] >= 0) {
+        if ((b == b0 ? tok0 : tokens[b]) >= 0) {
             seq_lens[b] += 1;
             positions[b] += 1;
-            int next = sampled[b];
+            int next = b == b0 ? smp0 : sampled[b];
             bool retire = retire_on_stop && next == stop_token;  // the model's own stop code
             if (remaining) {
                 const int r = remaining[b] - 1;
