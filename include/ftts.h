@@ -49,7 +49,7 @@ extern "C" {
 #define FTTS_E_ALIGN -4       /* pointer not 16-byte aligned                 */
 #define FTTS_E_RANGE -5       /* a host-visible value out of range           */
 #define FTTS_E_HIP -6         /* a HIP runtime call or launch failed         */
-#define FTTS_E_UNSUPPORTED -7 /* valid but not implemented in this build     */
+#define FTTS_E_UNSUPPORTED -7 /* valid but not implemented by this library   */
 #define FTTS_E_WORKSPACE -8   /* workspace missing or smaller than needed    */
 
 /* ---- weight storage modes (ftts_config.wdtype) ----------------------------- */
