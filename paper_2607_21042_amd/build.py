@@ -1,9 +1,13 @@
 """Build libftts.so (HIP, gfx950) in-tree with hipcc.
 
-    python -m paper_2607_21042_amd.build
+    python -m paper_2607_21042_amd.build            # the library
+    python -m paper_2607_21042_amd.build --trace    # also libftts_trace.so (below)
 
 Each translation unit under csrc/ is compiled in parallel, then linked into
-paper_2607_21042_amd/libftts.so next to this file.
+paper_2607_21042_amd/libftts.so next to this file.  `--trace` links a second
+library, libftts_trace.so, whose persistent decode step stamps a per-phase
+timeline (FTTS_MEGA_TRACE; read by `mega_timeline.py`); it is never loaded
+unless a tool asks for it by path.
 """
 from __future__ import annotations
 
@@ -19,6 +23,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libftts.so")
+TRACE_LIB = os.path.join(PKG, "libftts_trace.so")
 ARCH = "gfx950"
 
 # Packed-fp32 VALU ops are disabled on purpose: hipcc may otherwise emit them from
@@ -85,6 +90,33 @@ def build(verbose: bool = False, force: bool = True) -> str:
     return LIB
 
 
+def build_trace(verbose: bool = False) -> str:
+    """Link libftts_trace.so: the library's objects with the persistent step
+    recompiled under FTTS_MEGA_TRACE."""
+    build(verbose, force=False)
+    tdir = os.path.join(OBJDIR, "trace")
+    os.makedirs(tdir, exist_ok=True)
+    src = os.path.join(CSRC, "decode_mega.hip")
+    tobj = os.path.join(tdir, "decode_mega.o")
+    r = subprocess.run([hipcc(), *HIPFLAGS, "-DFTTS_MEGA_TRACE", "-c", src, "-o", tobj], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {src} (trace):\n{r.stdout}\n{r.stderr}")
+    objs = [os.path.join(OBJDIR, os.path.basename(f)[:-4] + ".o") for f in sources()
+            if os.path.basename(f) != "decode_mega.hip"] + [tobj]
+    tmp = TRACE_LIB + ".tmp"
+    r = subprocess.run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp],
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed (trace):\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, TRACE_LIB)
+    if verbose:
+        print(f"built {TRACE_LIB}")
+    return TRACE_LIB
+
+
 if __name__ == "__main__":
-    build(verbose=True, force="--incremental" not in sys.argv)
+    if "--trace" in sys.argv:
+        build_trace(verbose=True)
+    else:
+        build(verbose=True, force="--incremental" not in sys.argv)
     sys.exit(0)
