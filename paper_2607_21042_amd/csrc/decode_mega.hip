@@ -315,11 +315,11 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
 }
 
 // W4A16 dot of one 4-byte chunk (8 codes, columns 8c .. 8c+7, one quantisation
-// group) with 8 bf16 activations: the zero-point enters through the chunk's own
-// activation sum.
+// group) with 8 bf16 activations per row, already in registers: the zero-point
+// enters through the chunk's own activation sum.
 template <int B_>
-__device__ __forceinline__ void dot_w4_word(uint32_t word, const uint16_t* xs, int stride, int B, float (&acc)[B_],
-                                            float s4, float z4) {
+__device__ __forceinline__ void dot_w4_word(uint32_t word, const uint4 (&xv)[B_], float (&acc)[B_], float s4,
+                                            float z4) {
     // Codes c0..c7 sit at bits 4i, so c_i and c_{i+4} are 16 bits apart: masking
     // the word shifted by 4i with 0x000F000F and setting 0x4300 in both halves
     // gives the bf16 pair (128 + c_i, 128 + c_{i+4}), exactly.  The products
@@ -330,64 +330,61 @@ __device__ __forceinline__ void dot_w4_word(uint32_t word, const uint16_t* xs, i
     constexpr uint32_t kOnes = 0x3F803F80u;  // bf16 (1, 1)
 #pragma unroll
     for (int b = 0; b < B_; ++b) {
-        if (b < B) {
-            const uint4 xv = *reinterpret_cast<const uint4*>(xs + b * stride);
-            // (x_i, x_{i+4}) pairs from the (x_2j, x_2j+1) pairs in LDS
-            const uint32_t x04 = __builtin_amdgcn_perm(xv.z, xv.x, 0x05040100u);
-            const uint32_t x15 = __builtin_amdgcn_perm(xv.z, xv.x, 0x07060302u);
-            const uint32_t x26 = __builtin_amdgcn_perm(xv.w, xv.y, 0x05040100u);
-            const uint32_t x37 = __builtin_amdgcn_perm(xv.w, xv.y, 0x07060302u);
-            float t = dot2_bf16(cp[0], x04, 0.f);
-            t = dot2_bf16(cp[1], x15, t);
-            t = dot2_bf16(cp[2], x26, t);
-            t = dot2_bf16(cp[3], x37, t);
-            float sx = dot2_bf16(xv.x, kOnes, 0.f);
-            sx = dot2_bf16(xv.y, kOnes, sx);
-            sx = dot2_bf16(xv.z, kOnes, sx);
-            sx = dot2_bf16(xv.w, kOnes, sx);
-            acc[b] = fmaf(s4, fmaf(-(128.f + z4), sx, t), acc[b]);
-        }
+        const uint4 x = xv[b];
+        // (x_i, x_{i+4}) pairs from the (x_2j, x_2j+1) pairs in LDS
+        const uint32_t x04 = __builtin_amdgcn_perm(x.z, x.x, 0x05040100u);
+        const uint32_t x15 = __builtin_amdgcn_perm(x.z, x.x, 0x07060302u);
+        const uint32_t x26 = __builtin_amdgcn_perm(x.w, x.y, 0x05040100u);
+        const uint32_t x37 = __builtin_amdgcn_perm(x.w, x.y, 0x07060302u);
+        float t = dot2_bf16(cp[0], x04, 0.f);
+        t = dot2_bf16(cp[1], x15, t);
+        t = dot2_bf16(cp[2], x26, t);
+        t = dot2_bf16(cp[3], x37, t);
+        float sx = dot2_bf16(x.x, kOnes, 0.f);
+        sx = dot2_bf16(x.y, kOnes, sx);
+        sx = dot2_bf16(x.z, kOnes, sx);
+        sx = dot2_bf16(x.w, kOnes, sx);
+        acc[b] = fmaf(s4, fmaf(-(128.f + z4), sx, t), acc[b]);
     }
 }
 
-// One 16-byte weight chunk (8 bf16 or 16 int8 weights) against bf16 activations.
-template <int WT, int B_>
-__device__ __forceinline__ void dot_chunk16(const uint4 wv, const uint16_t* xs, int stride, int B, float (&acc)[B_]) {
-    if constexpr (WT == FTTS_BF16) {
+// One 16-byte chunk of bf16 weights (8 columns) against the rows' 8 activations, in registers.
+template <int B_>
+__device__ __forceinline__ void dot_bf16_chunk(const uint4 wv, const uint4 (&xv)[B_], float (&acc)[B_]) {
 #pragma unroll
-        for (int b = 0; b < B_; ++b) {
-            if (b < B) {
-                const uint4 xv = *reinterpret_cast<const uint4*>(xs + b * stride);
-                float t = acc[b];
-                t = dot2_bf16(wv.x, xv.x, t);
-                t = dot2_bf16(wv.y, xv.y, t);
-                t = dot2_bf16(wv.z, xv.z, t);
-                t = dot2_bf16(wv.w, xv.w, t);
-                acc[b] = t;
+    for (int b = 0; b < B_; ++b) {
+        float t = acc[b];
+        t = dot2_bf16(wv.x, xv[b].x, t);
+        t = dot2_bf16(wv.y, xv[b].y, t);
+        t = dot2_bf16(wv.z, xv[b].z, t);
+        t = dot2_bf16(wv.w, xv[b].w, t);
+        acc[b] = t;
+    }
+}
+
+// One 16-byte chunk of W8A16 codes (16 int8 weights) against bf16 activations in LDS.
+template <int B_>
+__device__ __forceinline__ void dot_w8_chunk(const uint4 wv, const uint16_t* xs, int stride, int B, float (&acc)[B_]) {
+    const uint32_t wd[4] = {wv.x, wv.y, wv.z, wv.w};
+    float wf[16];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) wf[4 * j + i] = (float)(int32_t)((int32_t)(wd[j] << (24 - 8 * i)) >> 24);
+    }
+#pragma unroll
+    for (int b = 0; b < B_; ++b) {
+        if (b < B) {
+            const uint4 x0 = *reinterpret_cast<const uint4*>(xs + b * stride);
+            const uint4 x1 = *reinterpret_cast<const uint4*>(xs + b * stride + 8);
+            const uint32_t xw[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+            float t = acc[b];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                t = fmaf(wf[2 * e], bf16lo(xw[e]), t);
+                t = fmaf(wf[2 * e + 1], bf16hi(xw[e]), t);
             }
-        }
-    } else {  // FTTS_W8A16: 16 int8 codes
-        const uint32_t wd[4] = {wv.x, wv.y, wv.z, wv.w};
-        float wf[16];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) wf[4 * j + i] = (float)(int32_t)((int32_t)(wd[j] << (24 - 8 * i)) >> 24);
-        }
-#pragma unroll
-        for (int b = 0; b < B_; ++b) {
-            if (b < B) {
-                const uint4 x0 = *reinterpret_cast<const uint4*>(xs + b * stride);
-                const uint4 x1 = *reinterpret_cast<const uint4*>(xs + b * stride + 8);
-                const uint32_t xw[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-                float t = acc[b];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    t = fmaf(wf[2 * e], bf16lo(xw[e]), t);
-                    t = fmaf(wf[2 * e + 1], bf16hi(xw[e]), t);
-                }
-                acc[b] = t;
-            }
+            acc[b] = t;
         }
     }
 }
@@ -434,21 +431,47 @@ struct Share {
         const int slot = min(t / LPR, R - 1);
 #pragma unroll
         for (int b = 0; b < B_; ++b) acc[b] = 0.f;
+        // bf16 and W4A16: every LDS read of the thread's share (weights and the
+        // rows' activations) is issued before the first product, so the reads
+        // overlap and the thread waits once, not once per chunk.  Rows past the
+        // batch are read and multiplied too (the buffers hold BMAX rows; their
+        // sums are never used).  W8A16 keeps each chunk's reads beside its
+        // longer conversion work, which measured faster for it.
         if constexpr (WT == FTTS_W4A16) {
             const uint32_t* wrow = reinterpret_cast<const uint32_t*>(buf + slot * ROW_BYTES);
             const int g0 = (li * NCH * EPC) >> 7;
+            uint32_t wv[NCH];
+            uint4 xv[NCH][B_];
 #pragma unroll
             for (int i = 0; i < NCH; ++i) {
                 const int c = li * NCH + i;
-                const bool second = ((c * EPC) >> 7) != g0;
-                dot_w4_word<B_>(wrow[c], s_in + c * EPC, K, B, acc, second ? s4[1] : s4[0], second ? z4[1] : z4[0]);
+                wv[i] = wrow[c];
+#pragma unroll
+                for (int b = 0; b < B_; ++b) xv[i][b] = *reinterpret_cast<const uint4*>(s_in + c * EPC + b * K);
             }
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) {
+                const bool second = (((li * NCH + i) * EPC) >> 7) != g0;
+                dot_w4_word<B_>(wv[i], xv[i], acc, second ? s4[1] : s4[0], second ? z4[1] : z4[0]);
+            }
+        } else if constexpr (WT == FTTS_BF16) {
+            const uint4* wrow = reinterpret_cast<const uint4*>(buf + slot * ROW_BYTES);
+            uint4 wv[NCH], xv[NCH][B_];
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) {
+                const int c = li + i * LPR;
+                wv[i] = wrow[c];
+#pragma unroll
+                for (int b = 0; b < B_; ++b) xv[i][b] = *reinterpret_cast<const uint4*>(s_in + c * EPC + b * K);
+            }
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) dot_bf16_chunk<B_>(wv[i], xv[i], acc);
         } else {
             const uint4* wrow = reinterpret_cast<const uint4*>(buf + slot * ROW_BYTES);
 #pragma unroll
             for (int i = 0; i < NCH; ++i) {
                 const int c = li + i * LPR;
-                dot_chunk16<WT, B_>(wrow[c], s_in + c * EPC, K, B, acc);
+                dot_w8_chunk<B_>(wrow[c], s_in + c * EPC, K, B, acc);
             }
         }
 #pragma unroll
