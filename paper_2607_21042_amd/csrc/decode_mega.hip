@@ -81,14 +81,10 @@ __device__ __forceinline__ void pair_rows_of(int N, int k, int NG, int& r0, int&
 }
 constexpr int max_pair_rows(int N, int NG) { return 2 * max_rows(N / 2, NG); }
 
-template <int WT> struct Tiles;  // (lanes per row, 16-byte chunks per lane) per phase, <= NC threads
-template <> struct Tiles<FTTS_BF16> {
-    static constexpr int QL = 16, QC = 10, OL = 32, OC = 5, AL = 16, AC = 10, BL = 64, BC = 10;
-};
-template <> struct Tiles<FTTS_W8A16> {
-    static constexpr int QL = 16, QC = 5, OL = 16, OC = 5, AL = 16, AC = 5, BL = 64, BC = 5;
-};
-template <> struct Tiles<FTTS_W4A16> {  // 4-byte chunks (8 codes): many more lanes per row than 16-byte ones
+// (lanes per row, chunks per lane) of each phase: a chunk is 8 weights in every
+// mode (16 bytes of bf16, 8 of int8 codes, 4 of W4A16 codes), so the three share
+// one tiling and a lane does the same number of products in each.
+template <int WT> struct Tiles {
     static constexpr int QL = 16, QC = 10, OL = 32, OC = 5, AL = 16, AC = 10, BL = 64, BC = 10;
 };
 constexpr int HL = 8, HC = 20;  // LM head (bf16)
@@ -362,39 +358,37 @@ __device__ __forceinline__ void dot_bf16_chunk(const uint4 wv, const uint4 (&xv)
     }
 }
 
-// One 16-byte chunk of W8A16 codes (16 int8 weights) against bf16 activations in LDS.
+// One 8-byte chunk of W8A16 codes (8 int8 weights, columns 8c .. 8c+7) against
+// the rows' 8 activations, in registers.  Every int8 code is a bf16 value
+// exactly (at most 8 significant bits), so each code becomes fp32 in one
+// conversion that selects and sign-extends its byte, two of them are packed as a
+// bf16 pair (their upper halves), and the pairs meet the activation pairs in
+// fp32-accumulating dot products.
+__device__ __forceinline__ uint32_t w8_pair(uint32_t w, int hi) {
+    const float a = (float)(int)(signed char)(w >> (16 * hi));
+    const float b = (float)(int)(signed char)(w >> (16 * hi + 8));
+    return __builtin_amdgcn_perm(__float_as_uint(b), __float_as_uint(a), 0x07060302u);
+}
 template <int B_>
-__device__ __forceinline__ void dot_w8_chunk(const uint4 wv, const uint16_t* xs, int stride, int B, float (&acc)[B_]) {
-    const uint32_t wd[4] = {wv.x, wv.y, wv.z, wv.w};
-    float wf[16];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) wf[4 * j + i] = (float)(int32_t)((int32_t)(wd[j] << (24 - 8 * i)) >> 24);
-    }
+__device__ __forceinline__ void dot_w8_chunk(const uint2 wv, const uint4 (&xv)[B_], float (&acc)[B_]) {
+    const uint32_t wp[4] = {w8_pair(wv.x, 0), w8_pair(wv.x, 1), w8_pair(wv.y, 0), w8_pair(wv.y, 1)};
 #pragma unroll
     for (int b = 0; b < B_; ++b) {
-        if (b < B) {
-            const uint4 x0 = *reinterpret_cast<const uint4*>(xs + b * stride);
-            const uint4 x1 = *reinterpret_cast<const uint4*>(xs + b * stride + 8);
-            const uint32_t xw[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-            float t = acc[b];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                t = fmaf(wf[2 * e], bf16lo(xw[e]), t);
-                t = fmaf(wf[2 * e + 1], bf16hi(xw[e]), t);
-            }
-            acc[b] = t;
-        }
+        float t = acc[b];
+        t = dot2_bf16(wp[0], xv[b].x, t);
+        t = dot2_bf16(wp[1], xv[b].y, t);
+        t = dot2_bf16(wp[2], xv[b].z, t);
+        t = dot2_bf16(wp[3], xv[b].w, t);
+        acc[b] = t;
     }
 }
 
 template <int WT, int LPR, int NCH, int K>
 struct Share {
     static constexpr int ROW_BYTES = row_bytes<WT, K>();
-    // bytes per chunk: 16 (one uint4) for 16-bit and int8 weights, 4 (8 codes) for W4A16
-    static constexpr int CB = WT == FTTS_W4A16 ? 4 : 16;
-    static constexpr int EPC = WT == FTTS_W4A16 ? 8 : WInfo<WT>::EPC;  // weights per chunk
+    // a chunk is 8 weights: 16 bytes of bf16, 8 of int8 codes, 4 of W4A16 codes
+    static constexpr int CB = WT == FTTS_W4A16 ? 4 : WT == FTTS_W8A16 ? 8 : 16;
+    static constexpr int EPC = 8;
     static_assert(LPR * NCH * CB == ROW_BYTES, "tiling must cover a row");
     static_assert(WT != FTTS_W4A16 || NCH * EPC <= 128, "a W4A16 lane must stay within two groups");
     float s4[2], z4[2];
@@ -426,17 +420,17 @@ struct Share {
     // acc[b] = dot product of this thread's row with the bf16 row s_in[b] (+ bias); every lane of the row gets it.
     template <int B_>
     __device__ __forceinline__ void dot(const uint16_t* s_in, int B, float (&acc)[B_]) const {
+        (void)B;  // every row slot is computed; callers use the rows below B
         const int t = fresh_tid();
         const int li = t & (LPR - 1);
         const int slot = min(t / LPR, R - 1);
 #pragma unroll
         for (int b = 0; b < B_; ++b) acc[b] = 0.f;
-        // bf16 and W4A16: every LDS read of the thread's share (weights and the
-        // rows' activations) is issued before the first product, so the reads
-        // overlap and the thread waits once, not once per chunk.  Rows past the
-        // batch are read and multiplied too (the buffers hold BMAX rows; their
-        // sums are never used).  W8A16 keeps each chunk's reads beside its
-        // longer conversion work, which measured faster for it.
+        // Every LDS read of the thread's share (weights and the rows'
+        // activations) is issued before the first product, so the reads overlap
+        // and the thread waits once, not once per chunk.  Rows past the batch
+        // are read and multiplied too (the buffers hold BMAX rows; their sums
+        // are never used).
         if constexpr (WT == FTTS_W4A16) {
             const uint32_t* wrow = reinterpret_cast<const uint32_t*>(buf + slot * ROW_BYTES);
             const int g0 = (li * NCH * EPC) >> 7;
@@ -466,13 +460,19 @@ struct Share {
             }
 #pragma unroll
             for (int i = 0; i < NCH; ++i) dot_bf16_chunk<B_>(wv[i], xv[i], acc);
-        } else {
-            const uint4* wrow = reinterpret_cast<const uint4*>(buf + slot * ROW_BYTES);
+        } else {  // W8A16
+            const uint2* wrow = reinterpret_cast<const uint2*>(buf + slot * ROW_BYTES);
+            uint2 wv[NCH];
+            uint4 xv[NCH][B_];
 #pragma unroll
             for (int i = 0; i < NCH; ++i) {
                 const int c = li + i * LPR;
-                dot_w8_chunk<B_>(wrow[c], s_in + c * EPC, K, B, acc);
+                wv[i] = wrow[c];
+#pragma unroll
+                for (int b = 0; b < B_; ++b) xv[i][b] = *reinterpret_cast<const uint4*>(s_in + c * EPC + b * K);
             }
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) dot_w8_chunk<B_>(wv[i], xv[i], acc);
         }
 #pragma unroll
         for (int b = 0; b < B_; ++b) acc[b] = fmaf(group_sum<LPR>(acc[b]), rs, bias);
@@ -784,15 +784,12 @@ __device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync&
         MEGA_LMARK(l, 6);
         wait_vm<0>();  // FC2 share in LDS
         MEGA_LMARK(l, 7);
-        // three regions: after the last layer's FC1 share has been read, A and B hold
-        // nothing the FC2 phase reads, so the head's first rows go out now
-        if constexpr (L::kThree) {
-            if (l + 1 == a.n_layer) dma_rows<HO>(a.head_w, 2 * D, v0, nA, s_w);
-        }
+        // after the last layer's FC1 share has been read, [0, kBuf) holds nothing
+        // the FC2 phase reads, so the head's first rows go out now
+        if (l + 1 == a.n_layer) dma_rows<HO>(a.head_w, 2 * D, v0, nA, s_w);
         if (!follow(sy)) goto out;  // h gathered
         if constexpr (!L::kThree) {
             if (l + 1 < a.n_layer) dma_rows<O::PQ>(a.qkv_w.at(l + 1), RD, q0, nq, s_w);
-            else dma_rows<HO>(a.head_w, 2 * D, v0, nA, s_w);
         }
     }
     // head
