@@ -426,6 +426,11 @@ struct Share {
         const int slot = min(t / LPR, R - 1);
 #pragma unroll
         for (int b = 0; b < B_; ++b) acc[b] = 0.f;
+        // A wave whose rows all lie past the share's last row has nothing to
+        // compute (its threads would re-read row R - 1) and skips the reads: the
+        // dots are bound by the LDS bandwidth all waves of the CU share.  Its
+        // acc stays 0 and its callers keep rows past R out of every store.
+        if (__builtin_amdgcn_readfirstlane(t & ~(kWave - 1)) / LPR >= R) return;
         // Every LDS read of the thread's share (weights and the rows'
         // activations) is issued before the first product, so the reads overlap
         // and the thread waits once, not once per chunk.  Rows past the batch
