@@ -526,7 +526,12 @@ __device__ __forceinline__ void layer_norm(const float* s_x, uint16_t* s_in, con
                 q = fmaf(d3, d3, q);
             }
             const float r = 1.0f / sqrtf(wave_sum(q) * (1.0f / (float)D) + eps);
-            const float4 v = *reinterpret_cast<const float4*>(x + tid * 4);
+            // this thread's columns 4 tid .. 4 tid + 3 are xv[wave] (tid = 64 wave + lane)
+            const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+            float4 v = xv[0];
+#pragma unroll
+            for (int i = 1; i < D / 256; ++i)
+                if (w == i) v = xv[i];
             float4 y;
             y.x = fmaf((v.x - m) * r, bf16lo(ln.g.x), bf16lo(ln.b.x));
             y.y = fmaf((v.y - m) * r, bf16hi(ln.g.x), bf16hi(ln.b.x));
