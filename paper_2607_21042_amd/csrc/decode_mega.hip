@@ -155,8 +155,16 @@ __device__ __forceinline__ void put(uint64_t* p, uint32_t epoch, float v) {
 }
 
 // Two values as bf16 in one exchange word: lo in the low half (the even column).
+// Two floats rounded to nearest even into packed bf16 (lo in bits 0-15): one
+// gfx950 conversion instruction, the same bits as f32_to_bf16 for finite values.
+typedef __bf16 bf16x2_cvt_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+    const bf16x2_cvt_t v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
 __device__ __forceinline__ void put2(uint64_t* p, uint32_t epoch, float lo, float hi) {
-    const uint32_t v = (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+    const uint32_t v = pack_bf16(lo, hi);
     __hip_atomic_store(p, ((uint64_t)epoch << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -232,7 +240,7 @@ __device__ __forceinline__ void give_up(const Sync& sy, uint32_t* ctl) {
 // A word's 32 value bits into LDS: an fp32 value as is or rounded to bf16, or a
 // pair of bf16 values as they were packed.
 __device__ __forceinline__ void store_to(float* dst, int j, uint32_t v) { dst[j] = __uint_as_float(v); }
-__device__ __forceinline__ void store_to(uint16_t* dst, int j, uint32_t v) { dst[j] = f32_to_bf16(__uint_as_float(v)); }
+__device__ __forceinline__ void store_to(uint16_t* dst, int j, uint32_t v) { dst[j] = (uint16_t)pack_bf16(__uint_as_float(v), 0.f); }
 __device__ __forceinline__ void store_to(uint32_t* dst, int j, uint32_t v) { dst[j] = v; }
 
 // The NTH threads that poll: wait until the n exchange words all carry `epoch`
@@ -538,8 +546,8 @@ __device__ __forceinline__ void layer_norm(const float* s_x, uint16_t* s_in, con
             y.z = fmaf((v.z - m) * r, bf16lo(ln.g.y), bf16lo(ln.b.y));
             y.w = fmaf((v.w - m) * r, bf16hi(ln.g.y), bf16hi(ln.b.y));
             uint2 pk;
-            pk.x = (uint32_t)f32_to_bf16(y.x) | ((uint32_t)f32_to_bf16(y.y) << 16);
-            pk.y = (uint32_t)f32_to_bf16(y.z) | ((uint32_t)f32_to_bf16(y.w) << 16);
+            pk.x = pack_bf16(y.x, y.y);
+            pk.y = pack_bf16(y.z, y.w);
             *reinterpret_cast<uint2*>(s_in + b * D + tid * 4) = pk;
             if (hid) *reinterpret_cast<float4*>(hid + b * D + tid * 4) = y;  // fp32, before rounding
         }
@@ -660,13 +668,11 @@ __device__ __forceinline__ void attention_group(const Args& a, int b, int h, int
         uint32_t qh[4], ql[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint16_t h0 = f32_to_bf16(q[2 * j]), h1 = f32_to_bf16(q[2 * j + 1]);
-            qh[j] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-            ql[j] = (uint32_t)f32_to_bf16(q[2 * j] - bf16_to_f32(h0)) |
-                    ((uint32_t)f32_to_bf16(q[2 * j + 1] - bf16_to_f32(h1)) << 16);
+            qh[j] = pack_bf16(q[2 * j], q[2 * j + 1]);
+            ql[j] = pack_bf16(q[2 * j] - __uint_as_float(qh[j] << 16), q[2 * j + 1] - __uint_as_float(qh[j] & 0xFFFF0000u));
         }
         // The cache holds keys and values in bf16; attend to the new token as cached.
-        auto cached = [](float v) { return bf16_to_f32(f32_to_bf16(v)); };
+        auto cached = [](float v) { return __uint_as_float(pack_bf16(v, 0.f) << 16); };
         float m = -INFINITY, lsum = 0.f, o[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) o[j] = 0.f;
