@@ -32,6 +32,7 @@ namespace ftts {
 
 typedef __bf16 bgemm_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float bgemm_f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bgemm_bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kBgemmRows = 32;  // sequences per launch
 constexpr int kBgemmFeat = 32;  // features per MFMA tile (a workgroup owns FT tiles)
@@ -70,8 +71,9 @@ constexpr int kLnMaxTP = 8;                                  // tiles per group:
 constexpr int kLnMaxK = kLnGroups * kLnMaxTP * kStatTile;
 
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {  // one packed conversion
+    const bgemm_bf16x2 v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 template <int WT, bool LN>

@@ -20,13 +20,12 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_floa
 __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// Round to nearest bf16, ties to even (NaN stays NaN, quietened).  Branch-free,
-// so a run of conversions stays one straight line of VALU selects.
+// Round to nearest bf16, ties to even (NaN stays NaN, quietened): gfx950's
+// packed conversion, one instruction.
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-    const uint32_t u = __float_as_uint(f);
-    const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-    const bool nan = (u & 0x7FFFFFFFu) > 0x7F800000u;
-    return (uint16_t)(nan ? ((u >> 16) | 0x40u) : r);
+    typedef __bf16 bf16x2_rne_t __attribute__((ext_vector_type(2)));
+    const bf16x2_rne_t v = {(__bf16)f, (__bf16)0.f};
+    return (uint16_t)__builtin_bit_cast(uint32_t, v);
 }
 
 // 16-byte streaming load (weights are read once per call; the hint keeps them from
