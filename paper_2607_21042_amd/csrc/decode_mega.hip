@@ -91,6 +91,8 @@ constexpr int HL = 8, HC = 20;  // LM head (bf16)
 
 template <int WT, int K>
 constexpr int row_bytes() { return WT == FTTS_W4A16 ? K / 2 : WT == FTTS_W8A16 ? K : 2 * K; }
+// A vmcnt wait for at most n outstanding copies (the counter holds 63).
+constexpr int vm_cap(int n) { return n > 63 ? 63 : n; }
 // Direct-to-LDS instructions (1 KB each) that copy `bytes`.
 constexpr int dma_ops(int bytes) { return (bytes + 1023) / 1024; }
 // Every share of a phase is copied with the same number of instructions (that of
@@ -117,12 +119,19 @@ template <int WT, int BMAX> struct Ops {
 template <int WT, int BMAX> struct Lds {
     using O = Ops<WT, BMAX>;
     static constexpr bool kThree = BMAX == 1 && WT == FTTS_BF16;
+    // quantised shares at batch 1 are small enough for four regions: q/k/v, FC1 and
+    // the out-projection in [0, kBuf), FC2 in [kBuf, 2 kBuf), so FC1, FC2 and the
+    // next layer's q/k/v all go out while attention runs and no copy lands during
+    // a dot or a gather
+    static constexpr bool kFour = BMAX == 1 && WT != FTTS_BF16;
+    static constexpr int kOffD = kFour ? O::PQ * 1024 : 0;  // FC1
     static constexpr int kA = (O::PQ > O::P1 ? O::PQ : O::P1) * 1024;
-    static constexpr int kOffB = kThree ? kA : kBuf;
+    static constexpr int kOffB = kThree ? kA : kFour ? kOffD + O::P1 * 1024 : kBuf;
     static constexpr int kEnd = kOffB + (O::PO + O::P2) * 1024;
     static constexpr int kBytes = kThree && kEnd > 2 * kBuf ? kEnd : 2 * kBuf;
     static constexpr int kOffC = kThree ? kBytes - O::P2 * 1024 : kBuf;  // C at the top
     static_assert(!kThree || kOffB + O::PO * 1024 <= kOffC, "regions apart");
+    static_assert(!kFour || kOffB + O::PO * 1024 <= kBuf, "the first three regions within one buffer");
 };
 constexpr int kHeadRowsPerBuf = kBuf / (2 * D);  // LM-head rows in one buffer
 static_assert(BM * NH < G, "attention groups leave GEMV groups");
@@ -782,29 +791,48 @@ __device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync&
         // P1: the FC1 share (and at batch 1 the FC2 share) go out while attention runs
         bar();             // the q/k/v share has been read
         MEGA_LMARK(l, 2);
-        dma_rows<O::P1>(a.fc1_w.at(l), RD, f0, nf, s_w);
-        wait_vm<O::P1>();  // out-proj share in LDS
-        if constexpr (L::kThree) dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + L::kOffC);
+        dma_rows<O::P1>(a.fc1_w.at(l), RD, f0, nf, s_w + L::kOffD);
+        if constexpr (L::kFour) {
+            // FC2 and the next layer's q/k/v follow at once (more than 63 copies in
+            // flight stall the issue until the oldest have landed, so a wait for
+            // at most 63 still covers the out-projection's)
+            dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + L::kOffC);
+            if (l + 1 < a.n_layer) {
+                dma_rows<O::PQ>(a.qkv_w.at(l + 1), RD, q0, nq, s_w);
+                wait_vm<vm_cap(O::P1 + O::P2 + O::PQ)>();  // out-proj share in LDS
+            } else {
+                wait_vm<O::P1 + O::P2>();
+            }
+        } else {
+            wait_vm<O::P1>();  // out-proj share in LDS
+            if constexpr (L::kThree) dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + L::kOffC);
+        }
         MEGA_LMARK(l, 3);
         if (!follow(sy)) goto out;  // o of every head gathered
         // P3
         bar();  // the out-proj share has been read
         MEGA_LMARK(l, 4);
         if (!follow(sy)) goto out;  // x gathered
-        if constexpr (!L::kThree) dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + L::kOffC);
-        wait_vm<O::P2>();  // FC1 share in LDS
+        if constexpr (L::kFour) {
+            if (l + 1 < a.n_layer) wait_vm<O::P2 + O::PQ>();  // FC1 share in LDS
+            else wait_vm<O::P2>();
+        } else {
+            if constexpr (!L::kThree) dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + L::kOffC);
+            wait_vm<O::P2>();  // FC1 share in LDS
+        }
         MEGA_LMARK(l, 5);
         bar();             // LN2 done
         // P4
         bar();  // the FC1 share has been read
         MEGA_LMARK(l, 6);
-        wait_vm<0>();  // FC2 share in LDS
+        if (L::kFour && l + 1 < a.n_layer) wait_vm<O::PQ>();  // FC2 share in LDS
+        else wait_vm<0>();
         MEGA_LMARK(l, 7);
         // after the last layer's FC1 share has been read, [0, kBuf) holds nothing
         // the FC2 phase reads, so the head's first rows go out now
         if (l + 1 == a.n_layer) dma_rows<HO>(a.head_w, 2 * D, v0, nA, s_w);
         if (!follow(sy)) goto out;  // h gathered
-        if constexpr (!L::kThree) {
+        if constexpr (!L::kThree && !L::kFour) {
             if (l + 1 < a.n_layer) dma_rows<O::PQ>(a.qkv_w.at(l + 1), RD, q0, nq, s_w);
         }
     }
@@ -947,7 +975,7 @@ __global__ __launch_bounds__(NT) void decode_mega_kernel(const Args a) {
         // ---------------- P1 + P2: attention elsewhere; out-proj + residual ------------------
         bar();  // P0's reads of s_w[0] are done
         MEGA_LMARK(l, 3);
-        p1.params(a.fc1_s.at(l), a.fc1_z.at(l), a.fc1_b.at(l), f0, nf, s_w);
+        p1.params(a.fc1_s.at(l), a.fc1_z.at(l), a.fc1_b.at(l), f0, nf, s_w + L::kOffD);
         // o of every head, straight from the attention groups (s_in was last read by P0's dot)
         if (!gather<uo<BMAX>(), NC>(a.ex_o, B * D / 2, Flat{}, E(5 * l + 2), reinterpret_cast<uint32_t*>(s_in), a.ctl,
                                     sy))
