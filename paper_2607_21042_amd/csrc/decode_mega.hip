@@ -757,9 +757,10 @@ __device__ __forceinline__ void attention_group(const Args& a, int b, int h, int
 // the memory system the exchanges cross), so where a share goes out is a trade
 // between holding up a barrier and slowing an exchange.  With three regions:
 // q/k/v while x is gathered, the out-projection during LN1, FC1 and FC2
-// together while attention runs elsewhere.  With two: FC2 waits for the
-// out-projection's buffer and goes out after x is gathered, and q/k/v of the
-// next layer once h is gathered.
+// together while attention runs elsewhere.  With four (quantised, batch 1):
+// FC1, FC2 and the next layer's q/k/v together while attention runs.  With two
+// (batch 2): FC2 waits for the out-projection's buffer and goes out after x is
+// gathered, and q/k/v of the next layer once h is gathered.
 template <int WT, int BMAX>
 __device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync& sy) {
     using O = Ops<WT, BMAX>;
