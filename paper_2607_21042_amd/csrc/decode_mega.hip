@@ -91,8 +91,6 @@ constexpr int HL = 8, HC = 20;  // LM head (bf16)
 
 template <int WT, int K>
 constexpr int row_bytes() { return WT == FTTS_W4A16 ? K / 2 : WT == FTTS_W8A16 ? K : 2 * K; }
-// A vmcnt wait for at most n outstanding copies (the counter holds 63).
-constexpr int vm_cap(int n) { return n > 63 ? 63 : n; }
 // Direct-to-LDS instructions (1 KB each) that copy `bytes`.
 constexpr int dma_ops(int bytes) { return (bytes + 1023) / 1024; }
 // Every share of a phase is copied with the same number of instructions (that of
@@ -132,6 +130,7 @@ template <int WT, int BMAX> struct Lds {
     static constexpr int kOffC = kThree ? kBytes - O::P2 * 1024 : kBuf;  // C at the top
     static_assert(!kThree || kOffB + O::PO * 1024 <= kOffC, "regions apart");
     static_assert(!kFour || kOffB + O::PO * 1024 <= kBuf, "the first three regions within one buffer");
+    static_assert(!kFour || (O::P1 + O::P2 <= 63 && O::P2 + O::PQ <= 63), "copy waits within vmcnt");
 };
 constexpr int kHeadRowsPerBuf = kBuf / (2 * D);  // LM-head rows in one buffer
 static_assert(BM * NH < G, "attention groups leave GEMV groups");
@@ -794,16 +793,11 @@ __device__ __forceinline__ void copy_wave(const Args& a, int k, char* s_w, Sync&
         MEGA_LMARK(l, 2);
         dma_rows<O::P1>(a.fc1_w.at(l), RD, f0, nf, s_w + L::kOffD);
         if constexpr (L::kFour) {
-            // FC2 and the next layer's q/k/v follow at once (more than 63 copies in
-            // flight stall the issue until the oldest have landed, so a wait for
-            // at most 63 still covers the out-projection's)
+            // FC2 follows at once; the next layer's q/k/v after the out-projection's
+            // share has landed, so every wait below is an exact count
             dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + L::kOffC);
-            if (l + 1 < a.n_layer) {
-                dma_rows<O::PQ>(a.qkv_w.at(l + 1), RD, q0, nq, s_w);
-                wait_vm<vm_cap(O::P1 + O::P2 + O::PQ)>();  // out-proj share in LDS
-            } else {
-                wait_vm<O::P1 + O::P2>();
-            }
+            wait_vm<O::P1 + O::P2>();  // out-proj share in LDS
+            if (l + 1 < a.n_layer) dma_rows<O::PQ>(a.qkv_w.at(l + 1), RD, q0, nq, s_w);
         } else {
             wait_vm<O::P1>();  // out-proj share in LDS
             if constexpr (L::kThree) dma_rows<O::P2>(a.fc2_w.at(l), RF, d0, nd, s_w + L::kOffC);
